@@ -1,0 +1,105 @@
+/* Plain CPU oracle for greedy self-speculative decoding (Draft & Verify,
+ * Zhang et al., arXiv 2309.08168).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library includes,
+ * links or calls this code; only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark use it.  It shares no code, header,
+ * table or helper with the GPU path.
+ *
+ * Arithmetic is float64 throughout.  Weights are read as stored (float32,
+ * or bfloat16 bit patterns expanded exactly) and the KV cache holds float64.
+ * Every output element is a sequential reduction over its inputs in index
+ * order, so a row's result does not depend on how many rows share the call
+ * or on the thread count.  Argmax and the top-1 probability are decided on
+ * logits rounded to float32, the precision the GPU path takes those
+ * decisions in.
+ *
+ * Model (pre-norm LLaMA decoder, the models the paper evaluates, Sec. 4.1):
+ *   h = E[x];  per layer l: attention sublayer unless skip[2l], MLP sublayer
+ *   unless skip[2l+1];  logits = W_lm * RMSNorm(h).
+ * A skipped sublayer is the identity on the residual stream (Sec. 3.2: the
+ * draft model bypasses intermediate layers); it computes nothing and writes
+ * no KV.
+ */
+#ifndef SD_ORACLE_H
+#define SD_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+    double rms_eps, rope_base;
+    int32_t wdtype; /* 0: float32 weights, 1: bfloat16 bit patterns (uint16) */
+} orc_config;
+
+/* Host pointers, row-major [out, in].  w_qkv = [(H + 2 KVH) dh, d] with q
+ * rows, then k rows, then v rows; w_gate_up = [2F, d], gate rows then up
+ * rows.  Per-layer members point to arrays of n_layers pointers, copied at
+ * create time; the tensors themselves are borrowed and must outlive the
+ * model. */
+typedef struct {
+    const void *tok_emb, *final_norm, *lm_head;
+    const void *const *attn_norm, *const *w_qkv, *const *w_o;
+    const void *const *mlp_norm, *const *w_gate_up, *const *w_down;
+} orc_weights;
+
+typedef struct orc_model orc_model;
+typedef struct orc_cache orc_cache;
+
+typedef struct {
+    int64_t n_stages;      /* drafting/verification stages */
+    int64_t n_drafted;     /* sum over stages of drafted tokens k_e */
+    int64_t n_accepted;    /* sum over stages of accepted drafts n_e */
+    int64_t n_emitted;     /* tokens emitted (= max_new) */
+    int64_t n_draft_steps; /* draft forwards run (= n_drafted) */
+    double min_gamma_gap;  /* min over draft steps of |p_max - gamma| */
+} orc_sd_stats;
+
+/* Errors: 0 ok, -1 invalid argument, -2 KV capacity exceeded, -3 out of memory. */
+
+orc_model *orc_create(const orc_config *cfg, const orc_weights *w);
+void orc_destroy(orc_model *m);
+int32_t orc_num_threads(void);
+
+orc_cache *orc_cache_create(const orc_model *m, int32_t capacity);
+void orc_cache_destroy(orc_cache *c);
+int32_t orc_cache_length(const orc_cache *c);
+int orc_cache_truncate(orc_cache *c, int32_t len);
+/* Load externally generated K/V for positions [0, len): kv is laid out
+ * [n_layers][2 (K, V)][n_kv_heads][len][head_dim] in kv_dtype (0 float32,
+ * 1 bfloat16 bits); sets the cache length to len. */
+int orc_cache_load(orc_cache *c, const void *kv, int32_t len, int32_t kv_dtype);
+
+/* One forward of n rows at positions [len, len + n) of the cache; writes
+ * K/V of every non-skipped attention sublayer and sets len += n.  skip is
+ * uint8[2 * n_layers] or NULL (full model).  Outputs are optional:
+ * logits float64 [n][vocab]; argmax int32 [n] (lowest id among equal float32
+ * logits); pmax float32 [n] = 1 / sum_v exp(l_v - l_max) over float32
+ * logits; margin float64 [n] = top-1 minus top-2 float64 logit. */
+int orc_forward(orc_model *m, orc_cache *c, const int32_t *tokens, int32_t n, const uint8_t *skip,
+                double *logits, int32_t *argmax, float *pmax, double *margin);
+
+/* Greedy autoregressive decoding (Alg. 1).  out int32 [max_new]; margin
+ * float64 [max_new] optional: top-2 margin of the logits each token came
+ * from. */
+int orc_generate_ar(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                    int32_t *out, double *margin);
+
+/* Greedy self-speculative decoding (Alg. 2 with the static-threshold draft
+ * exit of Sec. 3.4).  stage_log int32 [max_new][2] optional: (k_e, n_e) per
+ * stage; draft_pmax float32 [max_new * K_max] optional: p_max of every
+ * draft step in order; margin as for orc_generate_ar (from the
+ * verification forward). */
+int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                    const uint8_t *skip, int32_t k_max, float gamma, int32_t *out, double *margin,
+                    orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

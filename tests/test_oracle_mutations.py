@@ -1,0 +1,92 @@
+"""The oracle's pins are strong enough to catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle source, builds it on the
+CPU, and checks that the pins used in test_oracle.py (the library-built
+float64 model, losslessness, full acceptance with an empty skip set, the
+stage closed forms) reject it.  The real oracle is never modified.
+"""
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import sd_synth as S
+from tests import torch_ref
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "sd_oracle.c")
+
+MUTATIONS = {
+    "rope_sign": ("v[i + half] = b * cs + a * sn;", "v[i + half] = b * cs - a * sn;"),
+    "rope_pairing": ("double a = v[i], b = v[i + half];", "double a = v[2 * i], b = v[2 * i + 1];"),
+    "gqa_head_map": ("int g = j / grp;", "int g = j % cf->n_kv_heads;"),
+    "score_scale": ("double scale = 1.0 / sqrt((double)dh);", "double scale = 1.0 / (double)dh;"),
+    "block_not_causal": ("attend(c, l, qkv + (int64_t)r * nqkv, start + r,",
+                         "attend(c, l, qkv + (int64_t)r * nqkv, start + n - 1,"),
+    "attn_residual": ("linear(m, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] += t[i];",
+                      "linear(m, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] = t[i];"),
+    "gate_up_swap": ("mm[(int64_t)r * F + f] = silu(gr[f]) * gr[F + f];", "mm[(int64_t)r * F + f] = silu(gr[F + f]) * gr[f];"),
+    "silu_sign": ("return a / (1.0 + exp(-a));", "return a / (1.0 + exp(a));"),
+    "norm_mean": ("double inv = 1.0 / sqrt(ss / (double)d + m->c.rms_eps);", "double inv = 1.0 / sqrt(ss + m->c.rms_eps);"),
+    "accept_index": ("while (na < k && draft[na] == y[na])", "while (na < k && draft[na] == y[na + 1])"),
+    "rollback_len": ("rc = orc_cache_truncate(c, lc + na + 1);", "rc = orc_cache_truncate(c, lc + na);"),
+    "exit_after_token": ("if (p < gamma)\n                break;", "if (p >= gamma)\n                break;"),
+    "kcap": ("if (kcap > max_new - emitted - 1)\n            kcap = max_new - emitted - 1;",
+             "if (kcap > max_new - emitted - 2)\n            kcap = max_new - emitted - 2 > 0 ? max_new - emitted - 2 : 0;"),
+    "draft_input": ("int32_t in = j == 0 ? last : draft[j - 1];", "int32_t in = last;"),
+}
+
+
+def _pins_hold(lib_path) -> bool:
+    """True when every pin passes for the oracle built at lib_path."""
+    try:
+        cfg = S.micro_config()
+        w = S.make_weights(cfg, 0)
+        m = oracle.Model(cfg, w, lib_path=lib_path)
+        toks = S.prompt(cfg, 19, seed=3)
+        got = m.score(toks)["logits"]
+        ref = torch_ref.forward(cfg, S.weights_as_f64(cfg, w), toks)
+        if not np.max(np.abs(got - ref)) <= 1e-10 * np.max(np.abs(ref)):  # NaN fails too
+            return False
+        tiny = S.MODELS["tiny"]
+        mt = oracle.Model(tiny, S.make_weights(tiny, 0), lib_path=lib_path)
+        pr = S.prompt(tiny, 16)
+        ar, _ = mt.generate_ar(pr, 32)
+        for mask, k, g in (("tiny", 4, 0.6), ("random3", 6, 0.0), ("none", 4, 0.0), ("tiny", 3, 0.0028)):
+            sd = mt.generate_sd(pr, 32, S.skip_mask(tiny, mask, seed=11), k, g)
+            if not np.array_equal(sd["tokens"], ar):
+                return False
+            st = sd["stages"]
+            if int(np.sum(st[:, 1] + 1)) != 32 or np.any(st[:, 0] > k):
+                return False
+            if mask == "none" and g <= 0:
+                if not np.array_equal(st[:, 0], st[:, 1]) or sd["n_stages"] != -(-32 // (k + 1)):
+                    return False
+            if g > 0:
+                # drafts before the last of a stage were confident
+                pm, i, emitted = sd["draft_pmax"], 0, 0
+                for kk, nn in st:
+                    if kk and (np.any(pm[i:i + kk - 1] < np.float32(g)) or
+                               not (kk == min(k, 32 - emitted - 1) or pm[i + kk - 1] < np.float32(g))):
+                        return False
+                    i += kk
+                    emitted += nn + 1
+        return True
+    except oracle.OracleError:
+        return False
+
+
+def test_unmodified_oracle_passes(tmp_path):
+    assert _pins_hold(oracle.LIB_PATH)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name, tmp_path):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    mutated = tmp_path / "sd_oracle.c"
+    mutated.write_text(src.replace(old, new))
+    lib = oracle.build(src=str(mutated), out=str(tmp_path / f"liboracle_{name}.so"))
+    assert not _pins_hold(lib), f"planted mistake {name} passed every pin"
