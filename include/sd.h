@@ -1,0 +1,163 @@
+/* sd.h - C ABI of the MI355X self-speculative decoding library.
+ *
+ * Greedy self-speculative decoding (Draft & Verify, Zhang et al., arXiv
+ * 2309.08168) of a LLaMA-style decoder at batch size 1 on one GPU:
+ *   - draft: the model with a chosen set of attention / MLP sublayers
+ *     bypassed decodes tokens one at a time, until K_max tokens are drafted
+ *     or right after a token whose top-1 probability is below gamma
+ *     (Sec. 3.2 Algorithm 2, Sec. 3.4);
+ *   - verify: the full model scores the last committed token and all drafts
+ *     in one forward; the longest matching prefix is kept and the model's
+ *     own next token follows it (Algorithm 2).  The emitted tokens equal
+ *     greedy autoregressive decoding (Algorithm 1).
+ *
+ * Conventions for every function:
+ *   - returns SD_OK (0) or a negative sd_status; on failure nothing was
+ *     enqueued unless the status is SD_ERR_DEVICE, and sd_last_error()
+ *     returns a message for the calling thread;
+ *   - no C++ exception crosses this boundary;
+ *   - "device" pointers are HIP device allocations on the current device;
+ *     "host" pointers are ordinary CPU memory;
+ *   - a model and its caches are used by one host thread at a time; all
+ *     GPU work runs on the stream given to sd_model_create, in order.
+ */
+#ifndef SD_H
+#define SD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SD_OK = 0,
+    SD_ERR_INVALID_ARG = -1, /* a null pointer, a size out of range, a token id outside [0, vocab) */
+    SD_ERR_CAPACITY = -2,    /* the KV cache cannot hold the requested positions */
+    SD_ERR_OOM = -3,         /* a device or host allocation failed */
+    SD_ERR_DEVICE = -4,      /* a HIP call or a kernel failed; the stream may hold partial results */
+    SD_ERR_UNIMPLEMENTED = -5
+} sd_status;
+
+typedef enum { SD_F32 = 0, SD_BF16 = 1 } sd_dtype;
+
+/* Model shape (the LLaMA-2 family the paper evaluates, Sec. 4.1).
+ * head_dim must be even; n_heads a multiple of n_kv_heads (grouped-query
+ * attention when they differ).  dtype is the storage type of every weight
+ * and of the KV cache; activations and accumulations are float32. */
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+    float rms_eps;   /* RMSNorm epsilon */
+    float rope_base; /* rotary base; rotate-half pairing (i, i + head_dim/2) */
+    sd_dtype dtype;
+} sd_config;
+
+/* Weights: DEVICE pointers in dtype, row-major [out, in] like nn.Linear.
+ * Borrowed, never copied or freed ("no extra memory": the draft model is
+ * the same weights with sublayers bypassed, Sec. 3.2); they must outlive
+ * the model.  The per-layer members are HOST arrays of n_layers device
+ * pointers, copied at create time.
+ *   tok_emb   [vocab, d]            final_norm [d]     lm_head [vocab, d]
+ *   attn_norm [d]                   mlp_norm   [d]
+ *   w_qkv     [(n_heads + 2 n_kv_heads) head_dim, d]: q rows, k rows, v rows
+ *   w_o       [d, n_heads head_dim]
+ *   w_gate_up [2 ffn, d]: ffn gate rows, then ffn up rows
+ *   w_down    [d, ffn]
+ * Every device pointer must be 16-byte aligned. */
+typedef struct {
+    const void *tok_emb, *final_norm, *lm_head;
+    const void *const *attn_norm, *const *w_qkv, *const *w_o;
+    const void *const *mlp_norm, *const *w_gate_up, *const *w_down;
+} sd_weights;
+
+typedef struct sd_model sd_model;
+typedef struct sd_kv_cache sd_kv_cache;
+
+/* Statistics of one generate call.  stage_log, when not NULL, is a HOST
+ * array of stage_log_cap (k_e, n_e) pairs: drafts and accepted drafts of
+ * each stage in order (entries past stage_log_cap are dropped). */
+typedef struct {
+    int64_t n_stages;      /* draft/verify stages (0 for autoregressive) */
+    int64_t n_drafted;     /* sum of k_e */
+    int64_t n_accepted;    /* sum of n_e; acceptance rate = n_accepted / n_drafted */
+    int64_t n_emitted;     /* tokens written to out_tokens */
+    int64_t n_draft_steps; /* draft forwards run */
+    double prefill_ms;     /* prompt forward, GPU time */
+    double draft_ms;       /* all draft forwards, GPU time */
+    double verify_ms;      /* all verification forwards (with acceptance), GPU time */
+    double decode_ms;      /* GPU time from the end of prefill to the last token */
+    double total_ms;       /* GPU time of the whole call */
+    int32_t *stage_log;
+    int32_t stage_log_cap;
+} sd_stats;
+
+/* Creates a model over borrowed device weights.  hip_stream is a
+ * hipStream_t (NULL = the default stream).  Validates the shape and
+ * allocates the library's device workspace (activations of up to 16 rows,
+ * rotary table, reduction scratch).  Errors: INVALID_ARG, OOM, DEVICE. */
+sd_status sd_model_create(const sd_config *config, const sd_weights *weights, void *hip_stream, sd_model **out);
+sd_status sd_model_destroy(sd_model *model);
+
+/* Bytes of a KV cache for capacity positions:
+ * n_layers * 2 * n_kv_heads * capacity * head_dim * sizeof(dtype). */
+size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity);
+
+/* Creates a KV cache of capacity positions, length 0.  device_buf, when
+ * not NULL, is a caller-owned device buffer of sd_kv_cache_bytes() bytes
+ * (borrowed), laid out [n_layers][2 (K, V)][n_kv_heads][capacity][head_dim]
+ * in the model dtype, with rotary position embedding already applied to K;
+ * otherwise the library allocates it.  Errors: INVALID_ARG, OOM. */
+sd_status sd_kv_cache_create(sd_model *model, int32_t capacity, void *device_buf, sd_kv_cache **out);
+sd_status sd_kv_cache_destroy(sd_kv_cache *cache);
+int32_t sd_kv_cache_length(const sd_kv_cache *cache); /* -1 for NULL */
+/* Rolls the cache back to len positions (0 <= len <= length). */
+sd_status sd_kv_cache_truncate(sd_kv_cache *cache, int32_t len);
+/* Declares positions [0, len) valid, for caches the caller filled itself
+ * (0 <= len <= capacity). */
+sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len);
+
+/* One forward of n tokens (HOST int32 [n], each in [0, vocab)) at positions
+ * [len, len + n) of cache; writes K/V of every attention sublayer that
+ * skip_mask keeps and sets len += n.  skip_mask is a HOST uint8
+ * [2 n_layers] (entry 2l: attention of layer l, 2l+1: its MLP; 1 = bypass,
+ * i.e. the identity on the residual stream) or NULL for the full model.
+ * logits, when not NULL, is a DEVICE float32 [n, vocab].  Rows run in
+ * chunks of at most 16.  Errors: INVALID_ARG, CAPACITY (nothing enqueued),
+ * DEVICE. */
+sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
+                     sd_kv_cache *cache, float *logits);
+
+/* Greedy self-speculative decoding (Algorithm 2, static gamma exit of
+ * Sec. 3.4) of max_new tokens after a HOST prompt of prompt_len >= 1 ids.
+ * The prompt minus its last token is prefilled; every stage drafts at
+ * most min(K_max, tokens still to emit - 1) tokens with skip_mask (HOST,
+ * as in sd_forward), stopping right after a token whose top-1 probability
+ * is below gamma (that token is still verified), then verifies them in one
+ * forward of the full model and keeps the longest matching prefix plus the
+ * model's next token.  The draft shares the KV cache: it reads the
+ * committed positions and writes its own positions in the attention
+ * sublayers it runs; verification overwrites them.  0 <= K_max <= 15.
+ * out_tokens: HOST int32 [max_new].  stats may be NULL.  The host waits
+ * for each draft step's exit decision through a pinned mailbox; no other
+ * synchronisation happens per token.  Errors: INVALID_ARG, OOM, DEVICE. */
+sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                const uint8_t *skip_mask, int32_t K_max, float gamma, int32_t *out_tokens,
+                                sd_stats *stats);
+
+/* Greedy autoregressive decoding (Algorithm 1) with the same prefill
+ * convention; one full-model forward per token, no per-token host sync. */
+sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                     int32_t *out_tokens, sd_stats *stats);
+
+/* Message of the last non-OK status returned to this thread ("" if none). */
+const char *sd_last_error(void);
+
+/* Library version string. */
+const char *sd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -1,0 +1,251 @@
+"""ctypes binding of libsd.so (include/sd.h): argument marshalling only.
+
+Every computation of the decoding path runs in the library's HIP kernels.
+PyTorch provides device memory (weight and KV buffers) and the stream.
+If the library is not built, loading fails loudly; nothing falls back to
+another implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsd.so")
+
+SD_OK, SD_ERR_INVALID_ARG, SD_ERR_CAPACITY, SD_ERR_OOM, SD_ERR_DEVICE, SD_ERR_UNIMPLEMENTED = 0, -1, -2, -3, -4, -5
+SD_F32, SD_BF16 = 0, 1
+
+# Every entry point declared in include/sd.h.
+EXPORTS = (
+    "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
+    "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
+    "sd_self_spec_generate", "sd_autoregressive_generate", "sd_last_error", "sd_version",
+)
+
+
+class SDError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+class sd_config(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+        ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class sd_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("tok_emb", "final_norm", "lm_head")] + [
+        (n, ctypes.POINTER(ctypes.c_void_p))
+        for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+    ]
+
+
+class sd_stats(ctypes.Structure):
+    _fields_ = [
+        ("n_stages", ctypes.c_int64), ("n_drafted", ctypes.c_int64), ("n_accepted", ctypes.c_int64),
+        ("n_emitted", ctypes.c_int64), ("n_draft_steps", ctypes.c_int64),
+        ("prefill_ms", ctypes.c_double), ("draft_ms", ctypes.c_double), ("verify_ms", ctypes.c_double),
+        ("decode_ms", ctypes.c_double), ("total_ms", ctypes.c_double),
+        ("stage_log", ctypes.POINTER(ctypes.c_int32)), ("stage_log_cap", ctypes.c_int32),
+    ]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsd.so and declare every entry point's signature."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run `python -m paper_2309_08168_amd.build` first")
+    lib = ctypes.CDLL(path)
+    vp, i32, p = ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER
+    sig = {
+        "sd_model_create": ([p(sd_config), p(sd_weights), vp, p(vp)], ctypes.c_int),
+        "sd_model_destroy": ([vp], ctypes.c_int),
+        "sd_kv_cache_bytes": ([p(sd_config), i32], ctypes.c_size_t),
+        "sd_kv_cache_create": ([vp, i32, vp, p(vp)], ctypes.c_int),
+        "sd_kv_cache_destroy": ([vp], ctypes.c_int),
+        "sd_kv_cache_length": ([vp], i32),
+        "sd_kv_cache_truncate": ([vp, i32], ctypes.c_int),
+        "sd_kv_cache_set_length": ([vp, i32], ctypes.c_int),
+        "sd_forward": ([vp, vp, i32, vp, vp, vp], ctypes.c_int),
+        "sd_self_spec_generate": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_stats)], ctypes.c_int),
+        "sd_autoregressive_generate": ([vp, vp, i32, i32, vp, p(sd_stats)], ctypes.c_int),
+        "sd_last_error": ([], ctypes.c_char_p),
+        "sd_version": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def check(status: int):
+    if status != SD_OK:
+        raise SDError(status, load().sd_last_error().decode(errors="replace"))
+
+
+def make_config(cfg) -> sd_config:
+    """sd_config from a shape object with the fields of sd_synth.ModelConfig."""
+    return sd_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab,
+                     cfg.rms_eps, cfg.rope_base, SD_BF16 if cfg.dtype == "bf16" else SD_F32)
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+class DeviceWeights:
+    """Weight tensors in device memory (torch allocations), keyed like sd_synth."""
+
+    def __init__(self, cfg, host: Dict[str, np.ndarray], device="cuda"):
+        import torch
+
+        self.cfg = cfg
+        self.tensors = {}
+        for name, arr in host.items():
+            a = np.ascontiguousarray(arr)
+            t = torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a)
+            self.tensors[name] = t.to(device, non_blocking=False)
+
+    @classmethod
+    def from_generator(cls, cfg, make, names, device="cuda"):
+        """Upload tensors one by one from make(name) -> np.ndarray (host copies dropped)."""
+        import torch
+
+        self = cls.__new__(cls)
+        self.cfg = cfg
+        self.tensors = {}
+        for name in names:
+            a = np.ascontiguousarray(make(name))
+            t = torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a)
+            self.tensors[name] = t.to(device)
+            del a, t
+        return self
+
+    def ptr(self, name: str) -> int:
+        return self.tensors[name].data_ptr()
+
+
+class Model:
+    """An sd_model over DeviceWeights on a torch stream (default: current stream)."""
+
+    def __init__(self, cfg, weights: DeviceWeights, stream=None):
+        import torch
+
+        lib = load()
+        self.cfg = cfg
+        self.weights = weights
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        L = cfg.n_layers
+        self._arrays = {
+            key: (ctypes.c_void_p * L)(*[weights.ptr(f"layers.{l}.{key}") for l in range(L)])
+            for key in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")
+        }
+        w = sd_weights(weights.ptr("tok_emb"), weights.ptr("final_norm"), weights.ptr("lm_head"),
+                       *[ctypes.cast(self._arrays[k], ctypes.POINTER(ctypes.c_void_p))
+                         for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+        self._cfg = make_config(cfg)
+        h = ctypes.c_void_p()
+        check(lib.sd_model_create(ctypes.byref(self._cfg), ctypes.byref(w), ctypes.c_void_p(self.stream.cuda_stream),
+                                  ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().sd_model_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def kv_cache_bytes(self, capacity: int) -> int:
+        return int(load().sd_kv_cache_bytes(ctypes.byref(self._cfg), capacity))
+
+    def cache(self, capacity: int, device_buf=None) -> "KVCache":
+        return KVCache(self, capacity, device_buf)
+
+    def forward(self, tokens, cache: "KVCache", skip=None, logits=None):
+        """sd_forward; logits is an optional torch float32 cuda tensor [n, vocab]."""
+        tok = np.ascontiguousarray(tokens, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        lp = None if logits is None else ctypes.c_void_p(logits.data_ptr())
+        check(load().sd_forward(self._h, _ptr(tok), tok.size, _ptr(sk), cache._h, lp))
+        return logits
+
+    def generate_sd(self, prompt, max_new: int, skip, k_max: int, gamma: float, log_cap: Optional[int] = None):
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        out = np.zeros(max(max_new, 1), np.int32)
+        cap = max(max_new, 1) if log_cap is None else log_cap
+        log = np.zeros((cap, 2), np.int32)
+        st = sd_stats()
+        st.stage_log = log.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        st.stage_log_cap = cap
+        check(load().sd_self_spec_generate(self._h, _ptr(pr), pr.size, max_new, _ptr(sk), k_max,
+                                           ctypes.c_float(gamma), _ptr(out), ctypes.byref(st)))
+        return out[:max_new], _stats(st, log)
+
+    def generate_ar(self, prompt, max_new: int):
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.zeros(max(max_new, 1), np.int32)
+        st = sd_stats()
+        check(load().sd_autoregressive_generate(self._h, _ptr(pr), pr.size, max_new, _ptr(out), ctypes.byref(st)))
+        return out[:max_new], _stats(st, None)
+
+
+def _stats(st: sd_stats, log) -> dict:
+    d = {k: getattr(st, k) for k, _ in sd_stats._fields_ if k not in ("stage_log", "stage_log_cap")}
+    if log is not None:
+        d["stages"] = log[: min(st.n_stages, log.shape[0])].copy()
+    return d
+
+
+class KVCache:
+    def __init__(self, model: Model, capacity: int, device_buf=None):
+        self.model = model
+        self.capacity = capacity
+        self._buf = device_buf  # keep the caller's buffer alive
+        h = ctypes.c_void_p()
+        check(load().sd_kv_cache_create(model._h, capacity,
+                                        None if device_buf is None else ctypes.c_void_p(device_buf.data_ptr()),
+                                        ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().sd_kv_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def length(self) -> int:
+        return int(load().sd_kv_cache_length(self._h))
+
+    def truncate(self, n: int):
+        check(load().sd_kv_cache_truncate(self._h, n))
+
+    def set_length(self, n: int):
+        check(load().sd_kv_cache_set_length(self._h, n))

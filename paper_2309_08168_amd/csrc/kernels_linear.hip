@@ -1,0 +1,753 @@
+// Weight-streaming linear layers of the decoder forward, with their fused
+// prologue (RMSNorm) and epilogues (rotary embedding + KV append, SwiGLU,
+// residual add, greedy head with the draft-exit test and acceptance).
+//
+// Every step of greedy decoding at batch 1 streams the whole weight set
+// once (Sec. 3.1: model size over memory bandwidth bounds the decode
+// speed), so the three main loops below are built to read each weight byte
+// exactly once with 16-byte loads:
+//   - k_linear_valu, MR == 1: the GEMV of a draft or autoregressive step;
+//   - k_linear_valu, MR == 16: any row count, for float32 weights;
+//   - k_linear_mfma: the verification forward over up to 16 rows (the last
+//     committed token plus the drafts, Algorithm 2), bf16 MFMA tiles with
+//     the rows padded to 16.
+//
+// RMSNorm is folded in: y = W (g * h) / rms(h), so the kernel that reads h
+// as its input also accumulates sum(h^2) and scales its outputs at the end;
+// no separate normalisation pass.
+#include "sd_internal.h"
+
+namespace sdk {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8_t __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// float32 -> bfloat16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ void unpack8(u32x4_t v, float (&w)[8]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        w[2 * j] = __uint_as_float(v[j] << 16);
+        w[2 * j + 1] = __uint_as_float(v[j] & 0xffff0000u);
+    }
+}
+
+// Weights are read once per step: non-temporal loads keep them from
+// displacing the activations and KV in the caches.
+__device__ __forceinline__ void ldw8(const uint16_t *p, float (&w)[8]) {
+    unpack8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p)), w);
+}
+__device__ __forceinline__ void ldw8(const float *p, float (&w)[8]) {
+    f32x4_t a = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p));
+    f32x4_t b = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p) + 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        w[j] = a[j];
+        w[4 + j] = b[j];
+    }
+}
+__device__ __forceinline__ void ldg8(const uint16_t *p, float (&w)[8]) {
+    unpack8(*reinterpret_cast<const u32x4_t *>(p), w);
+}
+__device__ __forceinline__ void ldg8(const float *p, float (&w)[8]) {
+    f32x4_t a = reinterpret_cast<const f32x4_t *>(p)[0];
+    f32x4_t b = reinterpret_cast<const f32x4_t *>(p)[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        w[j] = a[j];
+        w[4 + j] = b[j];
+    }
+}
+
+__device__ __forceinline__ void store_kv(float *p, float v) { *p = v; }
+__device__ __forceinline__ void store_kv(uint16_t *p, float v) { *p = f2bf(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// Which weight rows a tile of R rows covers.
+//   QKV: R/2 rotary pairs (i, i + head_dim/2) of one head, so the epilogue
+//        can rotate q and k in place;
+//   SWIGLU: R/2 gate rows and the R/2 matching up rows;
+//   otherwise R consecutive rows.
+
+template <int EPI>
+__device__ __forceinline__ int tile_row(int t, int i, int R, const EpiArgs &e) {
+    if constexpr (EPI == EPI_QKV) {
+        const int P = R >> 1, half = e.head_dim >> 1, per_head = half / P;
+        const int head = t / per_head, p0 = (t - head * per_head) * P;
+        return head * e.head_dim + (i < P ? p0 + i : half + p0 + (i - P));
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        const int P = R >> 1;
+        return i < P ? t * P + i : e.ffn + t * P + (i - P);
+    } else {
+        return t * R + i;
+    }
+}
+
+template <int EPI>
+__device__ __forceinline__ bool row_valid(int t, int i, int R, int N, const EpiArgs &e) {
+    if constexpr (EPI == EPI_QKV) {
+        return true;
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        const int P = R >> 1;
+        return t * P + (i < P ? i : i - P) < e.ffn;
+    } else {
+        return t * R + i < N;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Greedy head: argmax and top-1 probability across all tiles.
+
+struct HeadPart {
+    float mx;
+    int idx;
+    float sum;  // sum over the part of exp(l - mx)
+};
+
+__device__ __forceinline__ HeadPart head_empty() { return HeadPart{-INFINITY, 0x7fffffff, 0.0f}; }
+
+__device__ __forceinline__ HeadPart head_comb(HeadPart a, HeadPart b) {
+    if (b.sum == 0.0f)
+        return a;
+    if (a.sum == 0.0f)
+        return b;
+    const float mx = fmaxf(a.mx, b.mx);
+    HeadPart r;
+    r.mx = mx;
+    r.idx = (b.mx > a.mx || (b.mx == a.mx && b.idx < a.idx)) ? b.idx : a.idx;
+    r.sum = a.sum * expf(a.mx - mx) + b.sum * expf(b.mx - mx);
+    return r;
+}
+
+__device__ void post_mailbox(DevState *st, Mailbox *mb) {
+    st->seq += 1;
+    __hip_atomic_store(&mb->phase, st->phase, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->gen_done, st->gen_done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->emitted, st->emitted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->seq, st->seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// The decoding decision after one step, taken by one thread once the
+// argmax y[r] and top-1 probability p[r] of every row are known.
+//   AR:     Algorithm 1, append y and feed it back.
+//   DRAFT:  Algorithm 2 drafting with the exit of Sec. 3.4: keep d_j, stop
+//           after it when p_j < gamma or the stage budget is reached; the
+//           next step is then the verification of [last, d_1..d_k].
+//   VERIFY: Algorithm 2 verification: the longest prefix of drafts equal
+//           to the model's own tokens is accepted, followed by the model's
+//           token at the first mismatch (or the bonus token); the committed
+//           length advances past them, which rolls back the KV positions of
+//           rejected drafts.
+__device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, const float *p) {
+    DevState *st = h.st;
+    if (h.mode == HEAD_AR) {
+        const int tok = y[0];
+        h.out_tokens[st->emitted] = tok;
+        st->emitted += 1;
+        st->lc += 1;
+        st->last = tok;
+        ctl->pos += 1;
+        ctl->tokens[0] = tok;
+    } else if (h.mode == HEAD_DRAFT) {
+        const int j = st->k;
+        st->drafts[j] = y[0];
+        st->dpmax[j] = p[0];
+        st->k = j + 1;
+        st->n_draft_steps += 1;
+        const bool exit_now = (p[0] < st->gamma) || (j + 1 >= st->kcap);
+        if (!exit_now) {
+            ctl->pos = st->lc + j + 1;
+            ctl->m = 1;
+            ctl->tokens[0] = y[0];
+        } else {
+            st->phase = PHASE_VERIFY;
+            ctl->pos = st->lc;
+            ctl->m = j + 2;
+            ctl->tokens[0] = st->last;
+            for (int i = 0; i <= j; ++i)
+                ctl->tokens[i + 1] = st->drafts[i];
+        }
+        post_mailbox(st, h.mb);
+    } else if (h.mode == HEAD_VERIFY) {
+        const int k = st->k;
+        int n = 0;
+        while (n < k && st->drafts[n] == y[n])
+            ++n;
+        int e = st->emitted;
+        for (int i = 0; i < n; ++i)
+            h.out_tokens[e + i] = st->drafts[i];
+        h.out_tokens[e + n] = y[n];
+        e += n + 1;
+        st->emitted = e;
+        if (h.stage_log && st->n_stages < h.stage_log_cap) {
+            h.stage_log[2 * st->n_stages] = k;
+            h.stage_log[2 * st->n_stages + 1] = n;
+        }
+        st->n_stages += 1;
+        st->n_drafted += k;
+        st->n_accepted += n;
+        st->lc += n + 1;
+        st->last = y[n];
+        if (e >= st->max_new) {
+            st->gen_done = 1;
+        } else {
+            const int kcap = min(st->k_max, st->max_new - e - 1);
+            st->k = 0;
+            st->kcap = kcap;
+            st->phase = kcap > 0 ? PHASE_DRAFT : PHASE_VERIFY;
+        }
+        ctl->pos = st->lc;
+        ctl->m = 1;
+        ctl->tokens[0] = st->last;
+        post_mailbox(st, h.mb);
+    }
+}
+
+// Last work-group of the head: combine the per-tile partials of every row
+// in a fixed order (deterministic), then take the decoding decision.
+__device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
+    __shared__ HeadPart hred[256];
+    __shared__ int ys[MAX_ROWS];
+    __shared__ float ps[MAX_ROWS];
+    const int tid = threadIdx.x;
+    const int m = tid >> 4, j = tid & 15;
+    const HeadArgs &h = a.epi.head;
+    HeadPart acc = head_empty();
+    if (m < M) {
+        for (int t = j; t < n_tiles; t += 16) {
+            const float4 v = h.partials[(int64_t)t * MAX_ROWS + m];
+            acc = head_comb(acc, HeadPart{v.x, __float_as_int(v.y), v.z});
+        }
+    }
+    hred[tid] = acc;
+    __syncthreads();
+    if (tid < M) {
+        HeadPart r = hred[tid * 16];
+        for (int jj = 1; jj < 16; ++jj)
+            r = head_comb(r, hred[tid * 16 + jj]);
+        ys[tid] = r.idx;
+        ps[tid] = 1.0f / r.sum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        *h.counter = 0;
+        decode_decision(h, const_cast<DevCtl *>(a.ctl), ys, ps);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Epilogues.  fin[i * MR + m] holds the raw dot product of tile row i and
+// input row m; inv[m] the RMSNorm scale of row m (1 without a norm).
+
+template <typename TK, int EPI>
+__device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, int R, int MR, const float *inv, int t,
+                                             int M) {
+    const int tid = threadIdx.x;
+    const EpiArgs &e = a.epi;
+    if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+        for (int j = tid; j < R * M; j += 256) {
+            const int i = j % R, m = j / R, n = t * R + i;
+            if (n < a.N) {
+                const float v = fin[i * MR + m] * inv[m];
+                float *o = e.out + (int64_t)m * e.ld_out + n;
+                if constexpr (EPI == EPI_RESID)
+                    *o += v;
+                else
+                    *o = v;
+            }
+        }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        const int P = R >> 1;
+        for (int j = tid; j < P * M; j += 256) {
+            const int i = j % P, m = j / P, f = t * P + i;
+            if (f < e.ffn) {
+                const float g = fin[i * MR + m] * inv[m];
+                const float u = fin[(i + P) * MR + m] * inv[m];
+                e.out[(int64_t)m * e.ld_out + f] = g / (1.0f + expf(-g)) * u;
+            }
+        }
+    } else if constexpr (EPI == EPI_QKV) {
+        const int P = R >> 1, dh = e.head_dim, half = dh >> 1;
+        const int H = e.n_heads, KVH = e.n_kv_heads;
+        for (int j = tid; j < P * M; j += 256) {
+            const int i = j % P, m = j / P;
+            const int n0 = tile_row<EPI>(t, i, R, e);
+            const int head = n0 / dh, ei = n0 - head * dh;
+            float y0 = fin[i * MR + m] * inv[m];
+            float y1 = fin[(i + P) * MR + m] * inv[m];
+            const int pos = a.ctl->pos + m;
+            if (head < H + KVH) {
+                const float2 cs = e.rope[(int64_t)pos * half + ei];
+                const float r0 = y0 * cs.x - y1 * cs.y;
+                const float r1 = y1 * cs.x + y0 * cs.y;
+                y0 = r0;
+                y1 = r1;
+            }
+            if (head < H) {
+                float *q = e.q + (int64_t)m * e.ld_q + (int64_t)head * dh + ei;
+                q[0] = y0;
+                q[half] = y1;
+            } else {
+                const bool is_k = head < H + KVH;
+                const int g = is_k ? head - H : head - H - KVH;
+                TK *base = reinterpret_cast<TK *>(is_k ? e.kcache : e.vcache) + (int64_t)g * e.kv_head_stride +
+                           (int64_t)pos * dh + ei;
+                store_kv(base, y0);
+                store_kv(base + half, y1);
+            }
+        }
+    } else if constexpr (EPI == EPI_HEAD) {
+        const HeadArgs &h = e.head;
+        for (int j = tid; j < R * M; j += 256) {
+            const int i = j % R, m = j / R, n = t * R + i;
+            if (n < a.N) {
+                const float v = fin[i * MR + m] * inv[m];
+                fin[i * MR + m] = v;
+                if (h.logits)
+                    h.logits[(int64_t)m * h.ld_logits + n] = v;
+            }
+        }
+        __syncthreads();
+        if (tid < M) {
+            const int m = tid;
+            float mx = -INFINITY;
+            int ix = 0x7fffffff;
+            for (int i = 0; i < R && t * R + i < a.N; ++i) {
+                const float v = fin[i * MR + m];
+                if (v > mx) {
+                    mx = v;
+                    ix = t * R + i;
+                }
+            }
+            float s = 0.0f;
+            for (int i = 0; i < R && t * R + i < a.N; ++i)
+                s += expf(fin[i * MR + m] - mx);
+            h.partials[(int64_t)t * MAX_ROWS + m] = make_float4(mx, __int_as_float(ix), s, 0.0f);
+        }
+        __syncthreads();
+    }
+}
+
+// After the head epilogue of every tile of this work-group: the last
+// work-group of the grid to finish combines all tiles.
+__device__ void head_complete(const LinearArgs &a, int n_tiles, int M) {
+    __shared__ int is_last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0)
+        is_last = atomicAdd(a.epi.head.counter, 1) == (int)gridDim.x - 1;
+    __syncthreads();
+    if (!is_last)
+        return;
+    __threadfence();
+    head_finalize(a, n_tiles, M);
+}
+
+// ---------------------------------------------------------------------------
+// VALU main loop: one work-group per tile of R weight rows; the 256
+// threads stride over the reduction dimension in chunks of 8 elements
+// (one 16-byte load of bf16 weights per row), then reduce across the
+// work-group.  MR is the largest row count handled (1: the GEMV).
+
+template <typename TW, int MR, int R, int EPI, bool NORM>
+__global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
+    constexpr int NV = MR * R + (NORM ? MR : 0);
+    __shared__ float red[4][NV];
+    __shared__ float fin[R * MR];
+    __shared__ float inv_s[MR];
+    const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int M = MR == 1 ? 1 : a.ctl->m;
+    const int K = a.K, nch = K >> 3;
+    const TW *W = reinterpret_cast<const TW *>(a.W);
+    const TW *G = reinterpret_cast<const TW *>(a.gain);
+
+    int64_t roff[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        roff[i] = row_valid<EPI>(t, i, R, a.N, a.epi) ? (int64_t)tile_row<EPI>(t, i, R, a.epi) * K : 0;
+
+    float acc[MR][R];
+    float ss[MR];
+#pragma unroll
+    for (int r = 0; r < MR; ++r) {
+        ss[r] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            acc[r][i] = 0.0f;
+    }
+
+    for (int c = tid; c < nch; c += 256) {
+        float w[R][8];
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            ldw8(W + roff[i] + (int64_t)c * 8, w[i]);
+        float g[8];
+        if constexpr (NORM)
+            ldg8(G + c * 8, g);
+#pragma unroll
+        for (int r = 0; r < MR; ++r) {
+            if (r < M) {
+                float x[8];
+                ldg8(a.X + (int64_t)r * a.ldx + c * 8, x);
+                if constexpr (NORM) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        ss[r] = fmaf(x[k], x[k], ss[r]);
+                        x[k] *= g[k];
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < R; ++i)
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        acc[r][i] = fmaf(w[i][k], x[k], acc[r][i]);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int r = 0; r < MR; ++r) {
+        if (r < M) {
+#pragma unroll
+            for (int i = 0; i < R; ++i) {
+                const float v = wave_sum(acc[r][i]);
+                if (lane == 0)
+                    red[wave][r * R + i] = v;
+            }
+            if constexpr (NORM) {
+                const float v = wave_sum(ss[r]);
+                if (lane == 0)
+                    red[wave][MR * R + r] = v;
+            }
+        }
+    }
+    __syncthreads();
+    for (int j = tid; j < MR * R; j += 256) {
+        const int r = j / R, i = j - r * R;
+        if (r < M)
+            fin[i * MR + r] = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+    }
+    if (tid < MR) {
+        float v = 1.0f;
+        if constexpr (NORM) {
+            if (tid < M) {
+                const int j = MR * R + tid;
+                const float s = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+                v = 1.0f / sqrtf(s / (float)K + a.eps);
+            }
+        }
+        inv_s[tid] = v;
+    }
+    __syncthreads();
+    run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, M);
+    if constexpr (EPI == EPI_HEAD)
+        head_complete(a, gridDim.x, M);
+}
+
+// ---------------------------------------------------------------------------
+// MFMA main loop (bf16 weights, up to 16 rows).  Work-group (group t, split
+// s) owns TN tiles of 16 weight rows and a contiguous range of 128-element
+// k-steps; its four waves take every fourth k-step.  In a k-step, lane l
+// loads 64 contiguous bytes (32 bf16) of weight row l % 16 of each tile at
+// k offset 32 (l / 16), and the same 32 activations of input row l % 16;
+// those feed four 16x16x32 MFMAs per tile.  The k order inside an MFMA is a
+// permutation shared by both operands, so the dot products are unchanged.
+// Activations enter as a hi + lo pair of bf16 (hi = the top 16 bits, lo =
+// the rest rounded down to bf16, two MFMAs per k-block), which keeps about
+// 16 bits of their mantissa; the weights are exact in bf16.  The split of
+// one activation serves TN tiles.  With more than one split, each
+// work-group writes its partial tiles and the last one to finish adds them
+// in split order (deterministic) and runs the epilogue.
+
+__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
+    return (a >> 16) | (b & 0xffff0000u);
+}
+
+template <int EPI, bool NORM, int TN>
+__global__ __launch_bounds__(256) void k_linear_mfma(LinearArgs a) {
+    __shared__ float red[4][TN * 16][17];
+    __shared__ float red_ss[4][16];
+    __shared__ float fin[TN * 16 * 16];
+    __shared__ float inv_s[16];
+    __shared__ int is_last;
+    const int S = a.splits;
+    const int grp = blockIdx.x / S, s = blockIdx.x - grp * S;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int M = a.ctl->m;
+    const int n_tiles = a.n_tiles;  // 16-row tiles in the layer
+    const uint16_t *Wr[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int t = grp * TN + j;
+        const bool nv = t < n_tiles && row_valid<EPI>(t, r16, 16, a.N, a.epi);
+        const int n = nv ? tile_row<EPI>(t, r16, 16, a.epi) : 0;
+        Wr[j] = reinterpret_cast<const uint16_t *>(a.W) + (int64_t)n * a.K + kg * 32;
+    }
+    const float *Xr = a.X + (int64_t)r16 * a.ldx + kg * 32;
+    const uint16_t *Gp = reinterpret_cast<const uint16_t *>(a.gain) + kg * 32;
+    const bool xrow = r16 < M;
+    const int KS = a.K >> 7;
+    const int sb = (int)(((int64_t)KS * s) / S), se = (int)(((int64_t)KS * (s + 1)) / S);
+
+    floatx4_t acc[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+        acc[j] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    float ss = 0.0f;
+    for (int q = sb + wave; q < se; q += 4) {
+        const int k0 = q << 7;
+        u32x4_t wv[TN][4];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                wv[j][i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 8 * i));
+        float x[32];
+        if (xrow) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const f32x4_t v = reinterpret_cast<const f32x4_t *>(Xr + k0)[j];
+                x[4 * j] = v[0];
+                x[4 * j + 1] = v[1];
+                x[4 * j + 2] = v[2];
+                x[4 * j + 3] = v[3];
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 32; ++j)
+                x[j] = 0.0f;
+        }
+        if constexpr (NORM) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float g[8];
+                ldg8(Gp + k0 + 8 * j, g);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    ss = fmaf(x[8 * j + e], x[8 * j + e], ss);
+                    x[8 * j + e] *= g[e];
+                }
+            }
+        }
+        u32x4_t bhi[4], blo[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t u0 = __float_as_uint(x[8 * i + 2 * e]);
+                const uint32_t u1 = __float_as_uint(x[8 * i + 2 * e + 1]);
+                const float l0 = x[8 * i + 2 * e] - __uint_as_float(u0 & 0xffff0000u);
+                const float l1 = x[8 * i + 2 * e + 1] - __uint_as_float(u1 & 0xffff0000u);
+                bhi[i][e] = pack_hi(u0, u1);
+                blo[i][e] = pack_hi(__float_as_uint(l0), __float_as_uint(l1));
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bhi[i]);
+            const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, blo[i]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, wv[j][i]);
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bh, acc[j], 0, 0, 0);
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bl, acc[j], 0, 0, 0);
+            }
+        }
+    }
+
+    // D[n_local][m]: lane l holds rows 4 (l / 16) + v, column l % 16.
+    ss += __shfl_xor(ss, 16, 64);
+    ss += __shfl_xor(ss, 32, 64);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            red[wave][16 * j + 4 * kg + v][r16] = acc[j][v];
+    if (kg == 0)
+        red_ss[wave][r16] = ss;
+    __syncthreads();
+    const int mi = tid & 15;
+    float val[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int ni = 16 * j + (tid >> 4);
+        val[j] = (red[0][ni][mi] + red[1][ni][mi]) + (red[2][ni][mi] + red[3][ni][mi]);
+    }
+    float ssv = 0.0f;
+    if (NORM && tid < 16)
+        ssv = (red_ss[0][tid] + red_ss[1][tid]) + (red_ss[2][tid] + red_ss[3][tid]);
+    if (S > 1) {
+        constexpr int PS = TN * 256 + 16;
+        float *pp = a.part + ((int64_t)grp * S + s) * PS;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            pp[256 * j + tid] = val[j];
+        if (NORM && tid < 16)
+            pp[TN * 256 + tid] = ssv;
+        __threadfence();
+        __syncthreads();
+        if (tid == 0)
+            is_last = atomicAdd(&a.tile_counter[grp], 1) == S - 1;
+        __syncthreads();
+        if (!is_last)
+            return;
+        __threadfence();
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            val[j] = 0.0f;
+        ssv = 0.0f;
+        for (int sp = 0; sp < S; ++sp) {
+            const float *pj = a.part + ((int64_t)grp * S + sp) * PS;
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                val[j] += pj[256 * j + tid];
+            if (NORM && tid < 16)
+                ssv += pj[TN * 256 + tid];
+        }
+        if (tid == 0)
+            a.tile_counter[grp] = 0;
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+        fin[256 * j + (tid >> 4) * 16 + mi] = val[j];
+    if (tid < 16)
+        inv_s[tid] = NORM ? 1.0f / sqrtf(ssv / (float)a.K + a.eps) : 1.0f;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int t = grp * TN + j;
+        if (t < n_tiles)
+            run_epilogue<uint16_t, EPI>(a, fin + 256 * j, 16, 16, inv_s, t, M);
+    }
+    if constexpr (EPI == EPI_HEAD)
+        head_complete(a, n_tiles, M);
+}
+
+// ---------------------------------------------------------------------------
+// dispatch
+
+template <typename TW, int MR, int R>
+static hipError_t launch_valu(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
+    dim3 grid(n_tiles), block(256);
+    const bool norm = a.gain != nullptr;
+    switch (epi) {
+    case EPI_STORE:
+        if (norm)
+            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, true>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, false>), grid, block, 0, s, a);
+        break;
+    case EPI_RESID:
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_RESID, false>), grid, block, 0, s, a);
+        break;
+    case EPI_SWIGLU:
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_SWIGLU, true>), grid, block, 0, s, a);
+        break;
+    case EPI_QKV:
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_QKV, true>), grid, block, 0, s, a);
+        break;
+    case EPI_HEAD:
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_HEAD, true>), grid, block, 0, s, a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <typename TW, int MR>
+static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s) {
+    switch (R) {
+    case 4:
+        return launch_valu<TW, MR, 4>(a, epi, n_tiles, s);
+    case 8:
+        return launch_valu<TW, MR, 8>(a, epi, n_tiles, s);
+    case 16:
+        if constexpr (MR == 1)
+            return launch_valu<TW, MR, 16>(a, epi, n_tiles, s);
+        return hipErrorInvalidValue;
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+template <int TN>
+static hipError_t launch_mfma(const LinearArgs &a0, int epi, int n_tiles, hipStream_t s) {
+    LinearArgs a = a0;
+    a.n_tiles = n_tiles;
+    const int groups = (n_tiles + TN - 1) / TN;
+    dim3 grid(groups * a.splits), block(256);
+    const bool norm = a.gain != nullptr;
+    switch (epi) {
+    case EPI_STORE:
+        if (norm)
+            hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, true, TN>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, false, TN>), grid, block, 0, s, a);
+        break;
+    case EPI_RESID:
+        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, false, TN>), grid, block, 0, s, a);
+        break;
+    case EPI_SWIGLU:
+        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, true, TN>), grid, block, 0, s, a);
+        break;
+    case EPI_QKV:
+        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, true, TN>), grid, block, 0, s, a);
+        break;
+    case EPI_HEAD:
+        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, true, TN>), grid, block, 0, s, a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
+                         hipStream_t s) {
+    if (n_tiles <= 0)
+        return hipSuccess;
+    if (path == PATH_MFMA) {
+        // rows_per_tile = 16 * TN; n_tiles counts 16-row tiles.
+        const int TN = rows_per_tile / 16;
+        if (!bf16 || (a.K & 127) || (TN != 1 && TN != 2 && TN != 4) || rows_per_tile != 16 * TN)
+            return hipErrorInvalidValue;
+        if (epi == EPI_HEAD && a.splits != 1)
+            return hipErrorInvalidValue;
+        switch (TN) {
+        case 1:
+            return launch_mfma<1>(a, epi, n_tiles, s);
+        case 2:
+            return launch_mfma<2>(a, epi, n_tiles, s);
+        default:
+            return launch_mfma<4>(a, epi, n_tiles, s);
+        }
+    }
+    if (a.K & 7)
+        return hipErrorInvalidValue;
+    if (path == PATH_GEMV)
+        return bf16 ? launch_valu_r<uint16_t, 1>(a, epi, rows_per_tile, n_tiles, s)
+                    : launch_valu_r<float, 1>(a, epi, rows_per_tile, n_tiles, s);
+    return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s)
+                : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s);
+}
+
+}  // namespace sdk

@@ -1,0 +1,885 @@
+// Host orchestration behind the C ABI of include/sd.h: model and cache
+// objects, the decoder forward as a sequence of kernel launches, and the
+// two decoding loops (greedy autoregressive, Algorithm 1; greedy
+// self-speculative, Algorithm 2 with the static draft exit of Sec. 3.4).
+#include "sd.h"
+#include "sd_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#if defined(__x86_64__)
+#include <immintrin.h>
+#endif
+
+using namespace sdk;
+
+namespace {
+
+thread_local std::string g_err;
+
+sd_status fail(sd_status st, const std::string &msg) {
+    g_err = msg;
+    return st;
+}
+
+#define SD_HIP(expr)                                                                                   \
+    do {                                                                                               \
+        hipError_t e_ = (expr);                                                                        \
+        if (e_ != hipSuccess)                                                                          \
+            return fail(SD_ERR_DEVICE, std::string(#expr) + " failed: " + hipGetErrorString(e_));     \
+    } while (0)
+
+#define SD_TRY(expr)                                                                                   \
+    do {                                                                                               \
+        sd_status s_ = (expr);                                                                         \
+        if (s_ != SD_OK)                                                                               \
+            return s_;                                                                                 \
+    } while (0)
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4, LK_COUNT = 5 };
+
+// How one linear layer is launched for one row regime.
+struct Plan {
+    int path;     // PATH_GEMV, PATH_VALU16 or PATH_MFMA
+    int rows;     // weight rows per work-group
+    int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
+    int splits;   // MFMA split-K factor
+    int N, K, epi;
+};
+
+}  // namespace
+
+struct sd_kv_cache {
+    sd_model *model;
+    void *buf;
+    bool owns;
+    int32_t cap;
+    int32_t len;
+};
+
+struct sd_model {
+    sd_config cfg{};
+    bool bf16 = false;
+    size_t wsize = 4;
+    const void *tok_emb = nullptr, *final_norm = nullptr, *lm_head = nullptr;
+    std::vector<const void *> attn_norm, w_qkv, w_o, mlp_norm, w_gate_up, w_down;
+    hipStream_t stream = nullptr;
+
+    Plan plan1[LK_COUNT];  // one row (draft / autoregressive step)
+    Plan planm[LK_COUNT];  // up to 16 rows (verification, prefill)
+
+    float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
+    float *part = nullptr;
+    int32_t *tile_counter = nullptr;
+    float4 *head_part = nullptr;
+    int32_t *head_counter = nullptr;
+    float *attn_o = nullptr;
+    float2 *attn_ml = nullptr;
+    int attn_splits_cap = 0;
+    float2 *rope = nullptr;
+    int rope_cap = 0;
+    DevCtl *ctl = nullptr;
+    DevState *st = nullptr;
+    Mailbox *mb_host = nullptr;
+    Mailbox *mb_dev = nullptr;
+    int32_t *d_tokens = nullptr;
+    int d_tokens_cap = 0;
+    int32_t *d_out = nullptr;
+    int d_out_cap = 0;
+    int32_t *d_log = nullptr;  // (k_e, n_e) pairs
+    int d_log_cap = 0;         // int32 elements
+    sd_kv_cache *gen_cache = nullptr;
+    hipEvent_t ev[6] = {};
+};
+
+namespace {
+
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Tile rows for the QKV layer must hold whole rotary pairs of one head.
+int qkv_gemv_rows(int head_dim) {
+    const int half = head_dim / 2;
+    for (int r : {4, 8})
+        if (half % (r / 2) == 0)
+            return r;
+    return 4;
+}
+
+Plan make_plan(const sd_model *m, LinearKind kind, bool multi) {
+    const sd_config &c = m->cfg;
+    Plan p{};
+    p.splits = 1;
+    switch (kind) {
+    case LK_QKV:
+        p.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+        p.K = c.d_model;
+        p.epi = EPI_QKV;
+        break;
+    case LK_O:
+        p.N = c.d_model;
+        p.K = c.n_heads * c.head_dim;
+        p.epi = EPI_RESID;
+        break;
+    case LK_GATE_UP:
+        p.N = 2 * c.ffn_dim;
+        p.K = c.d_model;
+        p.epi = EPI_SWIGLU;
+        break;
+    case LK_DOWN:
+        p.N = c.d_model;
+        p.K = c.ffn_dim;
+        p.epi = EPI_RESID;
+        break;
+    default:
+        p.N = c.vocab;
+        p.K = c.d_model;
+        p.epi = EPI_HEAD;
+        break;
+    }
+    const bool mfma_ok = m->bf16 && (p.K % 128 == 0) && (kind != LK_QKV || (c.head_dim / 2) % 8 == 0);
+    if (multi && mfma_ok) {
+        p.path = PATH_MFMA;
+        // 16-row tiles
+        if (kind == LK_QKV)
+            p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / 8);
+        else if (kind == LK_GATE_UP)
+            p.n_tiles = cdiv(c.ffn_dim, 8);
+        else
+            p.n_tiles = cdiv(p.N, 16);
+        // norm consumers convert each activation once for two tiles
+        const int TN = (kind == LK_O || kind == LK_DOWN) ? 1 : 2;
+        p.rows = 16 * TN;
+        const int groups = cdiv(p.n_tiles, TN);
+        const int ks = p.K / 128;
+        int splits = 1;
+        if (kind != LK_HEAD) {
+            const int want = cdiv(1536, groups);
+            splits = std::max(1, std::min(want, ks / 8));
+        }
+        p.splits = splits;
+        return p;
+    }
+    p.path = multi ? PATH_VALU16 : PATH_GEMV;
+    if (kind == LK_QKV) {
+        p.rows = qkv_gemv_rows(c.head_dim);
+        p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
+    } else if (kind == LK_GATE_UP) {
+        p.rows = 4;
+        p.n_tiles = cdiv(c.ffn_dim, 2);
+    } else if (kind == LK_HEAD && !multi) {
+        p.rows = 16;
+        p.n_tiles = cdiv(p.N, 16);
+    } else {
+        p.rows = 4;
+        p.n_tiles = cdiv(p.N, 4);
+    }
+    return p;
+}
+
+size_t part_floats(const Plan &p) {
+    if (p.path != PATH_MFMA || p.splits <= 1)
+        return 0;
+    const int TN = p.rows / 16;
+    return (size_t)cdiv(p.n_tiles, TN) * p.splits * (TN * 256 + 16);
+}
+
+int head_tiles(const Plan &p) { return p.n_tiles; }
+
+template <typename T>
+sd_status dev_alloc(T **p, size_t count) {
+    *p = nullptr;
+    if (count == 0)
+        count = 1;
+    if (hipMalloc(reinterpret_cast<void **>(p), count * sizeof(T)) != hipSuccess) {
+        *p = nullptr;
+        return fail(SD_ERR_OOM, "device allocation of " + std::to_string(count * sizeof(T)) + " bytes failed");
+    }
+    return SD_OK;
+}
+
+void dev_free(void *p) {
+    if (p)
+        (void)hipFree(p);
+}
+
+// Rotary table for positions [0, cap): (cos, sin) of pos * base^(-2i/dh),
+// computed in double and rounded to float.
+sd_status ensure_rope(sd_model *m, int cap) {
+    if (cap <= m->rope_cap)
+        return SD_OK;
+    const int half = m->cfg.head_dim / 2;
+    std::vector<float2> tab((size_t)cap * half);
+    for (int p = 0; p < cap; ++p)
+        for (int i = 0; i < half; ++i) {
+            const double theta = std::pow((double)m->cfg.rope_base, -2.0 * (double)i / (double)m->cfg.head_dim);
+            const double ang = (double)p * theta;
+            tab[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+        }
+    SD_HIP(hipStreamSynchronize(m->stream));
+    float2 *nt = nullptr;
+    SD_TRY(dev_alloc(&nt, tab.size()));
+    if (hipMemcpy(nt, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess) {
+        dev_free(nt);
+        return fail(SD_ERR_DEVICE, "rotary table upload failed");
+    }
+    dev_free(m->rope);
+    m->rope = nt;
+    m->rope_cap = cap;
+    return SD_OK;
+}
+
+sd_status ensure_attn(sd_model *m, int cap) {
+    const int splits = cdiv(cap, ATTN_CHUNK);
+    if (splits <= m->attn_splits_cap)
+        return SD_OK;
+    SD_HIP(hipStreamSynchronize(m->stream));
+    float *po = nullptr;
+    float2 *pml = nullptr;
+    const size_t slots = (size_t)splits * m->cfg.n_heads * MAX_ROWS;
+    SD_TRY(dev_alloc(&po, slots * m->cfg.head_dim));
+    if (dev_alloc(&pml, slots) != SD_OK) {
+        dev_free(po);
+        return SD_ERR_OOM;
+    }
+    dev_free(m->attn_o);
+    dev_free(m->attn_ml);
+    m->attn_o = po;
+    m->attn_ml = pml;
+    m->attn_splits_cap = splits;
+    return SD_OK;
+}
+
+sd_status ensure_i32(sd_model *m, int32_t **buf, int *cap, int need) {
+    if (need <= *cap)
+        return SD_OK;
+    SD_HIP(hipStreamSynchronize(m->stream));
+    int32_t *nb = nullptr;
+    SD_TRY(dev_alloc(&nb, (size_t)need));
+    dev_free(*buf);
+    *buf = nb;
+    *cap = need;
+    return SD_OK;
+}
+
+sd_status launch(hipError_t e, const char *what) {
+    if (e != hipSuccess)
+        return fail(SD_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+    return SD_OK;
+}
+
+sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, int64_t ldx, const void *gain,
+                     const EpiArgs &epi) {
+    LinearArgs a{};
+    a.W = W;
+    a.N = p.N;
+    a.K = p.K;
+    a.X = X;
+    a.ldx = ldx;
+    a.gain = gain;
+    a.eps = m->cfg.rms_eps;
+    a.ctl = m->ctl;
+    a.epi = epi;
+    a.part = m->part;
+    a.tile_counter = m->tile_counter;
+    a.splits = p.splits;
+    a.n_tiles = p.n_tiles;
+    return launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer");
+}
+
+struct HeadSpec {
+    int mode = HEAD_NONE;
+    float *logits = nullptr;
+    bool run = false;
+};
+
+// One decoder forward over the rows described by the device control block.
+// multi selects the up-to-16-row kernels; skip is a host mask or null.
+sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, bool multi, const HeadSpec &hs) {
+    const sd_config &c = m->cfg;
+    const Plan *P = multi ? m->planm : m->plan1;
+    const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
+    const size_t ksz = m->wsize;
+    const int64_t head_stride = (int64_t)cap * c.head_dim;
+    SD_TRY(launch(launch_embed(m->tok_emb, m->bf16, c.d_model, m->ctl, m->h, ldh, m->stream), "embedding"));
+    for (int l = 0; l < c.n_layers; ++l) {
+        if (!(skip && skip[2 * l])) {
+            char *kbase = static_cast<char *>(kv) + (size_t)(2 * l) * c.n_kv_heads * head_stride * ksz;
+            char *vbase = static_cast<char *>(kv) + (size_t)(2 * l + 1) * c.n_kv_heads * head_stride * ksz;
+            EpiArgs e{};
+            e.q = m->q;
+            e.ld_q = ldq;
+            e.kcache = kbase;
+            e.vcache = vbase;
+            e.kv_head_stride = head_stride;
+            e.rope = m->rope;
+            e.n_heads = c.n_heads;
+            e.n_kv_heads = c.n_kv_heads;
+            e.head_dim = c.head_dim;
+            e.ffn = c.ffn_dim;
+            SD_TRY(run_linear(m, P[LK_QKV], m->w_qkv[l], m->h, ldh, m->attn_norm[l], e));
+            AttnArgs at{};
+            at.q = m->q;
+            at.ld_q = ldq;
+            at.kcache = kbase;
+            at.vcache = vbase;
+            at.kv_head_stride = head_stride;
+            at.part_o = m->attn_o;
+            at.part_ml = m->attn_ml;
+            at.out = m->o;
+            at.ld_out = ldq;
+            at.n_heads = c.n_heads;
+            at.n_kv_heads = c.n_kv_heads;
+            at.head_dim = c.head_dim;
+            at.splits = cdiv(cap, ATTN_CHUNK);
+            at.ctl = m->ctl;
+            SD_TRY(launch(launch_attention(at, m->bf16, m->stream), "attention"));
+            EpiArgs eo{};
+            eo.out = m->h;
+            eo.ld_out = ldh;
+            SD_TRY(run_linear(m, P[LK_O], m->w_o[l], m->o, ldq, nullptr, eo));
+        }
+        if (!(skip && skip[2 * l + 1])) {
+            EpiArgs eg{};
+            eg.out = m->mbuf;
+            eg.ld_out = c.ffn_dim;
+            eg.ffn = c.ffn_dim;
+            SD_TRY(run_linear(m, P[LK_GATE_UP], m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg));
+            EpiArgs ed{};
+            ed.out = m->h;
+            ed.ld_out = ldh;
+            SD_TRY(run_linear(m, P[LK_DOWN], m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed));
+        }
+    }
+    if (hs.run) {
+        EpiArgs eh{};
+        eh.head.mode = hs.mode;
+        eh.head.logits = hs.logits;
+        eh.head.ld_logits = c.vocab;
+        eh.head.partials = m->head_part;
+        eh.head.counter = m->head_counter;
+        eh.head.st = m->st;
+        eh.head.mb = m->mb_dev;
+        eh.head.out_tokens = m->d_out;
+        eh.head.stage_log = m->d_log;
+        eh.head.stage_log_cap = m->d_log_cap / 2;
+        SD_TRY(run_linear(m, P[LK_HEAD], m->lm_head, m->h, ldh, m->final_norm, eh));
+    }
+    return SD_OK;
+}
+
+size_t kv_bytes(const sd_config &c, int32_t cap) {
+    const size_t es = c.dtype == SD_BF16 ? 2 : 4;
+    return (size_t)c.n_layers * 2 * (size_t)c.n_kv_heads * (size_t)cap * (size_t)c.head_dim * es;
+}
+
+sd_status check_config(const sd_config *c) {
+    if (!c)
+        return fail(SD_ERR_INVALID_ARG, "config is null");
+    if (c->n_layers < 1 || c->d_model < 8 || c->d_model % 8 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+        c->n_heads % c->n_kv_heads || c->head_dim < 8 || c->head_dim % 8 || c->head_dim > MAX_HEAD_DIM ||
+        c->ffn_dim < 8 || c->ffn_dim % 8 || c->vocab < 2 || (c->n_heads * c->head_dim) % 8)
+        return fail(SD_ERR_INVALID_ARG, "unsupported model shape (need d_model, ffn_dim, head_dim multiples of 8, "
+                                        "head_dim <= 128, n_heads a multiple of n_kv_heads)");
+    if (c->dtype != SD_F32 && c->dtype != SD_BF16)
+        return fail(SD_ERR_INVALID_ARG, "dtype must be SD_F32 or SD_BF16");
+    if (!(c->rms_eps > 0.0f) || !(c->rope_base > 0.0f))
+        return fail(SD_ERR_INVALID_ARG, "rms_eps and rope_base must be positive");
+    return SD_OK;
+}
+
+sd_status check_tokens(const sd_model *m, const int32_t *t, int32_t n, const char *what) {
+    if (!t)
+        return fail(SD_ERR_INVALID_ARG, std::string(what) + " is null");
+    for (int32_t i = 0; i < n; ++i)
+        if (t[i] < 0 || t[i] >= m->cfg.vocab)
+            return fail(SD_ERR_INVALID_ARG, std::string(what) + "[" + std::to_string(i) + "] = " +
+                                                std::to_string(t[i]) + " is outside [0, vocab)");
+    return SD_OK;
+}
+
+sd_status check_mask(const sd_model *m, const uint8_t *skip) {
+    if (!skip)
+        return SD_OK;
+    for (int i = 0; i < 2 * m->cfg.n_layers; ++i)
+        if (skip[i] > 1)
+            return fail(SD_ERR_INVALID_ARG, "skip_mask entries must be 0 or 1");
+    return SD_OK;
+}
+
+sd_status create_cache(sd_model *m, int32_t cap, void *buf, sd_kv_cache **out) {
+    if (cap < 1)
+        return fail(SD_ERR_INVALID_ARG, "capacity must be >= 1");
+    if (buf && !aligned16(buf))
+        return fail(SD_ERR_INVALID_ARG, "cache buffer must be 16-byte aligned");
+    SD_TRY(ensure_rope(m, cap));
+    SD_TRY(ensure_attn(m, cap));
+    sd_kv_cache *c = new (std::nothrow) sd_kv_cache{m, buf, buf == nullptr, cap, 0};
+    if (!c)
+        return fail(SD_ERR_OOM, "host allocation failed");
+    if (!buf) {
+        if (hipMalloc(&c->buf, kv_bytes(m->cfg, cap)) != hipSuccess) {
+            delete c;
+            return fail(SD_ERR_OOM, "KV cache allocation of " + std::to_string(kv_bytes(m->cfg, cap)) +
+                                        " bytes failed");
+        }
+    }
+    *out = c;
+    return SD_OK;
+}
+
+void destroy_cache(sd_kv_cache *c) {
+    if (!c)
+        return;
+    if (c->owns)
+        dev_free(c->buf);
+    delete c;
+}
+
+sd_status ensure_gen_cache(sd_model *m, int32_t cap) {
+    if (m->gen_cache && m->gen_cache->cap >= cap)
+        return SD_OK;
+    SD_HIP(hipStreamSynchronize(m->stream));
+    destroy_cache(m->gen_cache);
+    m->gen_cache = nullptr;
+    return create_cache(m, cap, nullptr, &m->gen_cache);
+}
+
+// Prefill: full-model forward of tokens [0, n) already on the device,
+// in chunks of up to MAX_ROWS rows, no head.
+sd_status enqueue_prefill(sd_model *m, sd_kv_cache *kc, const int32_t *dev_tokens, int32_t n, int32_t start) {
+    for (int32_t c = 0; c < n; c += MAX_ROWS) {
+        const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
+        SD_TRY(launch(launch_set_ctl(m->ctl, start + c, rows, dev_tokens + c, m->stream), "control block"));
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, rows > 1, HeadSpec{}));
+    }
+    return SD_OK;
+}
+
+sd_status wait_mailbox(sd_model *m, int32_t seq) {
+    uint64_t spins = 0;
+    for (;;) {
+        const int32_t v = __atomic_load_n(&m->mb_host->seq, __ATOMIC_ACQUIRE);
+        if (v == seq)
+            return SD_OK;
+        if ((++spins & 1023u) == 0) {
+            const hipError_t e = hipStreamQuery(m->stream);
+            if (e == hipSuccess) {
+                if (__atomic_load_n(&m->mb_host->seq, __ATOMIC_ACQUIRE) == seq)
+                    return SD_OK;
+                return fail(SD_ERR_DEVICE, "decode step " + std::to_string(seq) +
+                                               " finished without posting its result");
+            }
+            if (e != hipErrorNotReady)
+                return fail(SD_ERR_DEVICE, std::string("decode step failed: ") + hipGetErrorString(e));
+        }
+#if defined(__x86_64__)
+        _mm_pause();
+#endif
+    }
+}
+
+float elapsed(hipEvent_t a, hipEvent_t b) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess)
+        return 0.0f;
+    return ms;
+}
+
+sd_status copy_results(sd_model *m, int32_t max_new, int32_t *out_tokens, sd_stats *stats) {
+    if (max_new > 0)
+        SD_HIP(hipMemcpyAsync(out_tokens, m->d_out, sizeof(int32_t) * (size_t)max_new, hipMemcpyDeviceToHost,
+                              m->stream));
+    DevState st{};
+    SD_HIP(hipMemcpyAsync(&st, m->st, sizeof st, hipMemcpyDeviceToHost, m->stream));
+    std::vector<int32_t> log;
+    int64_t nlog = 0;
+    if (stats && stats->stage_log && stats->stage_log_cap > 0) {
+        nlog = std::min<int64_t>(stats->stage_log_cap, m->d_log_cap / 2);
+        log.resize((size_t)nlog * 2);
+        SD_HIP(hipMemcpyAsync(log.data(), m->d_log, sizeof(int32_t) * 2 * (size_t)nlog, hipMemcpyDeviceToHost,
+                              m->stream));
+    }
+    SD_HIP(hipStreamSynchronize(m->stream));
+    if (stats) {
+        stats->n_stages = st.n_stages;
+        stats->n_drafted = st.n_drafted;
+        stats->n_accepted = st.n_accepted;
+        stats->n_emitted = st.emitted;
+        stats->n_draft_steps = st.n_draft_steps;
+        if (nlog) {
+            const int64_t n = std::min<int64_t>(nlog, st.n_stages);
+            std::memcpy(stats->stage_log, log.data(), sizeof(int32_t) * 2 * (size_t)n);
+        }
+    }
+    return SD_OK;
+}
+
+sd_status check_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                         int32_t *out_tokens) {
+    if (!m)
+        return fail(SD_ERR_INVALID_ARG, "model is null");
+    if (prompt_len < 1)
+        return fail(SD_ERR_INVALID_ARG, "prompt_len must be >= 1");
+    if (max_new < 0)
+        return fail(SD_ERR_INVALID_ARG, "max_new must be >= 0");
+    if (max_new > 0 && !out_tokens)
+        return fail(SD_ERR_INVALID_ARG, "out_tokens is null");
+    if ((int64_t)prompt_len + max_new + MAX_ROWS > (int64_t)INT32_MAX / 2)
+        return fail(SD_ERR_INVALID_ARG, "prompt_len + max_new too large");
+    return check_tokens(m, prompt, prompt_len, "prompt");
+}
+
+// Shared start of both generate calls: buffers, prompt upload, prefill,
+// decode-state setup.
+sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new, int32_t k_max,
+                         float gamma) {
+    SD_TRY(ensure_gen_cache(m, prompt_len + max_new + k_max + 1));
+    SD_TRY(ensure_i32(m, &m->d_tokens, &m->d_tokens_cap, prompt_len));
+    SD_TRY(ensure_i32(m, &m->d_out, &m->d_out_cap, std::max(max_new, 1)));
+    SD_TRY(ensure_i32(m, &m->d_log, &m->d_log_cap, 2 * std::max(max_new, 1)));
+    SD_HIP(hipMemcpyAsync(m->d_tokens, prompt, sizeof(int32_t) * (size_t)prompt_len, hipMemcpyHostToDevice,
+                          m->stream));
+    SD_HIP(hipEventRecord(m->ev[0], m->stream));
+    m->gen_cache->len = 0;
+    SD_TRY(enqueue_prefill(m, m->gen_cache, m->d_tokens, prompt_len - 1, 0));
+    m->gen_cache->len = prompt_len - 1;
+    SD_HIP(hipEventRecord(m->ev[1], m->stream));
+    __atomic_store_n(&m->mb_host->seq, -1, __ATOMIC_RELEASE);
+    SD_TRY(launch(launch_init_decode(m->st, m->ctl, m->mb_dev, prompt_len - 1, m->d_tokens + prompt_len - 1,
+                                     max_new, k_max, gamma, m->stream),
+                  "decode setup"));
+    return SD_OK;
+}
+
+sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new, const uint8_t *skip,
+                    int32_t k_max, float gamma, int32_t *out_tokens, sd_stats *stats) {
+    SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
+    if (k_max < 0 || k_max > MAX_ROWS - 1)
+        return fail(SD_ERR_INVALID_ARG, "K_max must be in [0, 15]");
+    if (std::isnan(gamma))
+        return fail(SD_ERR_INVALID_ARG, "gamma is NaN");
+    SD_TRY(check_mask(m, skip));
+    SD_TRY(start_generate(m, prompt, prompt_len, max_new, k_max, gamma));
+    sd_kv_cache *kc = m->gen_cache;
+
+    // The host mirrors the phase and waits for each step's decision in the
+    // pinned mailbox before enqueueing the next step.
+    int phase = std::min(k_max, max_new - 1) > 0 ? PHASE_DRAFT : PHASE_VERIFY;
+    bool done = max_new <= 0;
+    int32_t seq = 0;
+    double draft_ms = 0.0, verify_ms = 0.0;
+    int prev_phase = -1;
+    int cur = 0;  // event pair in use: ev[2 + 2 cur], ev[3 + 2 cur]
+    while (!done) {
+        hipEvent_t e0 = m->ev[2 + 2 * cur], e1 = m->ev[3 + 2 * cur];
+        SD_HIP(hipEventRecord(e0, m->stream));
+        HeadSpec hs;
+        hs.run = true;
+        if (phase == PHASE_DRAFT) {
+            hs.mode = HEAD_DRAFT;
+            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, false, hs));
+        } else {
+            hs.mode = HEAD_VERIFY;
+            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, true, hs));
+        }
+        SD_HIP(hipEventRecord(e1, m->stream));
+        ++seq;
+        SD_TRY(wait_mailbox(m, seq));
+        // the previous step's events have completed: account for them
+        if (prev_phase >= 0) {
+            const float ms = elapsed(m->ev[2 + 2 * (1 - cur)], m->ev[3 + 2 * (1 - cur)]);
+            (prev_phase == PHASE_DRAFT ? draft_ms : verify_ms) += ms;
+        }
+        prev_phase = phase;
+        cur = 1 - cur;
+        phase = __atomic_load_n(&m->mb_host->phase, __ATOMIC_ACQUIRE);
+        done = __atomic_load_n(&m->mb_host->gen_done, __ATOMIC_ACQUIRE) != 0;
+    }
+    SD_TRY(copy_results(m, max_new, out_tokens, stats));
+    if (prev_phase >= 0) {
+        const float ms = elapsed(m->ev[2 + 2 * (1 - cur)], m->ev[3 + 2 * (1 - cur)]);
+        (prev_phase == PHASE_DRAFT ? draft_ms : verify_ms) += ms;
+    }
+    if (stats) {
+        stats->draft_ms = draft_ms;
+        stats->verify_ms = verify_ms;
+        stats->prefill_ms = elapsed(m->ev[0], m->ev[1]);
+        stats->total_ms = prev_phase >= 0 ? elapsed(m->ev[0], m->ev[3 + 2 * (1 - cur)]) : stats->prefill_ms;
+        stats->decode_ms = stats->total_ms - stats->prefill_ms;
+    }
+    kc->len = 0;
+    return SD_OK;
+}
+
+sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                         int32_t *out_tokens, sd_stats *stats) {
+    SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
+    SD_TRY(start_generate(m, prompt, prompt_len, max_new, 0, 0.0f));
+    sd_kv_cache *kc = m->gen_cache;
+    HeadSpec hs;
+    hs.run = true;
+    hs.mode = HEAD_AR;
+    for (int32_t i = 0; i < max_new; ++i)
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, false, hs));
+    SD_HIP(hipEventRecord(m->ev[2], m->stream));
+    SD_TRY(copy_results(m, max_new, out_tokens, stats));
+    if (stats) {
+        stats->prefill_ms = elapsed(m->ev[0], m->ev[1]);
+        stats->total_ms = elapsed(m->ev[0], m->ev[2]);
+        stats->decode_ms = stats->total_ms - stats->prefill_ms;
+        stats->draft_ms = 0.0;
+        stats->verify_ms = stats->decode_ms;
+        stats->n_stages = 0;
+    }
+    kc->len = 0;
+    return SD_OK;
+}
+
+sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *skip, sd_kv_cache *kc,
+                  float *logits) {
+    if (!m || !kc)
+        return fail(SD_ERR_INVALID_ARG, "model or cache is null");
+    if (kc->model != m)
+        return fail(SD_ERR_INVALID_ARG, "cache belongs to another model");
+    if (n < 1)
+        return fail(SD_ERR_INVALID_ARG, "n must be >= 1");
+    SD_TRY(check_tokens(m, tokens, n, "tokens"));
+    SD_TRY(check_mask(m, skip));
+    if ((int64_t)kc->len + n > kc->cap)
+        return fail(SD_ERR_CAPACITY, "cache of capacity " + std::to_string(kc->cap) + " holds " +
+                                         std::to_string(kc->len) + " positions; " + std::to_string(n) +
+                                         " more do not fit");
+    SD_TRY(ensure_i32(m, &m->d_tokens, &m->d_tokens_cap, n));
+    SD_HIP(hipMemcpyAsync(m->d_tokens, tokens, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, m->stream));
+    for (int32_t c = 0; c < n; c += MAX_ROWS) {
+        const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
+        SD_TRY(launch(launch_set_ctl(m->ctl, kc->len + c, rows, m->d_tokens + c, m->stream), "control block"));
+        HeadSpec hs;
+        hs.run = logits != nullptr;
+        hs.mode = HEAD_NONE;
+        hs.logits = logits ? logits + (size_t)c * m->cfg.vocab : nullptr;
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, rows > 1, hs));
+    }
+    SD_HIP(hipStreamSynchronize(m->stream));
+    kc->len += n;
+    return SD_OK;
+}
+
+void destroy_model(sd_model *m) {
+    if (!m)
+        return;
+    if (m->stream)
+        (void)hipStreamSynchronize(m->stream);
+    destroy_cache(m->gen_cache);
+    dev_free(m->h);
+    dev_free(m->q);
+    dev_free(m->o);
+    dev_free(m->mbuf);
+    dev_free(m->part);
+    dev_free(m->tile_counter);
+    dev_free(m->head_part);
+    dev_free(m->head_counter);
+    dev_free(m->attn_o);
+    dev_free(m->attn_ml);
+    dev_free(m->rope);
+    dev_free(m->ctl);
+    dev_free(m->st);
+    dev_free(m->d_tokens);
+    dev_free(m->d_out);
+    dev_free(m->d_log);
+    if (m->mb_host)
+        (void)hipHostFree(m->mb_host);
+    for (hipEvent_t &e : m->ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    delete m;
+}
+
+sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, sd_model **out) {
+    if (!out)
+        return fail(SD_ERR_INVALID_ARG, "out is null");
+    *out = nullptr;
+    SD_TRY(check_config(cfg));
+    if (!w)
+        return fail(SD_ERR_INVALID_ARG, "weights is null");
+    const int L = cfg->n_layers;
+    auto ok = [](const void *p) { return p != nullptr && aligned16(p); };
+    if (!ok(w->tok_emb) || !ok(w->final_norm) || !ok(w->lm_head) || !w->attn_norm || !w->w_qkv || !w->w_o ||
+        !w->mlp_norm || !w->w_gate_up || !w->w_down)
+        return fail(SD_ERR_INVALID_ARG, "a weight pointer is null or not 16-byte aligned");
+    for (int l = 0; l < L; ++l)
+        if (!ok(w->attn_norm[l]) || !ok(w->w_qkv[l]) || !ok(w->w_o[l]) || !ok(w->mlp_norm[l]) ||
+            !ok(w->w_gate_up[l]) || !ok(w->w_down[l]))
+            return fail(SD_ERR_INVALID_ARG, "a layer weight pointer is null or not 16-byte aligned (layer " +
+                                                std::to_string(l) + ")");
+    sd_model *m = new (std::nothrow) sd_model;
+    if (!m)
+        return fail(SD_ERR_OOM, "host allocation failed");
+    m->cfg = *cfg;
+    m->bf16 = cfg->dtype == SD_BF16;
+    m->wsize = m->bf16 ? 2 : 4;
+    m->tok_emb = w->tok_emb;
+    m->final_norm = w->final_norm;
+    m->lm_head = w->lm_head;
+    m->attn_norm.assign(w->attn_norm, w->attn_norm + L);
+    m->w_qkv.assign(w->w_qkv, w->w_qkv + L);
+    m->w_o.assign(w->w_o, w->w_o + L);
+    m->mlp_norm.assign(w->mlp_norm, w->mlp_norm + L);
+    m->w_gate_up.assign(w->w_gate_up, w->w_gate_up + L);
+    m->w_down.assign(w->w_down, w->w_down + L);
+    m->stream = reinterpret_cast<hipStream_t>(stream);
+
+    size_t part = 0;
+    int max_groups = 1, max_head_tiles = 1;
+    for (int k = 0; k < LK_COUNT; ++k) {
+        m->plan1[k] = make_plan(m, (LinearKind)k, false);
+        m->planm[k] = make_plan(m, (LinearKind)k, true);
+        for (const Plan *p : {&m->plan1[k], &m->planm[k]}) {
+            part = std::max(part, part_floats(*p));
+            max_groups = std::max(max_groups, p->n_tiles);
+            if (k == LK_HEAD)
+                max_head_tiles = std::max(max_head_tiles, head_tiles(*p));
+        }
+    }
+    const sd_config &c = *cfg;
+    sd_status st = SD_OK;
+    auto chain = [&](sd_status s) {
+        if (st == SD_OK)
+            st = s;
+    };
+    chain(dev_alloc(&m->h, (size_t)MAX_ROWS * c.d_model));
+    chain(dev_alloc(&m->q, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
+    chain(dev_alloc(&m->o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
+    chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
+    chain(dev_alloc(&m->part, part));
+    chain(dev_alloc(&m->tile_counter, (size_t)max_groups));
+    chain(dev_alloc(&m->head_part, (size_t)max_head_tiles * MAX_ROWS));
+    chain(dev_alloc(&m->head_counter, 1));
+    chain(dev_alloc(&m->ctl, 1));
+    chain(dev_alloc(&m->st, 1));
+    if (st != SD_OK) {
+        destroy_model(m);
+        return st;
+    }
+    if (hipHostMalloc(reinterpret_cast<void **>(&m->mb_host), sizeof(Mailbox), hipHostMallocCoherent) !=
+        hipSuccess) {
+        m->mb_host = nullptr;
+        destroy_model(m);
+        return fail(SD_ERR_OOM, "pinned mailbox allocation failed");
+    }
+    std::memset(m->mb_host, 0, sizeof(Mailbox));
+    if (hipHostGetDevicePointer(reinterpret_cast<void **>(&m->mb_dev), m->mb_host, 0) != hipSuccess) {
+        destroy_model(m);
+        return fail(SD_ERR_DEVICE, "mailbox device pointer failed");
+    }
+    for (hipEvent_t &e : m->ev)
+        if (hipEventCreate(&e) != hipSuccess) {
+            destroy_model(m);
+            return fail(SD_ERR_DEVICE, "event creation failed");
+        }
+    // self-resetting counters and scratch start at zero
+    if (hipMemsetAsync(m->tile_counter, 0, sizeof(int32_t) * (size_t)max_groups, m->stream) != hipSuccess ||
+        hipMemsetAsync(m->head_counter, 0, sizeof(int32_t), m->stream) != hipSuccess ||
+        hipMemsetAsync(m->h, 0, sizeof(float) * (size_t)MAX_ROWS * c.d_model, m->stream) != hipSuccess ||
+        hipMemsetAsync(m->mbuf, 0, sizeof(float) * (size_t)MAX_ROWS * c.ffn_dim, m->stream) != hipSuccess ||
+        hipMemsetAsync(m->o, 0, sizeof(float) * (size_t)MAX_ROWS * c.n_heads * c.head_dim, m->stream) !=
+            hipSuccess ||
+        hipStreamSynchronize(m->stream) != hipSuccess) {
+        destroy_model(m);
+        return fail(SD_ERR_DEVICE, "workspace initialisation failed");
+    }
+    *out = m;
+    return SD_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+
+#define SD_GUARD(body)                                                                                 \
+    try {                                                                                              \
+        body                                                                                           \
+    } catch (const std::bad_alloc &) {                                                                 \
+        return fail(SD_ERR_OOM, "host allocation failed");                                             \
+    } catch (...) {                                                                                    \
+        return fail(SD_ERR_DEVICE, "unexpected internal error");                                       \
+    }
+
+extern "C" {
+
+sd_status sd_model_create(const sd_config *config, const sd_weights *weights, void *hip_stream, sd_model **out) {
+    SD_GUARD(g_err.clear(); return create_model(config, weights, hip_stream, out);)
+}
+
+sd_status sd_model_destroy(sd_model *model) {
+    SD_GUARD(if (!model) return fail(SD_ERR_INVALID_ARG, "model is null"); destroy_model(model); return SD_OK;)
+}
+
+size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity) {
+    if (!config || capacity < 0 || check_config(config) != SD_OK)
+        return 0;
+    return kv_bytes(*config, capacity);
+}
+
+sd_status sd_kv_cache_create(sd_model *model, int32_t capacity, void *device_buf, sd_kv_cache **out) {
+    SD_GUARD(if (!model || !out) return fail(SD_ERR_INVALID_ARG, "model or out is null");
+             *out = nullptr; return create_cache(model, capacity, device_buf, out);)
+}
+
+sd_status sd_kv_cache_destroy(sd_kv_cache *cache) {
+    SD_GUARD(if (!cache) return fail(SD_ERR_INVALID_ARG, "cache is null");
+             (void)hipStreamSynchronize(cache->model->stream); destroy_cache(cache); return SD_OK;)
+}
+
+int32_t sd_kv_cache_length(const sd_kv_cache *cache) { return cache ? cache->len : -1; }
+
+sd_status sd_kv_cache_truncate(sd_kv_cache *cache, int32_t len) {
+    if (!cache)
+        return fail(SD_ERR_INVALID_ARG, "cache is null");
+    if (len < 0 || len > cache->len)
+        return fail(SD_ERR_INVALID_ARG, "truncate length must be in [0, length]");
+    cache->len = len;
+    return SD_OK;
+}
+
+sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len) {
+    if (!cache)
+        return fail(SD_ERR_INVALID_ARG, "cache is null");
+    if (len < 0 || len > cache->cap)
+        return fail(SD_ERR_CAPACITY, "length must be in [0, capacity]");
+    cache->len = len;
+    return SD_OK;
+}
+
+sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
+                     sd_kv_cache *cache, float *logits) {
+    SD_GUARD(return forward(model, tokens, n, skip_mask, cache, logits);)
+}
+
+sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                const uint8_t *skip_mask, int32_t K_max, float gamma, int32_t *out_tokens,
+                                sd_stats *stats) {
+    SD_GUARD(return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, gamma, out_tokens, stats);)
+}
+
+sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                     int32_t *out_tokens, sd_stats *stats) {
+    SD_GUARD(return autoregressive(model, prompt, prompt_len, max_new, out_tokens, stats);)
+}
+
+const char *sd_last_error(void) { return g_err.c_str(); }
+
+const char *sd_version(void) { return "sd-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

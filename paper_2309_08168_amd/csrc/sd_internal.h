@@ -1,0 +1,124 @@
+// Library-internal declarations shared by the HIP kernels and the host
+// orchestration.  Not part of the public ABI (include/sd.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sdk {
+
+// Rows of one forward: the verification of K_max <= 15 drafts plus the last
+// committed token, one 16-row MFMA tile, and the prefill chunk size.
+constexpr int MAX_ROWS = 16;
+// Keys per attention work-group (split-KV chunk).
+constexpr int ATTN_CHUNK = 64;
+// Largest head_dim the attention kernel stages in LDS.
+constexpr int MAX_HEAD_DIM = 128;
+
+// Where and what the current forward computes.  Device resident: the
+// greedy head of one step writes the control block of the next step, so
+// the host never needs token ids or positions during decoding.
+struct DevCtl {
+    int32_t pos;               // position of row 0
+    int32_t m;                 // rows in this forward, 1..MAX_ROWS
+    int32_t tokens[MAX_ROWS];  // input token of every row
+};
+
+enum Phase : int32_t { PHASE_DRAFT = 0, PHASE_VERIFY = 1 };
+
+// Decoding state of one generate call (device resident).
+struct DevState {
+    int32_t lc;        // committed KV length: the cache holds every committed token but the last
+    int32_t last;      // last committed token, input of the next forward
+    int32_t emitted;   // tokens written to out_tokens
+    int32_t max_new;
+    int32_t k;         // drafts of the current stage so far
+    int32_t kcap;      // draft budget of the current stage
+    int32_t k_max;
+    int32_t phase;     // what the next step is
+    int32_t gen_done;
+    int32_t seq;       // steps finished (mirrors the mailbox)
+    float gamma;
+    int32_t pad;
+    int32_t drafts[MAX_ROWS];
+    float dpmax[MAX_ROWS];
+    int64_t n_stages, n_drafted, n_accepted, n_draft_steps;
+};
+
+// Pinned host memory the GPU writes after every self-speculative step.
+struct Mailbox {
+    int32_t seq, phase, gen_done, emitted;
+};
+
+enum HeadMode : int32_t { HEAD_NONE = 0, HEAD_AR = 1, HEAD_DRAFT = 2, HEAD_VERIFY = 3 };
+
+enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_HEAD = 4 };
+
+struct HeadArgs {
+    int32_t mode;
+    float *logits;       // optional float32 [m][ld_logits]
+    int64_t ld_logits;
+    float4 *partials;    // [n_tiles][MAX_ROWS]: (max, argmax bits, sum exp(l - max), 0)
+    int32_t *counter;    // one self-resetting counter
+    DevState *st;
+    Mailbox *mb;         // device view of the pinned mailbox (HEAD_DRAFT / HEAD_VERIFY)
+    int32_t *out_tokens;
+    int32_t *stage_log;  // [stage_log_cap][2]
+    int32_t stage_log_cap;
+};
+
+struct EpiArgs {
+    float *out;            // STORE/RESID: [m][ld_out]; SWIGLU: [m][ffn]
+    int64_t ld_out;
+    float *q;              // QKV: rotated queries [m][n_heads * head_dim]
+    int64_t ld_q;
+    void *kcache, *vcache; // QKV: this layer's K and V: [n_kv_heads][cap][head_dim]
+    int64_t kv_head_stride;
+    const float2 *rope;    // [positions][head_dim / 2] of (cos, sin)
+    int32_t n_heads, n_kv_heads, head_dim, ffn;
+    HeadArgs head;
+};
+
+struct LinearArgs {
+    const void *W;         // [N][K] row-major, weight dtype
+    int32_t N, K;
+    const float *X;        // activations [m][ldx] float32
+    int64_t ldx;
+    const void *gain;      // RMSNorm gain [K] (weight dtype), or null: no norm
+    float eps;
+    const DevCtl *ctl;
+    EpiArgs epi;
+    float *part;           // split-K partial tiles
+    int32_t *tile_counter; // one self-resetting counter per work-group column of tiles
+    int32_t splits;
+    int32_t n_tiles;       // tiles in the layer (set by launch_linear)
+};
+
+struct AttnArgs {
+    const float *q;        // [m][n_heads * head_dim]
+    int64_t ld_q;
+    const void *kcache, *vcache;  // this layer: [n_kv_heads][cap][head_dim]
+    int64_t kv_head_stride;
+    float *part_o;         // [splits][n_heads][MAX_ROWS][head_dim]
+    float2 *part_ml;       // [splits][n_heads][MAX_ROWS]: (running max, sum of exp)
+    float *out;            // [m][n_heads * head_dim]
+    int64_t ld_out;
+    int32_t n_heads, n_kv_heads, head_dim, splits;
+    const DevCtl *ctl;
+};
+
+// Kernel paths of the linear layers.
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2 };
+
+// Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
+hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
+                         hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
+hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
+                        hipStream_t s);
+hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *dev_tokens, hipStream_t s);
+hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,
+                              int32_t max_new, int32_t k_max, float gamma, hipStream_t s);
+hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);
+
+}  // namespace sdk
