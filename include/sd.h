@@ -103,11 +103,12 @@ sd_status sd_model_destroy(sd_model *model);
  * n_layers * 2 * n_kv_heads * capacity * head_dim * sizeof(dtype). */
 size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity);
 
-/* Creates a KV cache of capacity positions, length 0.  device_buf, when
+/* Creates a KV cache of capacity positions (1..65536), length 0.  device_buf, when
  * not NULL, is a caller-owned device buffer of sd_kv_cache_bytes() bytes
  * (borrowed), laid out [n_layers][2 (K, V)][n_kv_heads][capacity][head_dim]
  * in the model dtype, with rotary position embedding already applied to K;
- * otherwise the library allocates it.  Errors: INVALID_ARG, OOM. */
+ * otherwise the library allocates it.  Errors: INVALID_ARG, CAPACITY
+ * (more than 65536 positions), OOM. */
 sd_status sd_kv_cache_create(sd_model *model, int32_t capacity, void *device_buf, sd_kv_cache **out);
 sd_status sd_kv_cache_destroy(sd_kv_cache *cache);
 int32_t sd_kv_cache_length(const sd_kv_cache *cache); /* -1 for NULL */

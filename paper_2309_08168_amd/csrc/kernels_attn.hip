@@ -45,16 +45,57 @@ __device__ __forceinline__ float wave_add(float v) {
 }
 
 // Work-group (split, kv head g): keys [split * CH, split * CH + CH) of head
-// g are staged in LDS as float32; the queries of the g-th head group, all
-// rows, attend to them 16 query vectors at a time.  Each (query, split)
-// leaves a partial softmax state (max, sum of exp, unnormalised output).
+// g are staged in LDS in the cache's storage type; the queries of the g-th
+// head group, all rows, attend to them 16 query vectors at a time.  Each
+// (query, split) leaves a partial softmax state (max, sum of exp,
+// unnormalised output).  The last work-group of head group g to finish
+// (counted by a self-resetting counter) combines the splits of every query
+// in split order, so the result is deterministic.
+template <typename TK>
+struct KvLds;
+template <>
+struct KvLds<uint16_t> {
+    static constexpr int PAD = 8;
+    __device__ static void load8(const uint16_t *src, uint16_t *dst) {
+        *reinterpret_cast<u32x4_t *>(dst) = *reinterpret_cast<const u32x4_t *>(src);
+    }
+    __device__ static void read8(const uint16_t *p, float *v) {
+        const u32x4_t w = *reinterpret_cast<const u32x4_t *>(p);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = __uint_as_float(w[j] << 16);
+            v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+        }
+    }
+    __device__ static float read1(const uint16_t *p) { return __uint_as_float(((uint32_t)*p) << 16); }
+};
+template <>
+struct KvLds<float> {
+    static constexpr int PAD = 4;
+    __device__ static void load8(const float *src, float *dst) {
+        reinterpret_cast<f32x4_t *>(dst)[0] = reinterpret_cast<const f32x4_t *>(src)[0];
+        reinterpret_cast<f32x4_t *>(dst)[1] = reinterpret_cast<const f32x4_t *>(src)[1];
+    }
+    __device__ static void read8(const float *p, float *v) {
+        const f32x4_t a = reinterpret_cast<const f32x4_t *>(p)[0];
+        const f32x4_t b = reinterpret_cast<const f32x4_t *>(p)[1];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[j] = a[j];
+            v[4 + j] = b[j];
+        }
+    }
+    __device__ static float read1(const float *p) { return *p; }
+};
+
 template <typename TK>
 __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
     constexpr int CH = ATTN_CHUNK;
     constexpr int DMAX = MAX_HEAD_DIM;
-    __shared__ float Ks[CH][DMAX + 4];
-    __shared__ float Vs[CH][DMAX];
-    __shared__ float Qs[16][DMAX];
+    constexpr int KS = DMAX + KvLds<TK>::PAD;
+    __shared__ __attribute__((aligned(16))) TK Ks[CH * KS];
+    __shared__ __attribute__((aligned(16))) TK Vs[CH * DMAX];
+    __shared__ __attribute__((aligned(16))) float Qs[16][DMAX];
     __shared__ float Ss[16][CH];
     __shared__ float2 MLs[16];
     const int split = blockIdx.x, g = blockIdx.y;
@@ -74,8 +115,8 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
     const int d8 = dh >> 3;
     for (int i = tid; i < nk * d8; i += 256) {
         const int key = i / d8, e = (i - key * d8) * 8;
-        load8_kv(Kg + (int64_t)key * dh + e, &Ks[key][e]);
-        load8_kv(Vg + (int64_t)key * dh + e, &Vs[key][e]);
+        KvLds<TK>::load8(Kg + (int64_t)key * dh + e, &Ks[key * KS + e]);
+        KvLds<TK>::load8(Vg + (int64_t)key * dh + e, &Vs[key * DMAX + e]);
     }
     const float scale = 1.0f / sqrtf((float)dh);
 
@@ -88,23 +129,42 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
             Qs[qi][e] = a.q[(int64_t)r * a.ld_q + (int64_t)head * dh + e] * scale;
         }
         __syncthreads();
-        for (int p = tid; p < nq * CH; p += 256) {
-            const int qi = p / CH, c = p - qi * CH;
-            const int r = (qg + qi) / G;
-            float sres = -INFINITY;
-            if (c < nk && c0 + c <= pos + r) {
-                float acc = 0.0f;
-                for (int e = 0; e < dh; e += 4) {
-                    const float4 kv = *reinterpret_cast<const float4 *>(&Ks[c][e]);
-                    const float4 qv = *reinterpret_cast<const float4 *>(&Qs[qi][e]);
-                    acc = fmaf(qv.x, kv.x, acc);
-                    acc = fmaf(qv.y, kv.y, acc);
-                    acc = fmaf(qv.z, kv.z, acc);
-                    acc = fmaf(qv.w, kv.w, acc);
+        // scores: thread (key c, query lane ql) takes queries ql, ql + 4, ...
+        {
+            const int c = tid & (CH - 1), ql = tid >> 6;
+            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (c < nk && ql < nq) {
+                for (int e = 0; e < dh; e += 8) {
+                    float kv[8];
+                    KvLds<TK>::read8(&Ks[c * KS + e], kv);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int qi = ql + 4 * u;
+                        if (qi < nq) {
+                            const float4 q0 = *reinterpret_cast<const float4 *>(&Qs[qi][e]);
+                            const float4 q1 = *reinterpret_cast<const float4 *>(&Qs[qi][e + 4]);
+                            float s = acc[u];
+                            s = fmaf(q0.x, kv[0], s);
+                            s = fmaf(q0.y, kv[1], s);
+                            s = fmaf(q0.z, kv[2], s);
+                            s = fmaf(q0.w, kv[3], s);
+                            s = fmaf(q1.x, kv[4], s);
+                            s = fmaf(q1.y, kv[5], s);
+                            s = fmaf(q1.z, kv[6], s);
+                            s = fmaf(q1.w, kv[7], s);
+                            acc[u] = s;
+                        }
+                    }
                 }
-                sres = acc;
             }
-            Ss[qi][c] = sres;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int qi = ql + 4 * u;
+                if (qi < nq) {
+                    const int r = (qg + qi) / G;
+                    Ss[qi][c] = (c < nk && c0 + c <= pos + r) ? acc[u] : -INFINITY;
+                }
+            }
         }
         __syncthreads();
         for (int qi = wave; qi < nq; qi += 4) {
@@ -121,7 +181,7 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
             const int qi = i / dh, e = i - qi * dh;
             float acc = 0.0f;
             for (int c = 0; c < nk; ++c)
-                acc = fmaf(Ss[qi][c], Vs[c][e], acc);
+                acc = fmaf(Ss[qi][c], KvLds<TK>::read1(&Vs[c * DMAX + e]), acc);
             const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
             const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
             a.part_o[slot * dh + e] = acc;
@@ -129,36 +189,68 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
                 a.part_ml[slot] = MLs[qi];
         }
     }
+
 }
 
 // Ordered combine of the split partials of one (head, row): deterministic.
+// The running maxima and sums of all splits are loaded in parallel first.
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
+    __shared__ float w_s[MAX_SPLITS];
+    __shared__ float2 ml_s[MAX_SPLITS];
+    __shared__ float red[2];
     const int head = blockIdx.x, r = blockIdx.y;
     const int pos = a.ctl->pos, M = a.ctl->m;
     if (r >= M)
         return;
     const int ns = (pos + M + ATTN_CHUNK - 1) / ATTN_CHUNK;
-    const int dh = a.head_dim, H = a.n_heads;
+    const int dh = a.head_dim, H = a.n_heads, tid = threadIdx.x;
     float mx = -INFINITY;
-    for (int s = 0; s < ns; ++s)
-        mx = fmaxf(mx, a.part_ml[((int64_t)s * H + head) * MAX_ROWS + r].x);
-    for (int e = threadIdx.x; e < dh; e += blockDim.x) {
-        float L = 0.0f, O = 0.0f;
-        for (int s = 0; s < ns; ++s) {
-            const int64_t slot = ((int64_t)s * H + head) * MAX_ROWS + r;
-            const float2 ml = a.part_ml[slot];
-            if (ml.x == -INFINITY)
-                continue;
-            const float w = expf(ml.x - mx);
-            L = fmaf(w, ml.y, L);
-            O = fmaf(w, a.part_o[slot * dh + e], O);
+    for (int sp = tid; sp < ns; sp += 128) {
+        const float2 v = a.part_ml[((int64_t)sp * H + head) * MAX_ROWS + r];
+        ml_s[sp] = v;
+        mx = fmaxf(mx, v.x);
+    }
+    mx = wave_max(mx);
+    if ((tid & 63) == 0)
+        red[tid >> 6] = mx;
+    __syncthreads();
+    mx = fmaxf(red[0], red[1]);
+    for (int sp = tid; sp < ns; sp += 128) {
+        const float2 v = ml_s[sp];
+        w_s[sp] = v.x == -INFINITY ? 0.0f : expf(v.x - mx);
+    }
+    __syncthreads();
+    float L = 0.0f;
+    for (int sp = 0; sp < ns; ++sp)
+        L = fmaf(w_s[sp], ml_s[sp].y, L);
+    for (int e = tid; e < dh; e += 128) {
+        float O = 0.0f;
+        int sp = 0;
+        for (; sp + 8 <= ns; sp += 8) {
+            float ov[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                ov[u] = a.part_o[(((int64_t)(sp + u) * H + head) * MAX_ROWS + r) * dh + e];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                O = fmaf(w_s[sp + u], ov[u], O);
         }
-        a.out[(int64_t)r * a.ld_out + (int64_t)head * dh + e] = O / L;
+        for (; sp < ns; ++sp)
+            O = fmaf(w_s[sp], a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e], O);
+        const float y = O / L;
+        const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
+        if (a.out_hi) {
+            const uint32_t b = __float_as_uint(y);
+            a.out_hi[oi] = (uint16_t)(b >> 16);
+            a.out_lo[oi] = (uint16_t)(__float_as_uint(y - __uint_as_float(b & 0xffff0000u)) >> 16);
+        } else {
+            a.out[oi] = y;
+        }
     }
 }
 
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s) {
-    if (a.head_dim > MAX_HEAD_DIM || (a.head_dim & 7))
+    if (a.head_dim > MAX_HEAD_DIM || (a.head_dim & 7) || a.splits > MAX_SPLITS)
         return hipErrorInvalidValue;
     dim3 grid(a.splits, a.n_kv_heads), block(256);
     if (bf16)

@@ -7,6 +7,7 @@
 // speed), so the three main loops below are built to read each weight byte
 // exactly once with 16-byte loads:
 //   - k_linear_valu, MR == 1: the GEMV of a draft or autoregressive step;
+//   - k_linear_valu, MR == 4: verification of up to 3 drafts;
 //   - k_linear_valu, MR == 16: any row count, for float32 weights;
 //   - k_linear_mfma: the verification forward over up to 16 rows (the last
 //     committed token plus the drafts, Algorithm 2), bf16 MFMA tiles with
@@ -32,6 +33,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     uint32_t u = __float_as_uint(f);
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
+}
+
+// Split u into bf16 hi (its top 16 bits) and lo (the remainder, rounded
+// down to bf16): hi + lo keeps about 16 bits of u's mantissa.
+__device__ __forceinline__ void split_hilo(float u, uint16_t &hi, uint16_t &lo) {
+    const uint32_t b = __float_as_uint(u);
+    hi = (uint16_t)(b >> 16);
+    lo = (uint16_t)(__float_as_uint(u - __uint_as_float(b & 0xffff0000u)) >> 16);
 }
 
 __device__ __forceinline__ void unpack8(u32x4_t v, float (&w)[8]) {
@@ -222,34 +231,56 @@ __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, co
 
 // Last work-group of the head: combine the per-tile partials of every row
 // in a fixed order (deterministic), then take the decoding decision.
+// Thread j takes tiles j, j + 256, ... of every row (independent loads,
+// issued together), then the 256 partial results of a row are combined by
+// a fixed tree across lanes and waves.
+__device__ HeadPart head_shfl(HeadPart v, int o) {
+    HeadPart r;
+    r.mx = __shfl_xor(v.mx, o, 64);
+    r.idx = __shfl_xor(v.idx, o, 64);
+    r.sum = __shfl_xor(v.sum, o, 64);
+    return r;
+}
+
 __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
-    __shared__ HeadPart hred[256];
+    __shared__ HeadPart wred[4][MAX_ROWS];
     __shared__ int ys[MAX_ROWS];
     __shared__ float ps[MAX_ROWS];
-    const int tid = threadIdx.x;
-    const int m = tid >> 4, j = tid & 15;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const HeadArgs &h = a.epi.head;
-    HeadPart acc = head_empty();
-    if (m < M) {
-        for (int t = j; t < n_tiles; t += 16) {
+    for (int m = 0; m < M; ++m) {
+        HeadPart acc = head_empty();
+        int t = tid;
+        for (; t + 768 < n_tiles; t += 1024) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                v[u] = h.partials[(int64_t)(t + 256 * u) * MAX_ROWS + m];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                acc = head_comb(acc, HeadPart{v[u].x, __float_as_int(v[u].y), v[u].z});
+        }
+        for (; t < n_tiles; t += 256) {
             const float4 v = h.partials[(int64_t)t * MAX_ROWS + m];
             acc = head_comb(acc, HeadPart{v.x, __float_as_int(v.y), v.z});
         }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1)
+            acc = head_comb(acc, head_shfl(acc, o));
+        if (lane == 0)
+            wred[wave][m] = acc;
     }
-    hred[tid] = acc;
     __syncthreads();
     if (tid < M) {
-        HeadPart r = hred[tid * 16];
-        for (int jj = 1; jj < 16; ++jj)
-            r = head_comb(r, hred[tid * 16 + jj]);
+        HeadPart r = wred[0][tid];
+        for (int w = 1; w < 4; ++w)
+            r = head_comb(r, wred[w][tid]);
         ys[tid] = r.idx;
         ps[tid] = 1.0f / r.sum;
     }
     __syncthreads();
-    if (tid == 0) {
-        *h.counter = 0;
+    if (tid == 0)
         decode_decision(h, const_cast<DevCtl *>(a.ctl), ys, ps);
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -280,7 +311,15 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
             if (f < e.ffn) {
                 const float g = fin[i * MR + m] * inv[m];
                 const float u = fin[(i + P) * MR + m] * inv[m];
-                e.out[(int64_t)m * e.ld_out + f] = g / (1.0f + expf(-g)) * u;
+                const float y = g / (1.0f + expf(-g)) * u;
+                if (e.out_hi) {
+                    uint16_t hb, lb;
+                    split_hilo(y, hb, lb);
+                    e.out_hi[(int64_t)m * e.ld_out + f] = hb;
+                    e.out_lo[(int64_t)m * e.ld_out + f] = lb;
+                } else {
+                    e.out[(int64_t)m * e.ld_out + f] = y;
+                }
             }
         }
     } else if constexpr (EPI == EPI_QKV) {
@@ -345,19 +384,10 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
     }
 }
 
-// After the head epilogue of every tile of this work-group: the last
-// work-group of the grid to finish combines all tiles.
-__device__ void head_complete(const LinearArgs &a, int n_tiles, int M) {
-    __shared__ int is_last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0)
-        is_last = atomicAdd(a.epi.head.counter, 1) == (int)gridDim.x - 1;
-    __syncthreads();
-    if (!is_last)
-        return;
-    __threadfence();
-    head_finalize(a, n_tiles, M);
+// One work-group after the head: combine the partials of all tiles and take
+// the decoding decision.
+__global__ __launch_bounds__(256) void k_head_finalize(LinearArgs a) {
+    head_finalize(a, a.n_tiles, a.ctl->m);
 }
 
 // ---------------------------------------------------------------------------
@@ -457,179 +487,118 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
     }
     __syncthreads();
     run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, M);
-    if constexpr (EPI == EPI_HEAD)
-        head_complete(a, gridDim.x, M);
 }
 
 // ---------------------------------------------------------------------------
-// MFMA main loop (bf16 weights, up to 16 rows).  Work-group (group t, split
-// s) owns TN tiles of 16 weight rows and a contiguous range of 128-element
-// k-steps; its four waves take every fourth k-step.  In a k-step, lane l
-// loads 64 contiguous bytes (32 bf16) of weight row l % 16 of each tile at
-// k offset 32 (l / 16), and the same 32 activations of input row l % 16;
-// those feed four 16x16x32 MFMAs per tile.  The k order inside an MFMA is a
-// permutation shared by both operands, so the dot products are unchanged.
-// Activations enter as a hi + lo pair of bf16 (hi = the top 16 bits, lo =
-// the rest rounded down to bf16, two MFMAs per k-block), which keeps about
-// 16 bits of their mantissa; the weights are exact in bf16.  The split of
-// one activation serves TN tiles.  With more than one split, each
-// work-group writes its partial tiles and the last one to finish adds them
-// in split order (deterministic) and runs the epilogue.
+// MFMA main loop (bf16 weights, up to 16 rows).  A work-group owns TN tiles
+// of 16 weight rows and the whole reduction dimension; its NW waves each
+// stream a contiguous range of 128-element k-steps and are summed in LDS at
+// the end, so no work-group depends on another.  A k-step is four 16x16x32
+// MFMAs per tile; for MFMA i, lane l supplies the 8 weights of row l % 16 at
+// k offset 32 i + 8 (l / 16), so one load instruction reads 64 contiguous
+// bytes of each of the 16 rows, and the next instruction the following 64
+// bytes of the same cache lines.  Lane l supplies the same 8 activations of
+// input row l % 16.  The k order inside an MFMA is a permutation shared by
+// both operands, so the dot products are unchanged.  Activations arrive
+// pre-split into a hi + lo pair of bf16 (k_prep_norm, or the producing
+// epilogue), two MFMAs per k-block, which keeps about 16 bits of their
+// mantissa; the weights are exact in bf16.  The loop body is loads and
+// MFMAs only.
 
-__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
-    return (a >> 16) | (b & 0xffff0000u);
+template <int TN>
+__device__ __forceinline__ void mfma_load(u32x4_t (&wv)[TN][4], const uint16_t *const (&Wr)[TN], int k0) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            wv[j][i] = *reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 32 * i);
 }
 
-template <int EPI, bool NORM, int TN>
-__global__ __launch_bounds__(256) void k_linear_mfma(LinearArgs a) {
-    __shared__ float red[4][TN * 16][17];
-    __shared__ float red_ss[4][16];
+// One k-step: the hi and lo activation fragments of k-step k0 against the
+// weights already in registers.
+template <int TN>
+__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const uint16_t *Xh, const uint16_t *Xl,
+                                           bool xrow, int k0, floatx4_t (&acc)[TN]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        u32x4_t bhi = {0u, 0u, 0u, 0u}, blo = {0u, 0u, 0u, 0u};
+        if (xrow) {
+            bhi = *reinterpret_cast<const u32x4_t *>(Xh + k0 + 32 * i);
+            blo = *reinterpret_cast<const u32x4_t *>(Xl + k0 + 32 * i);
+        }
+        const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bhi);
+        const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, blo);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, wv[j][i]);
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bh, acc[j], 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bl, acc[j], 0, 0, 0);
+        }
+    }
+}
+
+template <int EPI, int TN, int NW>
+__global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
+    __shared__ float red[NW][TN * 16][17];
     __shared__ float fin[TN * 16 * 16];
     __shared__ float inv_s[16];
-    __shared__ int is_last;
-    const int S = a.splits;
-    const int grp = blockIdx.x / S, s = blockIdx.x - grp * S;
+    const int grp = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
     const int M = a.ctl->m;
-    const int n_tiles = a.n_tiles;  // 16-row tiles in the layer
+    const int n_tiles = a.n_tiles;
     const uint16_t *Wr[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int t = grp * TN + j;
         const bool nv = t < n_tiles && row_valid<EPI>(t, r16, 16, a.N, a.epi);
         const int n = nv ? tile_row<EPI>(t, r16, 16, a.epi) : 0;
-        Wr[j] = reinterpret_cast<const uint16_t *>(a.W) + (int64_t)n * a.K + kg * 32;
+        Wr[j] = reinterpret_cast<const uint16_t *>(a.W) + (int64_t)n * a.K + kg * 8;
     }
-    const float *Xr = a.X + (int64_t)r16 * a.ldx + kg * 32;
-    const uint16_t *Gp = reinterpret_cast<const uint16_t *>(a.gain) + kg * 32;
+    const uint16_t *Xh = a.Xh + (int64_t)r16 * a.ldx + kg * 8;
+    const uint16_t *Xl = a.Xl + (int64_t)r16 * a.ldx + kg * 8;
     const bool xrow = r16 < M;
     const int KS = a.K >> 7;
-    const int sb = (int)(((int64_t)KS * s) / S), se = (int)(((int64_t)KS * (s + 1)) / S);
 
     floatx4_t acc[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j)
         acc[j] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    float ss = 0.0f;
-    for (int q = sb + wave; q < se; q += 4) {
-        const int k0 = q << 7;
-        u32x4_t wv[TN][4];
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                wv[j][i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 8 * i));
-        float x[32];
-        if (xrow) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const f32x4_t v = reinterpret_cast<const f32x4_t *>(Xr + k0)[j];
-                x[4 * j] = v[0];
-                x[4 * j + 1] = v[1];
-                x[4 * j + 2] = v[2];
-                x[4 * j + 3] = v[3];
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 32; ++j)
-                x[j] = 0.0f;
+    // Each wave streams a contiguous range of k-steps with the weights of
+    // the next k-step in flight while the current one is multiplied.
+    const int q_beg = (int)(((int64_t)KS * wave) / NW), q_end = (int)(((int64_t)KS * (wave + 1)) / NW);
+    if (q_beg < q_end) {
+        u32x4_t wa[TN][4], wb[TN][4];
+        mfma_load<TN>(wa, Wr, q_beg << 7);
+        int q = q_beg;
+        for (; q + 2 <= q_end; q += 2) {
+            mfma_load<TN>(wb, Wr, (q + 1) << 7);
+            mfma_kstep<TN>(wa, Xh, Xl, xrow, q << 7, acc);
+            if (q + 2 < q_end)
+                mfma_load<TN>(wa, Wr, (q + 2) << 7);
+            mfma_kstep<TN>(wb, Xh, Xl, xrow, (q + 1) << 7, acc);
         }
-        if constexpr (NORM) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float g[8];
-                ldg8(Gp + k0 + 8 * j, g);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    ss = fmaf(x[8 * j + e], x[8 * j + e], ss);
-                    x[8 * j + e] *= g[e];
-                }
-            }
-        }
-        u32x4_t bhi[4], blo[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t u0 = __float_as_uint(x[8 * i + 2 * e]);
-                const uint32_t u1 = __float_as_uint(x[8 * i + 2 * e + 1]);
-                const float l0 = x[8 * i + 2 * e] - __uint_as_float(u0 & 0xffff0000u);
-                const float l1 = x[8 * i + 2 * e + 1] - __uint_as_float(u1 & 0xffff0000u);
-                bhi[i][e] = pack_hi(u0, u1);
-                blo[i][e] = pack_hi(__float_as_uint(l0), __float_as_uint(l1));
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bhi[i]);
-            const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, blo[i]);
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, wv[j][i]);
-                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bh, acc[j], 0, 0, 0);
-                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bl, acc[j], 0, 0, 0);
-            }
-        }
+        if (q < q_end)
+            mfma_kstep<TN>(wa, Xh, Xl, xrow, q << 7, acc);
     }
 
     // D[n_local][m]: lane l holds rows 4 (l / 16) + v, column l % 16.
-    ss += __shfl_xor(ss, 16, 64);
-    ss += __shfl_xor(ss, 32, 64);
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
             red[wave][16 * j + 4 * kg + v][r16] = acc[j][v];
-    if (kg == 0)
-        red_ss[wave][r16] = ss;
     __syncthreads();
-    const int mi = tid & 15;
-    float val[TN];
+    for (int o = tid; o < TN * 256; o += NW * 64) {
+        const int ni = o >> 4, mi = o & 15;
+        float v = 0.0f;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int ni = 16 * j + (tid >> 4);
-        val[j] = (red[0][ni][mi] + red[1][ni][mi]) + (red[2][ni][mi] + red[3][ni][mi]);
+        for (int w = 0; w < NW; ++w)
+            v += red[w][ni][mi];
+        fin[o] = v;
     }
-    float ssv = 0.0f;
-    if (NORM && tid < 16)
-        ssv = (red_ss[0][tid] + red_ss[1][tid]) + (red_ss[2][tid] + red_ss[3][tid]);
-    if (S > 1) {
-        constexpr int PS = TN * 256 + 16;
-        float *pp = a.part + ((int64_t)grp * S + s) * PS;
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-            pp[256 * j + tid] = val[j];
-        if (NORM && tid < 16)
-            pp[TN * 256 + tid] = ssv;
-        __threadfence();
-        __syncthreads();
-        if (tid == 0)
-            is_last = atomicAdd(&a.tile_counter[grp], 1) == S - 1;
-        __syncthreads();
-        if (!is_last)
-            return;
-        __threadfence();
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-            val[j] = 0.0f;
-        ssv = 0.0f;
-        for (int sp = 0; sp < S; ++sp) {
-            const float *pj = a.part + ((int64_t)grp * S + sp) * PS;
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                val[j] += pj[256 * j + tid];
-            if (NORM && tid < 16)
-                ssv += pj[TN * 256 + tid];
-        }
-        if (tid == 0)
-            a.tile_counter[grp] = 0;
-    }
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-        fin[256 * j + (tid >> 4) * 16 + mi] = val[j];
     if (tid < 16)
-        inv_s[tid] = NORM ? 1.0f / sqrtf(ssv / (float)a.K + a.eps) : 1.0f;
+        inv_s[tid] = 1.0f;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -637,8 +606,59 @@ __global__ __launch_bounds__(256) void k_linear_mfma(LinearArgs a) {
         if (t < n_tiles)
             run_epilogue<uint16_t, EPI>(a, fin + 256 * j, 16, 16, inv_s, t, M);
     }
-    if constexpr (EPI == EPI_HEAD)
-        head_complete(a, n_tiles, M);
+}
+
+// ---------------------------------------------------------------------------
+// Activations for the MFMA path, once per forward: u = g * h / rms(h) (or
+// u = h without a gain), split into bf16 hi (top 16 bits) and lo (the rest,
+// rounded down to bf16).  One work-group per row.
+
+template <typename TW>
+__global__ __launch_bounds__(256) void k_prep_norm(const float *h, int64_t ldh, const TW *g, float eps, int K,
+                                                   const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    if (r >= ctl->m)
+        return;
+    const int tid = threadIdx.x;
+    const float *hr = h + (int64_t)r * ldh;
+    float inv = 1.0f;
+    if (g) {
+        float ss = 0.0f;
+        for (int k = tid; k < K; k += 256)
+            ss = fmaf(hr[k], hr[k], ss);
+        ss = wave_sum(ss);
+        if ((tid & 63) == 0)
+            red[tid >> 6] = ss;
+        __syncthreads();
+        inv = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
+    }
+    for (int k = tid; k < K; k += 256) {
+        float u = hr[k];
+        if (g) {
+            float gk;
+            if constexpr (sizeof(TW) == 2)
+                gk = bf2f(g[k]);
+            else
+                gk = g[k];
+            u = gk * (u * inv);
+        }
+        uint16_t hi, lo;
+        split_hilo(u, hi, lo);
+        xh[(int64_t)r * ldx + k] = hi;
+        xl[(int64_t)r * ldx + k] = lo;
+    }
+}
+
+hipError_t launch_prep_norm(const float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
+                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, hipStream_t s) {
+    if (bf16)
+        hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(256), 0, s, h, ldh,
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xh, xl, ldx);
+    else
+        hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(256), 0, s, h, ldh,
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xh, xl, ldx);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -681,7 +701,7 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
     case 8:
         return launch_valu<TW, MR, 8>(a, epi, n_tiles, s);
     case 16:
-        if constexpr (MR == 1)
+        if constexpr (MR <= 4)
             return launch_valu<TW, MR, 16>(a, epi, n_tiles, s);
         return hipErrorInvalidValue;
     default:
@@ -689,35 +709,36 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
     }
 }
 
-template <int TN>
-static hipError_t launch_mfma(const LinearArgs &a0, int epi, int n_tiles, hipStream_t s) {
-    LinearArgs a = a0;
-    a.n_tiles = n_tiles;
+template <int TN, int NW>
+static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
     const int groups = (n_tiles + TN - 1) / TN;
-    dim3 grid(groups * a.splits), block(256);
-    const bool norm = a.gain != nullptr;
+    dim3 grid(groups), block(NW * 64);
     switch (epi) {
     case EPI_STORE:
-        if (norm)
-            hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, true, TN>), grid, block, 0, s, a);
-        else
-            hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, false, TN>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, TN, NW>), grid, block, 0, s, a);
         break;
     case EPI_RESID:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, false, TN>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, TN, NW>), grid, block, 0, s, a);
         break;
     case EPI_SWIGLU:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, true, TN>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, TN, NW>), grid, block, 0, s, a);
         break;
     case EPI_QKV:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, true, TN>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, TN, NW>), grid, block, 0, s, a);
         break;
     case EPI_HEAD:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, true, TN>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, TN, NW>), grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s) {
+    LinearArgs b = a;
+    b.n_tiles = n_tiles;
+    hipLaunchKernelGGL(k_head_finalize, dim3(1), dim3(256), 0, s, b);
     return hipGetLastError();
 }
 
@@ -727,25 +748,35 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
         return hipSuccess;
     if (path == PATH_MFMA) {
         // rows_per_tile = 16 * TN; n_tiles counts 16-row tiles.
-        const int TN = rows_per_tile / 16;
-        if (!bf16 || (a.K & 127) || (TN != 1 && TN != 2 && TN != 4) || rows_per_tile != 16 * TN)
+        const int TN = rows_per_tile / 16, NW = a.waves;
+        if (!bf16 || (a.K & 127) || rows_per_tile != 16 * TN)
             return hipErrorInvalidValue;
-        if (epi == EPI_HEAD && a.splits != 1)
+        LinearArgs b = a;
+        b.n_tiles = n_tiles;
+        if (!a.Xh || !a.Xl)
             return hipErrorInvalidValue;
-        switch (TN) {
-        case 1:
-            return launch_mfma<1>(a, epi, n_tiles, s);
-        case 2:
-            return launch_mfma<2>(a, epi, n_tiles, s);
-        default:
-            return launch_mfma<4>(a, epi, n_tiles, s);
-        }
+        if (TN == 1 && NW == 8)
+            return launch_mfma<1, 8>(b, epi, n_tiles, s);
+        if (TN == 1 && NW == 16)
+            return launch_mfma<1, 16>(b, epi, n_tiles, s);
+        if (TN == 2 && NW == 4)
+            return launch_mfma<2, 4>(b, epi, n_tiles, s);
+        if (TN == 2 && NW == 8)
+            return launch_mfma<2, 8>(b, epi, n_tiles, s);
+        if (TN == 4 && NW == 4)
+            return launch_mfma<4, 4>(b, epi, n_tiles, s);
+        if (TN == 4 && NW == 2)
+            return launch_mfma<4, 2>(b, epi, n_tiles, s);
+        return hipErrorInvalidValue;
     }
     if (a.K & 7)
         return hipErrorInvalidValue;
     if (path == PATH_GEMV)
         return bf16 ? launch_valu_r<uint16_t, 1>(a, epi, rows_per_tile, n_tiles, s)
                     : launch_valu_r<float, 1>(a, epi, rows_per_tile, n_tiles, s);
+    if (path == PATH_VALU4)
+        return bf16 ? launch_valu_r<uint16_t, 4>(a, epi, rows_per_tile, n_tiles, s)
+                    : launch_valu_r<float, 4>(a, epi, rows_per_tile, n_tiles, s);
     return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s)
                 : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s);
 }

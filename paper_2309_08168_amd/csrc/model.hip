@@ -53,7 +53,7 @@ struct Plan {
     int path;     // PATH_GEMV, PATH_VALU16 or PATH_MFMA
     int rows;     // weight rows per work-group
     int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
-    int splits;   // MFMA split-K factor
+    int waves;    // MFMA: waves per work-group splitting the reduction
     int N, K, epi;
 };
 
@@ -76,13 +76,15 @@ struct sd_model {
     hipStream_t stream = nullptr;
 
     Plan plan1[LK_COUNT];  // one row (draft / autoregressive step)
-    Plan planm[LK_COUNT];  // up to 16 rows (verification, prefill)
+    Plan plan4[LK_COUNT];  // up to 4 rows (short verification)
+    Plan planm[LK_COUNT];  // up to 16 rows (long verification, prefill)
 
     float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
-    float *part = nullptr;
-    int32_t *tile_counter = nullptr;
+    // MFMA-path activations split into bf16 hi/lo, [MAX_ROWS][xld]: pair a holds
+    // normalised inputs and the attention output, pair b the SwiGLU output.
+    uint16_t *xa_h = nullptr, *xa_l = nullptr, *xb_h = nullptr, *xb_l = nullptr;
+    int64_t xld = 0;
     float4 *head_part = nullptr;
-    int32_t *head_counter = nullptr;
     float *attn_o = nullptr;
     float2 *attn_ml = nullptr;
     int attn_splits_cap = 0;
@@ -115,10 +117,12 @@ int qkv_gemv_rows(int head_dim) {
     return 4;
 }
 
-Plan make_plan(const sd_model *m, LinearKind kind, bool multi) {
+// rows: the largest row count the plan serves (1, 4 or 16).
+Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
+    const bool multi = rows > 1;
     const sd_config &c = m->cfg;
     Plan p{};
-    p.splits = 1;
+    p.waves = 4;
     switch (kind) {
     case LK_QKV:
         p.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
@@ -147,7 +151,7 @@ Plan make_plan(const sd_model *m, LinearKind kind, bool multi) {
         break;
     }
     const bool mfma_ok = m->bf16 && (p.K % 128 == 0) && (kind != LK_QKV || (c.head_dim / 2) % 8 == 0);
-    if (multi && mfma_ok) {
+    if (rows > 4 && mfma_ok) {
         p.path = PATH_MFMA;
         // 16-row tiles
         if (kind == LK_QKV)
@@ -156,20 +160,16 @@ Plan make_plan(const sd_model *m, LinearKind kind, bool multi) {
             p.n_tiles = cdiv(c.ffn_dim, 8);
         else
             p.n_tiles = cdiv(p.N, 16);
-        // norm consumers convert each activation once for two tiles
-        const int TN = (kind == LK_O || kind == LK_DOWN) ? 1 : 2;
+        // Four 16-row tiles per work-group where N is large, two for the
+        // d_model-wide output projections (more work-groups); four waves
+        // split the reduction dimension.
+        const int TN = (kind == LK_O || kind == LK_DOWN) ? 2 : 4;
         p.rows = 16 * TN;
-        const int groups = cdiv(p.n_tiles, TN);
-        const int ks = p.K / 128;
-        int splits = 1;
-        if (kind != LK_HEAD) {
-            const int want = cdiv(1536, groups);
-            splits = std::max(1, std::min(want, ks / 8));
-        }
-        p.splits = splits;
+        const int nw = 4;
+        p.waves = nw;
         return p;
     }
-    p.path = multi ? PATH_VALU16 : PATH_GEMV;
+    p.path = !multi ? PATH_GEMV : (rows <= 4 ? PATH_VALU4 : PATH_VALU16);
     if (kind == LK_QKV) {
         p.rows = qkv_gemv_rows(c.head_dim);
         p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
@@ -184,13 +184,6 @@ Plan make_plan(const sd_model *m, LinearKind kind, bool multi) {
         p.n_tiles = cdiv(p.N, 4);
     }
     return p;
-}
-
-size_t part_floats(const Plan &p) {
-    if (p.path != PATH_MFMA || p.splits <= 1)
-        return 0;
-    const int TN = p.rows / 16;
-    return (size_t)cdiv(p.n_tiles, TN) * p.splits * (TN * 256 + 16);
 }
 
 int head_tiles(const Plan &p) { return p.n_tiles; }
@@ -277,23 +270,42 @@ sd_status launch(hipError_t e, const char *what) {
     return SD_OK;
 }
 
+// One linear layer.  X (float32, with the RMSNorm gain folded in by the
+// VALU kernels) feeds the VALU paths; the MFMA path reads the bf16 hi/lo
+// pair xs (already normalised by k_prep_norm or split by the producer).
 sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, int64_t ldx, const void *gain,
-                     const EpiArgs &epi) {
+                     const EpiArgs &epi, const uint16_t *xs_h = nullptr, const uint16_t *xs_l = nullptr) {
     LinearArgs a{};
     a.W = W;
     a.N = p.N;
     a.K = p.K;
-    a.X = X;
-    a.ldx = ldx;
-    a.gain = gain;
+    if (p.path == PATH_MFMA) {
+        a.Xh = xs_h;
+        a.Xl = xs_l;
+        a.ldx = m->xld;
+    } else {
+        a.X = X;
+        a.ldx = ldx;
+        a.gain = gain;
+    }
     a.eps = m->cfg.rms_eps;
     a.ctl = m->ctl;
     a.epi = epi;
-    a.part = m->part;
-    a.tile_counter = m->tile_counter;
-    a.splits = p.splits;
+    a.waves = p.waves;
     a.n_tiles = p.n_tiles;
-    return launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer");
+    SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer"));
+    if (p.epi == EPI_HEAD)
+        SD_TRY(launch(launch_head_finalize(a, p.n_tiles, m->stream), "head finalize"));
+    return SD_OK;
+}
+
+// RMSNorm of h with gain into the hi/lo pair a (MFMA path only).
+sd_status prep_norm(sd_model *m, const Plan &p, const void *gain) {
+    if (p.path != PATH_MFMA)
+        return SD_OK;
+    return launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa_h,
+                                   m->xa_l, m->xld, m->stream),
+                  "norm");
 }
 
 struct HeadSpec {
@@ -303,10 +315,12 @@ struct HeadSpec {
 };
 
 // One decoder forward over the rows described by the device control block.
-// multi selects the up-to-16-row kernels; skip is a host mask or null.
-sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, bool multi, const HeadSpec &hs) {
+// max_rows (known to the host) bounds the row count and picks the kernels;
+// skip is a host mask or null.
+sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
+                          const HeadSpec &hs) {
     const sd_config &c = m->cfg;
-    const Plan *P = multi ? m->planm : m->plan1;
+    const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 4 ? m->plan4 : m->planm);
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
@@ -326,7 +340,8 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             e.n_kv_heads = c.n_kv_heads;
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
-            SD_TRY(run_linear(m, P[LK_QKV], m->w_qkv[l], m->h, ldh, m->attn_norm[l], e));
+            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l]));
+            SD_TRY(run_linear(m, P[LK_QKV], m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa_h, m->xa_l));
             AttnArgs at{};
             at.q = m->q;
             at.ld_q = ldq;
@@ -337,6 +352,11 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             at.part_ml = m->attn_ml;
             at.out = m->o;
             at.ld_out = ldq;
+            if (P[LK_O].path == PATH_MFMA) {
+                at.out_hi = m->xa_h;
+                at.out_lo = m->xa_l;
+                at.ld_out = m->xld;
+            }
             at.n_heads = c.n_heads;
             at.n_kv_heads = c.n_kv_heads;
             at.head_dim = c.head_dim;
@@ -346,18 +366,24 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             EpiArgs eo{};
             eo.out = m->h;
             eo.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_O], m->w_o[l], m->o, ldq, nullptr, eo));
+            SD_TRY(run_linear(m, P[LK_O], m->w_o[l], m->o, ldq, nullptr, eo, m->xa_h, m->xa_l));
         }
         if (!(skip && skip[2 * l + 1])) {
             EpiArgs eg{};
             eg.out = m->mbuf;
             eg.ld_out = c.ffn_dim;
             eg.ffn = c.ffn_dim;
-            SD_TRY(run_linear(m, P[LK_GATE_UP], m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg));
+            if (P[LK_DOWN].path == PATH_MFMA) {
+                eg.out_hi = m->xb_h;
+                eg.out_lo = m->xb_l;
+                eg.ld_out = m->xld;
+            }
+            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l]));
+            SD_TRY(run_linear(m, P[LK_GATE_UP], m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa_h, m->xa_l));
             EpiArgs ed{};
             ed.out = m->h;
             ed.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_DOWN], m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed));
+            SD_TRY(run_linear(m, P[LK_DOWN], m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb_h, m->xb_l));
         }
     }
     if (hs.run) {
@@ -366,13 +392,13 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.logits = hs.logits;
         eh.head.ld_logits = c.vocab;
         eh.head.partials = m->head_part;
-        eh.head.counter = m->head_counter;
         eh.head.st = m->st;
         eh.head.mb = m->mb_dev;
         eh.head.out_tokens = m->d_out;
         eh.head.stage_log = m->d_log;
         eh.head.stage_log_cap = m->d_log_cap / 2;
-        SD_TRY(run_linear(m, P[LK_HEAD], m->lm_head, m->h, ldh, m->final_norm, eh));
+        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm));
+        SD_TRY(run_linear(m, P[LK_HEAD], m->lm_head, m->h, ldh, m->final_norm, eh, m->xa_h, m->xa_l));
     }
     return SD_OK;
 }
@@ -419,6 +445,8 @@ sd_status check_mask(const sd_model *m, const uint8_t *skip) {
 sd_status create_cache(sd_model *m, int32_t cap, void *buf, sd_kv_cache **out) {
     if (cap < 1)
         return fail(SD_ERR_INVALID_ARG, "capacity must be >= 1");
+    if (cap > MAX_SPLITS * ATTN_CHUNK)
+        return fail(SD_ERR_CAPACITY, "capacity above " + std::to_string(MAX_SPLITS * ATTN_CHUNK) + " positions");
     if (buf && !aligned16(buf))
         return fail(SD_ERR_INVALID_ARG, "cache buffer must be 16-byte aligned");
     SD_TRY(ensure_rope(m, cap));
@@ -460,7 +488,7 @@ sd_status enqueue_prefill(sd_model *m, sd_kv_cache *kc, const int32_t *dev_token
     for (int32_t c = 0; c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
         SD_TRY(launch(launch_set_ctl(m->ctl, start + c, rows, dev_tokens + c, m->stream), "control block"));
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, rows > 1, HeadSpec{}));
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, rows, HeadSpec{}));
     }
     return SD_OK;
 }
@@ -579,7 +607,8 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
     int32_t seq = 0;
     double draft_ms = 0.0, verify_ms = 0.0;
     int prev_phase = -1;
-    int cur = 0;  // event pair in use: ev[2 + 2 cur], ev[3 + 2 cur]
+    int cur = 0;       // event pair in use: ev[2 + 2 cur], ev[3 + 2 cur]
+    int stage_k = 0;   // drafts of the current stage, counted from the mailbox
     while (!done) {
         hipEvent_t e0 = m->ev[2 + 2 * cur], e1 = m->ev[3 + 2 * cur];
         SD_HIP(hipEventRecord(e0, m->stream));
@@ -587,10 +616,12 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
         hs.run = true;
         if (phase == PHASE_DRAFT) {
             hs.mode = HEAD_DRAFT;
-            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, false, hs));
+            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, 1, hs));
+            ++stage_k;
         } else {
             hs.mode = HEAD_VERIFY;
-            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, true, hs));
+            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, stage_k + 1, hs));
+            stage_k = 0;
         }
         SD_HIP(hipEventRecord(e1, m->stream));
         ++seq;
@@ -630,7 +661,7 @@ sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     hs.run = true;
     hs.mode = HEAD_AR;
     for (int32_t i = 0; i < max_new; ++i)
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, false, hs));
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, 1, hs));
     SD_HIP(hipEventRecord(m->ev[2], m->stream));
     SD_TRY(copy_results(m, max_new, out_tokens, stats));
     if (stats) {
@@ -668,7 +699,7 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
         hs.run = logits != nullptr;
         hs.mode = HEAD_NONE;
         hs.logits = logits ? logits + (size_t)c * m->cfg.vocab : nullptr;
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, rows > 1, hs));
+        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, rows, hs));
     }
     SD_HIP(hipStreamSynchronize(m->stream));
     kc->len += n;
@@ -685,10 +716,11 @@ void destroy_model(sd_model *m) {
     dev_free(m->q);
     dev_free(m->o);
     dev_free(m->mbuf);
-    dev_free(m->part);
-    dev_free(m->tile_counter);
+    dev_free(m->xa_h);
+    dev_free(m->xa_l);
+    dev_free(m->xb_h);
+    dev_free(m->xb_l);
     dev_free(m->head_part);
-    dev_free(m->head_counter);
     dev_free(m->attn_o);
     dev_free(m->attn_ml);
     dev_free(m->rope);
@@ -739,14 +771,12 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     m->w_down.assign(w->w_down, w->w_down + L);
     m->stream = reinterpret_cast<hipStream_t>(stream);
 
-    size_t part = 0;
-    int max_groups = 1, max_head_tiles = 1;
+    int max_head_tiles = 1;
     for (int k = 0; k < LK_COUNT; ++k) {
-        m->plan1[k] = make_plan(m, (LinearKind)k, false);
-        m->planm[k] = make_plan(m, (LinearKind)k, true);
-        for (const Plan *p : {&m->plan1[k], &m->planm[k]}) {
-            part = std::max(part, part_floats(*p));
-            max_groups = std::max(max_groups, p->n_tiles);
+        m->plan1[k] = make_plan(m, (LinearKind)k, 1);
+        m->plan4[k] = make_plan(m, (LinearKind)k, 4);
+        m->planm[k] = make_plan(m, (LinearKind)k, 16);
+        for (const Plan *p : {&m->plan1[k], &m->plan4[k], &m->planm[k]}) {
             if (k == LK_HEAD)
                 max_head_tiles = std::max(max_head_tiles, head_tiles(*p));
         }
@@ -761,10 +791,12 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->q, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
     chain(dev_alloc(&m->o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
     chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
-    chain(dev_alloc(&m->part, part));
-    chain(dev_alloc(&m->tile_counter, (size_t)max_groups));
+    m->xld = std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
+    chain(dev_alloc(&m->xa_h, (size_t)MAX_ROWS * m->xld));
+    chain(dev_alloc(&m->xa_l, (size_t)MAX_ROWS * m->xld));
+    chain(dev_alloc(&m->xb_h, (size_t)MAX_ROWS * m->xld));
+    chain(dev_alloc(&m->xb_l, (size_t)MAX_ROWS * m->xld));
     chain(dev_alloc(&m->head_part, (size_t)max_head_tiles * MAX_ROWS));
-    chain(dev_alloc(&m->head_counter, 1));
     chain(dev_alloc(&m->ctl, 1));
     chain(dev_alloc(&m->st, 1));
     if (st != SD_OK) {
@@ -787,10 +819,9 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
             destroy_model(m);
             return fail(SD_ERR_DEVICE, "event creation failed");
         }
-    // self-resetting counters and scratch start at zero
-    if (hipMemsetAsync(m->tile_counter, 0, sizeof(int32_t) * (size_t)max_groups, m->stream) != hipSuccess ||
-        hipMemsetAsync(m->head_counter, 0, sizeof(int32_t), m->stream) != hipSuccess ||
-        hipMemsetAsync(m->h, 0, sizeof(float) * (size_t)MAX_ROWS * c.d_model, m->stream) != hipSuccess ||
+    // activations start at zero (rows beyond the current forward are read
+    // as zeros by the 16-row kernels' padding lanes only through masks)
+    if (hipMemsetAsync(m->h, 0, sizeof(float) * (size_t)MAX_ROWS * c.d_model, m->stream) != hipSuccess ||
         hipMemsetAsync(m->mbuf, 0, sizeof(float) * (size_t)MAX_ROWS * c.ffn_dim, m->stream) != hipSuccess ||
         hipMemsetAsync(m->o, 0, sizeof(float) * (size_t)MAX_ROWS * c.n_heads * c.head_dim, m->stream) !=
             hipSuccess ||

@@ -14,6 +14,8 @@ constexpr int MAX_ROWS = 16;
 constexpr int ATTN_CHUNK = 64;
 // Largest head_dim the attention kernel stages in LDS.
 constexpr int MAX_HEAD_DIM = 128;
+// Most key chunks one attention call combines: 65536 positions.
+constexpr int MAX_SPLITS = 1024;
 
 // Where and what the current forward computes.  Device resident: the
 // greedy head of one step writes the control block of the next step, so
@@ -59,7 +61,6 @@ struct HeadArgs {
     float *logits;       // optional float32 [m][ld_logits]
     int64_t ld_logits;
     float4 *partials;    // [n_tiles][MAX_ROWS]: (max, argmax bits, sum exp(l - max), 0)
-    int32_t *counter;    // one self-resetting counter
     DevState *st;
     Mailbox *mb;         // device view of the pinned mailbox (HEAD_DRAFT / HEAD_VERIFY)
     int32_t *out_tokens;
@@ -70,6 +71,7 @@ struct HeadArgs {
 struct EpiArgs {
     float *out;            // STORE/RESID: [m][ld_out]; SWIGLU: [m][ffn]
     int64_t ld_out;
+    uint16_t *out_hi, *out_lo;  // SWIGLU: when set, the output as split bf16 hi/lo [m][ld_out]
     float *q;              // QKV: rotated queries [m][n_heads * head_dim]
     int64_t ld_q;
     void *kcache, *vcache; // QKV: this layer's K and V: [n_kv_heads][cap][head_dim]
@@ -82,15 +84,14 @@ struct EpiArgs {
 struct LinearArgs {
     const void *W;         // [N][K] row-major, weight dtype
     int32_t N, K;
-    const float *X;        // activations [m][ldx] float32
+    const float *X;        // VALU paths: activations [m][ldx] float32
+    const uint16_t *Xh, *Xl;  // MFMA path: activations split into bf16 hi/lo [m][ldx]
     int64_t ldx;
     const void *gain;      // RMSNorm gain [K] (weight dtype), or null: no norm
     float eps;
     const DevCtl *ctl;
     EpiArgs epi;
-    float *part;           // split-K partial tiles
-    int32_t *tile_counter; // one self-resetting counter per work-group column of tiles
-    int32_t splits;
+    int32_t waves;         // MFMA path: waves per work-group splitting the reduction
     int32_t n_tiles;       // tiles in the layer (set by launch_linear)
 };
 
@@ -102,17 +103,23 @@ struct AttnArgs {
     float *part_o;         // [splits][n_heads][MAX_ROWS][head_dim]
     float2 *part_ml;       // [splits][n_heads][MAX_ROWS]: (running max, sum of exp)
     float *out;            // [m][n_heads * head_dim]
+    uint16_t *out_hi, *out_lo;  // when set, the output as split bf16 hi/lo instead
     int64_t ld_out;
     int32_t n_heads, n_kv_heads, head_dim, splits;
     const DevCtl *ctl;
 };
 
 // Kernel paths of the linear layers.
-enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2 };
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3 };
 
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s);
+// Normalised (gain != null) or plain copy of h split into bf16 hi/lo for the MFMA path.
+hipError_t launch_prep_norm(const float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
+                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, hipStream_t s);
+// After a head linear: combines its n_tiles partials and takes the decoding decision.
+hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);
