@@ -43,8 +43,9 @@ typedef enum {
 typedef enum { SD_F32 = 0, SD_BF16 = 1 } sd_dtype;
 
 /* Model shape (the LLaMA-2 family the paper evaluates, Sec. 4.1).
- * head_dim must be even; n_heads a multiple of n_kv_heads (grouped-query
- * attention when they differ).  dtype is the storage type of every weight
+ * d_model and ffn_dim are multiples of 8; head_dim is a power of two in
+ * [16, 128]; n_heads is a multiple of n_kv_heads (grouped-query attention
+ * when they differ).  dtype is the storage type of every weight
  * and of the KV cache; activations and accumulations are float32. */
 typedef struct {
     int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;

@@ -44,62 +44,56 @@ __device__ __forceinline__ float wave_add(float v) {
     return v;
 }
 
-// Work-group (split, kv head g): keys [split * CH, split * CH + CH) of head
-// g are staged in LDS in the cache's storage type; the queries of the g-th
-// head group, all rows, attend to them 16 query vectors at a time.  Each
-// (query, split) leaves a partial softmax state (max, sum of exp,
-// unnormalised output).  The last work-group of head group g to finish
-// (counted by a self-resetting counter) combines the splits of every query
-// in split order, so the result is deterministic.
-template <typename TK>
-struct KvLds;
-template <>
-struct KvLds<uint16_t> {
-    static constexpr int PAD = 8;
-    __device__ static void load8(const uint16_t *src, uint16_t *dst) {
-        *reinterpret_cast<u32x4_t *>(dst) = *reinterpret_cast<const u32x4_t *>(src);
-    }
-    __device__ static void read8(const uint16_t *p, float *v) {
-        const u32x4_t w = *reinterpret_cast<const u32x4_t *>(p);
+// One wave per (key chunk of CH keys, kv head g): flash-decoding without
+// LDS or barriers.  Lanes form 4 groups of 16; group j holds keys j, j + 4,
+// ..., j + CH - 4 of the chunk, and lane e16 of a group holds head_dim / 16
+// consecutive elements of q, K and V, so each K or V row is one coalesced
+// load by 16 lanes.  All K and V of the chunk are loaded into registers up
+// front; every group then scores its 16 keys for up to QB query vectors,
+// and the four groups' softmax states are merged by shuffles.  The chunk
+// leaves a partial state per (query, split) for the ordered combine.
+template <typename TK, int ED>
+struct KvFrag {
+    float v[ED];
+    __device__ __forceinline__ void load(const TK *p, bool ok) {
+        if (!ok) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            v[2 * j] = __uint_as_float(w[j] << 16);
-            v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+            for (int e = 0; e < ED; ++e)
+                v[e] = 0.0f;
+            return;
+        }
+        if constexpr (sizeof(TK) == 2) {
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                v[e] = __uint_as_float(((uint32_t)reinterpret_cast<const uint16_t *>(p)[e]) << 16);
+        } else {
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                v[e] = reinterpret_cast<const float *>(p)[e];
         }
     }
-    __device__ static float read1(const uint16_t *p) { return __uint_as_float(((uint32_t)*p) << 16); }
+    __device__ __forceinline__ float at(int e) const { return v[e]; }
 };
+// bf16 rows of 8 elements stay packed (16 bytes) until used
 template <>
-struct KvLds<float> {
-    static constexpr int PAD = 4;
-    __device__ static void load8(const float *src, float *dst) {
-        reinterpret_cast<f32x4_t *>(dst)[0] = reinterpret_cast<const f32x4_t *>(src)[0];
-        reinterpret_cast<f32x4_t *>(dst)[1] = reinterpret_cast<const f32x4_t *>(src)[1];
+struct KvFrag<uint16_t, 8> {
+    u32x4_t w;
+    __device__ __forceinline__ void load(const uint16_t *p, bool ok) {
+        w = ok ? *reinterpret_cast<const u32x4_t *>(p) : u32x4_t{0u, 0u, 0u, 0u};
     }
-    __device__ static void read8(const float *p, float *v) {
-        const f32x4_t a = reinterpret_cast<const f32x4_t *>(p)[0];
-        const f32x4_t b = reinterpret_cast<const f32x4_t *>(p)[1];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            v[j] = a[j];
-            v[4 + j] = b[j];
-        }
+    __device__ __forceinline__ float at(int e) const {
+        const uint32_t x = w[e >> 1];
+        return __uint_as_float((e & 1) ? (x & 0xffff0000u) : (x << 16));
     }
-    __device__ static float read1(const float *p) { return *p; }
 };
 
-template <typename TK>
+template <typename TK, int ED>
 __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
     constexpr int CH = ATTN_CHUNK;
-    constexpr int DMAX = MAX_HEAD_DIM;
-    constexpr int KS = DMAX + KvLds<TK>::PAD;
-    __shared__ __attribute__((aligned(16))) TK Ks[CH * KS];
-    __shared__ __attribute__((aligned(16))) TK Vs[CH * DMAX];
-    __shared__ __attribute__((aligned(16))) float Qs[16][DMAX];
-    __shared__ float Ss[16][CH];
-    __shared__ float2 MLs[16];
-    const int split = blockIdx.x, g = blockIdx.y;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int KPG = CH / 4;  // keys per lane group
+    constexpr int QB = 4;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int split = blockIdx.x * 4 + wave, g = blockIdx.y;
     const int pos = a.ctl->pos, M = a.ctl->m;
     const int ctx = pos + M;
     const int c0 = split * CH;
@@ -109,87 +103,258 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
     const int dh = a.head_dim, H = a.n_heads;
     const int G = H / a.n_kv_heads;
     const int Q = G * M;
-
-    const TK *Kg = reinterpret_cast<const TK *>(a.kcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh;
-    const TK *Vg = reinterpret_cast<const TK *>(a.vcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh;
-    const int d8 = dh >> 3;
-    for (int i = tid; i < nk * d8; i += 256) {
-        const int key = i / d8, e = (i - key * d8) * 8;
-        KvLds<TK>::load8(Kg + (int64_t)key * dh + e, &Ks[key * KS + e]);
-        KvLds<TK>::load8(Vg + (int64_t)key * dh + e, &Vs[key * DMAX + e]);
-    }
+    const int ks = lane >> 4, e16 = lane & 15;
+    const TK *Kg = reinterpret_cast<const TK *>(a.kcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh + e16 * ED;
+    const TK *Vg = reinterpret_cast<const TK *>(a.vcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh + e16 * ED;
     const float scale = 1.0f / sqrtf((float)dh);
 
-    for (int qg = 0; qg < Q; qg += 16) {
-        const int nq = min(16, Q - qg);
-        __syncthreads();
-        for (int i = tid; i < nq * dh; i += 256) {
-            const int qi = i / dh, e = i - qi * dh;
-            const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
-            Qs[qi][e] = a.q[(int64_t)r * a.ld_q + (int64_t)head * dh + e] * scale;
-        }
-        __syncthreads();
-        // scores: thread (key c, query lane ql) takes queries ql, ql + 4, ...
-        {
-            const int c = tid & (CH - 1), ql = tid >> 6;
-            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (c < nk && ql < nq) {
-                for (int e = 0; e < dh; e += 8) {
-                    float kv[8];
-                    KvLds<TK>::read8(&Ks[c * KS + e], kv);
+    KvFrag<TK, ED> kf[KPG], vf[KPG];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int qi = ql + 4 * u;
-                        if (qi < nq) {
-                            const float4 q0 = *reinterpret_cast<const float4 *>(&Qs[qi][e]);
-                            const float4 q1 = *reinterpret_cast<const float4 *>(&Qs[qi][e + 4]);
-                            float s = acc[u];
-                            s = fmaf(q0.x, kv[0], s);
-                            s = fmaf(q0.y, kv[1], s);
-                            s = fmaf(q0.z, kv[2], s);
-                            s = fmaf(q0.w, kv[3], s);
-                            s = fmaf(q1.x, kv[4], s);
-                            s = fmaf(q1.y, kv[5], s);
-                            s = fmaf(q1.z, kv[6], s);
-                            s = fmaf(q1.w, kv[7], s);
-                            acc[u] = s;
-                        }
-                    }
+    for (int j = 0; j < KPG; ++j) {
+        const int c = ks + 4 * j;
+        kf[j].load(Kg + (int64_t)c * dh, c < nk);
+        vf[j].load(Vg + (int64_t)c * dh, c < nk);
+    }
+
+    for (int qg = 0; qg < Q; qg += QB) {
+        const int nq = min(QB, Q - qg);
+#pragma unroll
+        for (int qi = 0; qi < QB; ++qi) {
+            if (qi >= nq)
+                break;
+            const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
+            const float *qs = a.q + (int64_t)r * a.ld_q + (int64_t)head * dh + e16 * ED;
+            float qv[ED];
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                qv[e] = qs[e] * scale;
+            const int lim = pos + r - c0;  // last key row r sees, relative to the chunk
+            float s[KPG];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < KPG; ++j) {
+                float t = 0.0f;
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    t = fmaf(qv[e], kf[j].at(e), t);
+                t += __shfl_xor(t, 1, 64);
+                t += __shfl_xor(t, 2, 64);
+                t += __shfl_xor(t, 4, 64);
+                t += __shfl_xor(t, 8, 64);
+                const int c = ks + 4 * j;
+                s[j] = (c < nk && c <= lim) ? t : -INFINITY;
+                mx = fmaxf(mx, s[j]);
+            }
+            float l = 0.0f, o[ED];
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                o[e] = 0.0f;
+            if (mx != -INFINITY) {
+#pragma unroll
+                for (int j = 0; j < KPG; ++j) {
+                    const float p = expf(s[j] - mx);
+                    l += p;
+#pragma unroll
+                    for (int e = 0; e < ED; ++e)
+                        o[e] = fmaf(p, vf[j].at(e), o[e]);
                 }
             }
+            // merge the four key groups
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int qi = ql + 4 * u;
-                if (qi < nq) {
-                    const int r = (qg + qi) / G;
-                    Ss[qi][c] = (c < nk && c0 + c <= pos + r) ? acc[u] : -INFINITY;
+            for (int x = 16; x <= 32; x <<= 1) {
+                const float m2 = __shfl_xor(mx, x, 64), l2 = __shfl_xor(l, x, 64);
+                float o2[ED];
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    o2[e] = __shfl_xor(o[e], x, 64);
+                const float mn = fmaxf(mx, m2);
+                if (mn != -INFINITY) {
+                    const float wa = expf(mx - mn), wb = expf(m2 - mn);
+                    l = l * wa + l2 * wb;
+#pragma unroll
+                    for (int e = 0; e < ED; ++e)
+                        o[e] = o[e] * wa + o2[e] * wb;
+                    mx = mn;
                 }
             }
+            if (ks == 0) {
+                const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    a.part_o[slot * dh + e16 * ED + e] = o[e];
+                if (e16 == 0)
+                    a.part_ml[slot] = make_float2(mx, l);
+            }
         }
-        __syncthreads();
-        for (int qi = wave; qi < nq; qi += 4) {
-            const float v = Ss[qi][lane];
-            const float mx = wave_max(v);
-            const float e = (mx == -INFINITY) ? 0.0f : expf(v - mx);
-            const float l = wave_add(e);
-            Ss[qi][lane] = e;
-            if (lane == 0)
-                MLs[qi] = make_float2(mx, l);
+    }
+}
+
+// Decode attention without a combine pass: one work-group of HW waves per
+// kv head, for up to QH query vectors (the draft, autoregressive and short
+// verification steps of multi-head attention).  Wave w takes the 16-key
+// blocks w, w + HW, ...; within a block, lane group j (16 lanes) takes keys
+// j, j + 4, j + 8, j + 12 and lane e16 holds head_dim / 16 elements.  Each
+// group keeps an online-softmax state; the block after next is loaded while
+// the current one is used.  The groups merge by shuffles, the waves in LDS
+// in wave order, and the result goes straight to the output.
+constexpr int QH = 4;
+constexpr int HW = 8;
+
+template <typename TK, int ED>
+__global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
+    __shared__ float wst[HW][QH][2];
+    __shared__ float wo[HW][QH][MAX_HEAD_DIM];
+    const int g = blockIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int pos = a.ctl->pos, M = a.ctl->m;
+    const int ctx = pos + M;
+    const int dh = a.head_dim, H = a.n_heads;
+    const int G = H / a.n_kv_heads;
+    const int nq = G * M;  // <= QH, checked by the host
+    const int ks = lane >> 4, e16 = lane & 15;
+    const TK *Kg = reinterpret_cast<const TK *>(a.kcache) + (int64_t)g * a.kv_head_stride + e16 * ED;
+    const TK *Vg = reinterpret_cast<const TK *>(a.vcache) + (int64_t)g * a.kv_head_stride + e16 * ED;
+    const float scale = 1.0f / sqrtf((float)dh);
+
+    float qv[QH][ED], o[QH][ED], mr[QH], lr[QH];
+    int lim[QH];
+#pragma unroll
+    for (int qi = 0; qi < QH; ++qi) {
+        mr[qi] = -INFINITY;
+        lr[qi] = 0.0f;
+        lim[qi] = -1;
+#pragma unroll
+        for (int e = 0; e < ED; ++e) {
+            qv[qi][e] = 0.0f;
+            o[qi][e] = 0.0f;
         }
-        __syncthreads();
-        for (int i = tid; i < nq * dh; i += 256) {
-            const int qi = i / dh, e = i - qi * dh;
-            float acc = 0.0f;
-            for (int c = 0; c < nk; ++c)
-                acc = fmaf(Ss[qi][c], KvLds<TK>::read1(&Vs[c * DMAX + e]), acc);
-            const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
-            const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
-            a.part_o[slot * dh + e] = acc;
-            if (e == 0)
-                a.part_ml[slot] = MLs[qi];
+        if (qi < nq) {
+            const int r = qi / G, head = g * G + (qi - r * G);
+            const float *qs = a.q + (int64_t)r * a.ld_q + (int64_t)head * dh + e16 * ED;
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                qv[qi][e] = qs[e] * scale;
+            lim[qi] = pos + r;
         }
     }
 
+    const int nblk = (ctx + 15) >> 4;
+    KvFrag<TK, ED> kc[4], vc[4], kn[4], vn[4];
+    auto load_blk = [&](int b, KvFrag<TK, ED>(&kk)[4], KvFrag<TK, ED>(&vv)[4]) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int c = b * 16 + ks + 4 * jj;
+            const bool ok = b < nblk && c < ctx;
+            kk[jj].load(Kg + (int64_t)(ok ? c : 0) * dh, ok);
+            vv[jj].load(Vg + (int64_t)(ok ? c : 0) * dh, ok);
+        }
+    };
+    load_blk(wave, kc, vc);
+    for (int b = wave; b < nblk; b += HW) {
+        load_blk(b + HW, kn, vn);
+#pragma unroll
+        for (int qi = 0; qi < QH; ++qi) {
+            if (qi >= nq)
+                break;
+            float s[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                float t = 0.0f;
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    t = fmaf(qv[qi][e], kc[jj].at(e), t);
+                t += __shfl_xor(t, 1, 64);
+                t += __shfl_xor(t, 2, 64);
+                t += __shfl_xor(t, 4, 64);
+                t += __shfl_xor(t, 8, 64);
+                const int c = b * 16 + ks + 4 * jj;
+                s[jj] = (c < ctx && c <= lim[qi]) ? t : -INFINITY;
+                mx = fmaxf(mx, s[jj]);
+            }
+            const float mn = fmaxf(mr[qi], mx);
+            if (mn != -INFINITY) {
+                const float so = expf(mr[qi] - mn);
+                float l = lr[qi] * so;
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    o[qi][e] *= so;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const float p = expf(s[jj] - mn);
+                    l += p;
+#pragma unroll
+                    for (int e = 0; e < ED; ++e)
+                        o[qi][e] = fmaf(p, vc[jj].at(e), o[qi][e]);
+                }
+                lr[qi] = l;
+                mr[qi] = mn;
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            kc[jj] = kn[jj];
+            vc[jj] = vn[jj];
+        }
+    }
+    // merge the four lane groups, then the waves
+#pragma unroll
+    for (int qi = 0; qi < QH; ++qi) {
+        if (qi >= nq)
+            break;
+#pragma unroll
+        for (int x = 16; x <= 32; x <<= 1) {
+            const float m2 = __shfl_xor(mr[qi], x, 64), l2 = __shfl_xor(lr[qi], x, 64);
+            float o2[ED];
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                o2[e] = __shfl_xor(o[qi][e], x, 64);
+            const float mn = fmaxf(mr[qi], m2);
+            if (mn != -INFINITY) {
+                const float wa = expf(mr[qi] - mn), wb = expf(m2 - mn);
+                lr[qi] = lr[qi] * wa + l2 * wb;
+#pragma unroll
+                for (int e = 0; e < ED; ++e)
+                    o[qi][e] = o[qi][e] * wa + o2[e] * wb;
+                mr[qi] = mn;
+            }
+        }
+        if (ks == 0) {
+#pragma unroll
+            for (int e = 0; e < ED; ++e)
+                wo[wave][qi][e16 * ED + e] = o[qi][e];
+            if (e16 == 0) {
+                wst[wave][qi][0] = mr[qi];
+                wst[wave][qi][1] = lr[qi];
+            }
+        }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < nq * dh; t += HW * 64) {
+        const int qi = t / dh, e = t - qi * dh;
+        float mx = -INFINITY;
+        for (int w = 0; w < HW; ++w)
+            mx = fmaxf(mx, wst[w][qi][0]);
+        float L = 0.0f, O = 0.0f;
+        for (int w = 0; w < HW; ++w) {
+            const float m = wst[w][qi][0];
+            if (m == -INFINITY)
+                continue;
+            const float wgt = expf(m - mx);
+            L = fmaf(wgt, wst[w][qi][1], L);
+            O = fmaf(wgt, wo[w][qi][e], O);
+        }
+        const int r = qi / G, head = g * G + (qi - r * G);
+        const float y = O / L;
+        const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
+        if (a.out_hi) {
+            const uint32_t bits = __float_as_uint(y);
+            a.out_hi[oi] = (uint16_t)(bits >> 16);
+            a.out_lo[oi] = (uint16_t)(__float_as_uint(y - __uint_as_float(bits & 0xffff0000u)) >> 16);
+        } else {
+            a.out[oi] = y;
+        }
+    }
 }
 
 // Ordered combine of the split partials of one (head, row): deterministic.
@@ -249,14 +414,61 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
     }
 }
 
-hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s) {
-    if (a.head_dim > MAX_HEAD_DIM || (a.head_dim & 7) || a.splits > MAX_SPLITS)
+template <typename TK>
+static hipError_t launch_attn_split(const AttnArgs &a, hipStream_t s) {
+    dim3 grid((a.splits + 3) / 4, a.n_kv_heads), block(256);
+    switch (a.head_dim) {
+    case 16:
+        hipLaunchKernelGGL((k_attn_split<TK, 1>), grid, block, 0, s, a);
+        break;
+    case 32:
+        hipLaunchKernelGGL((k_attn_split<TK, 2>), grid, block, 0, s, a);
+        break;
+    case 64:
+        hipLaunchKernelGGL((k_attn_split<TK, 4>), grid, block, 0, s, a);
+        break;
+    case 128:
+        hipLaunchKernelGGL((k_attn_split<TK, 8>), grid, block, 0, s, a);
+        break;
+    default:
         return hipErrorInvalidValue;
-    dim3 grid(a.splits, a.n_kv_heads), block(256);
-    if (bf16)
-        hipLaunchKernelGGL(k_attn_split<uint16_t>, grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL(k_attn_split<float>, grid, block, 0, s, a);
+    }
+    return hipSuccess;
+}
+
+template <typename TK>
+static hipError_t launch_attn_head(const AttnArgs &a, hipStream_t s) {
+    dim3 grid(a.n_kv_heads), block(HW * 64);
+    switch (a.head_dim) {
+    case 16:
+        hipLaunchKernelGGL((k_attn_head<TK, 1>), grid, block, 0, s, a);
+        break;
+    case 32:
+        hipLaunchKernelGGL((k_attn_head<TK, 2>), grid, block, 0, s, a);
+        break;
+    case 64:
+        hipLaunchKernelGGL((k_attn_head<TK, 4>), grid, block, 0, s, a);
+        break;
+    case 128:
+        hipLaunchKernelGGL((k_attn_head<TK, 8>), grid, block, 0, s, a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s) {
+    if (a.splits > MAX_SPLITS)
+        return hipErrorInvalidValue;
+    const int G = a.n_heads / a.n_kv_heads;
+    // one work-group per kv head while the context is short and the query
+    // vectors per head fit; otherwise split the keys over work-groups
+    if (G * max_rows <= QH && a.splits <= 4)
+        return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
+    const hipError_t e = bf16 ? launch_attn_split<uint16_t>(a, s) : launch_attn_split<float>(a, s);
+    if (e != hipSuccess)
+        return e;
     hipLaunchKernelGGL(k_attn_combine, dim3(a.n_heads, MAX_ROWS), dim3(128), 0, s, a);
     return hipGetLastError();
 }

@@ -7,7 +7,7 @@
 // speed), so the three main loops below are built to read each weight byte
 // exactly once with 16-byte loads:
 //   - k_linear_valu, MR == 1: the GEMV of a draft or autoregressive step;
-//   - k_linear_valu, MR == 4: verification of up to 3 drafts;
+//   - k_linear_valu, MR == 2 or 4: verification of 1 or up to 3 drafts;
 //   - k_linear_valu, MR == 16: any row count, for float32 weights;
 //   - k_linear_mfma: the verification forward over up to 16 rows (the last
 //     committed token plus the drafts, Algorithm 2), bf16 MFMA tiles with
@@ -292,7 +292,14 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                                              int M) {
     const int tid = threadIdx.x;
     const EpiArgs &e = a.epi;
-    if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+    if constexpr (EPI == EPI_PARTIAL) {
+        float *dst = a.part + (int64_t)(blockIdx.x % a.splits) * MAX_ROWS * a.N;
+        for (int j = tid; j < R * M; j += blockDim.x) {
+            const int i = j % R, m = j / R, n = t * R + i;
+            if (n < a.N)
+                dst[(int64_t)m * a.N + n] = fin[i * MR + m];
+        }
+    } else if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
         for (int j = tid; j < R * M; j += 256) {
             const int i = j % R, m = j / R, n = t * R + i;
             if (n < a.N) {
@@ -542,7 +549,8 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     __shared__ float red[NW][TN * 16][17];
     __shared__ float fin[TN * 16 * 16];
     __shared__ float inv_s[16];
-    const int grp = blockIdx.x;
+    const int S = EPI == EPI_PARTIAL ? a.splits : 1;
+    const int grp = blockIdx.x / S, sp = blockIdx.x - grp * S;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
     const int M = a.ctl->m;
@@ -558,7 +566,9 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     const uint16_t *Xh = a.Xh + (int64_t)r16 * a.ldx + kg * 8;
     const uint16_t *Xl = a.Xl + (int64_t)r16 * a.ldx + kg * 8;
     const bool xrow = r16 < M;
-    const int KS = a.K >> 7;
+    // k-steps of this split, shared out among the waves
+    const int KS_all = a.K >> 7;
+    const int ks0 = (int)(((int64_t)KS_all * sp) / S), KS = (int)(((int64_t)KS_all * (sp + 1)) / S) - ks0;
 
     floatx4_t acc[TN];
 #pragma unroll
@@ -566,7 +576,7 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         acc[j] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     // Each wave streams a contiguous range of k-steps with the weights of
     // the next k-step in flight while the current one is multiplied.
-    const int q_beg = (int)(((int64_t)KS * wave) / NW), q_end = (int)(((int64_t)KS * (wave + 1)) / NW);
+    const int q_beg = ks0 + (int)(((int64_t)KS * wave) / NW), q_end = ks0 + (int)(((int64_t)KS * (wave + 1)) / NW);
     if (q_beg < q_end) {
         u32x4_t wa[TN][4], wb[TN][4];
         mfma_load<TN>(wa, Wr, q_beg << 7);
@@ -614,50 +624,86 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 // rounded down to bf16).  One work-group per row.
 
 template <typename TW>
-__global__ __launch_bounds__(256) void k_prep_norm(const float *h, int64_t ldh, const TW *g, float eps, int K,
-                                                   const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx) {
-    __shared__ float red[4];
+__global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
+                                                    const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx,
+                                                    const float *part, int n_part) {
+    __shared__ float red[16];
     const int r = blockIdx.x;
     if (r >= ctl->m)
         return;
     const int tid = threadIdx.x;
-    const float *hr = h + (int64_t)r * ldh;
+    float4 *hr = reinterpret_cast<float4 *>(h + (int64_t)r * ldh);
+    const int K4 = K >> 2;
+    // pending split-K partials of the last output projection, added in
+    // split order; every load of an element is issued before the adds
+    float ss = 0.0f;
+    for (int k = tid; k < K4; k += 1024) {
+        float4 v = hr[k];
+        if (n_part > 0) {
+            float4 p[8];
+#pragma unroll
+            for (int sp = 0; sp < 8; ++sp)
+                if (sp < n_part)
+                    p[sp] = reinterpret_cast<const float4 *>(part + ((int64_t)sp * MAX_ROWS + r) * K)[k];
+#pragma unroll
+            for (int sp = 0; sp < 8; ++sp)
+                if (sp < n_part) {
+                    v.x += p[sp].x;
+                    v.y += p[sp].y;
+                    v.z += p[sp].z;
+                    v.w += p[sp].w;
+                }
+            hr[k] = v;
+        }
+        ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+    }
     float inv = 1.0f;
     if (g) {
-        float ss = 0.0f;
-        for (int k = tid; k < K; k += 256)
-            ss = fmaf(hr[k], hr[k], ss);
         ss = wave_sum(ss);
         if ((tid & 63) == 0)
             red[tid >> 6] = ss;
         __syncthreads();
-        inv = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
+        float t = 0.0f;
+        for (int w = 0; w < 16; ++w)
+            t += red[w];
+        inv = 1.0f / sqrtf(t / (float)K + eps);
     }
-    for (int k = tid; k < K; k += 256) {
-        float u = hr[k];
-        if (g) {
-            float gk;
-            if constexpr (sizeof(TW) == 2)
-                gk = bf2f(g[k]);
-            else
-                gk = g[k];
-            u = gk * (u * inv);
+    for (int k = tid; k < K4; k += 1024) {
+        const float4 v = hr[k];
+        float u[4] = {v.x, v.y, v.z, v.w};
+        uint16_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (g) {
+                float gk;
+                if constexpr (sizeof(TW) == 2)
+                    gk = bf2f(g[4 * k + e]);
+                else
+                    gk = g[4 * k + e];
+                u[e] = gk * (u[e] * inv);
+            }
+            split_hilo(u[e], hi[e], lo[e]);
         }
-        uint16_t hi, lo;
-        split_hilo(u, hi, lo);
-        xh[(int64_t)r * ldx + k] = hi;
-        xl[(int64_t)r * ldx + k] = lo;
+        uint2 ph, pl;
+        ph.x = hi[0] | ((uint32_t)hi[1] << 16);
+        ph.y = hi[2] | ((uint32_t)hi[3] << 16);
+        pl.x = lo[0] | ((uint32_t)lo[1] << 16);
+        pl.y = lo[2] | ((uint32_t)lo[3] << 16);
+        *reinterpret_cast<uint2 *>(xh + (int64_t)r * ldx + 4 * k) = ph;
+        *reinterpret_cast<uint2 *>(xl + (int64_t)r * ldx + 4 * k) = pl;
     }
 }
 
-hipError_t launch_prep_norm(const float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, hipStream_t s) {
+hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
+                            uint16_t *xh, uint16_t *xl, int64_t ldx, const float *part, int n_part, hipStream_t s) {
+    if ((K & 3) || (ldh & 3) || (ldx & 3) || n_part > 8)
+        return hipErrorInvalidValue;
     if (bf16)
-        hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(256), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xh, xl, ldx);
+        hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xh, xl, ldx, part, n_part);
     else
-        hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(256), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xh, xl, ldx);
+        hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xh, xl, ldx, part, n_part);
     return hipGetLastError();
 }
 
@@ -712,8 +758,13 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
 template <int TN, int NW>
 static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
     const int groups = (n_tiles + TN - 1) / TN;
-    dim3 grid(groups), block(NW * 64);
+    dim3 grid(groups * (epi == EPI_PARTIAL ? a.splits : 1)), block(NW * 64);
     switch (epi) {
+    case EPI_PARTIAL:
+        if (a.splits < 1 || !a.part)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_linear_mfma<EPI_PARTIAL, TN, NW>), grid, block, 0, s, a);
+        break;
     case EPI_STORE:
         hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, TN, NW>), grid, block, 0, s, a);
         break;
@@ -755,6 +806,8 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
         b.n_tiles = n_tiles;
         if (!a.Xh || !a.Xl)
             return hipErrorInvalidValue;
+        if (TN == 1 && NW == 4)
+            return launch_mfma<1, 4>(b, epi, n_tiles, s);
         if (TN == 1 && NW == 8)
             return launch_mfma<1, 8>(b, epi, n_tiles, s);
         if (TN == 1 && NW == 16)
@@ -777,6 +830,9 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
     if (path == PATH_VALU4)
         return bf16 ? launch_valu_r<uint16_t, 4>(a, epi, rows_per_tile, n_tiles, s)
                     : launch_valu_r<float, 4>(a, epi, rows_per_tile, n_tiles, s);
+    if (path == PATH_VALU2)
+        return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s)
+                    : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s);
     return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s)
                 : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s);
 }

@@ -54,6 +54,7 @@ struct Plan {
     int rows;     // weight rows per work-group
     int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
     int waves;    // MFMA: waves per work-group splitting the reduction
+    int splits;   // MFMA output projections: split-K partials folded by the next norm
     int N, K, epi;
 };
 
@@ -76,8 +77,9 @@ struct sd_model {
     hipStream_t stream = nullptr;
 
     Plan plan1[LK_COUNT];  // one row (draft / autoregressive step)
-    Plan plan4[LK_COUNT];  // up to 4 rows (short verification)
-    Plan planm[LK_COUNT];  // up to 16 rows (long verification, prefill)
+    Plan plan2[LK_COUNT];  // up to 2 rows (verification of one draft)
+    Plan planm[LK_COUNT];  // up to 16 rows (longer verification, prefill)
+    float *part = nullptr;  // split-K partials of the MFMA output projections
 
     float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
     // MFMA-path activations split into bf16 hi/lo, [MAX_ROWS][xld]: pair a holds
@@ -109,20 +111,27 @@ namespace {
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Tile rows for the QKV layer must hold whole rotary pairs of one head.
-int qkv_gemv_rows(int head_dim) {
+int qkv_gemv_rows(int head_dim, int want) {
     const int half = head_dim / 2;
-    for (int r : {4, 8})
+    for (int r = want; r >= 4; r /= 2)
         if (half % (r / 2) == 0)
             return r;
     return 4;
 }
 
-// rows: the largest row count the plan serves (1, 4 or 16).
+bool mfma_ok(const sd_model *m, LinearKind kind) {
+    const sd_config &c = m->cfg;
+    const int K = kind == LK_O ? c.n_heads * c.head_dim : (kind == LK_DOWN ? c.ffn_dim : c.d_model);
+    return m->bf16 && K % 128 == 0 && (kind != LK_QKV || (c.head_dim / 2) % 8 == 0);
+}
+
+// rows: the largest row count the plan serves (1, 2 or 16).  Tile sizes
+// follow measurements at the 13B shape.
 Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
-    const bool multi = rows > 1;
     const sd_config &c = m->cfg;
     Plan p{};
     p.waves = 4;
+    p.splits = 1;
     switch (kind) {
     case LK_QKV:
         p.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
@@ -150,38 +159,46 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
         p.epi = EPI_HEAD;
         break;
     }
-    const bool mfma_ok = m->bf16 && (p.K % 128 == 0) && (kind != LK_QKV || (c.head_dim / 2) % 8 == 0);
-    if (rows > 4 && mfma_ok) {
+    if (rows > 2 && mfma_ok(m, kind)) {
         p.path = PATH_MFMA;
-        // 16-row tiles
         if (kind == LK_QKV)
             p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / 8);
         else if (kind == LK_GATE_UP)
             p.n_tiles = cdiv(c.ffn_dim, 8);
         else
             p.n_tiles = cdiv(p.N, 16);
-        // Four 16-row tiles per work-group where N is large, two for the
-        // d_model-wide output projections (more work-groups); four waves
-        // split the reduction dimension.
-        const int TN = (kind == LK_O || kind == LK_DOWN) ? 2 : 4;
-        p.rows = 16 * TN;
-        const int nw = 4;
-        p.waves = nw;
+        if (kind == LK_O || kind == LK_DOWN) {
+            // Narrow outputs: two tiles per work-group and the reduction split
+            // over work-groups, the partial sums folded into the residual
+            // stream by the norm that reads it next (all readers of the
+            // residual stream must then be MFMA layers).
+            p.rows = 32;
+            const bool fold = mfma_ok(m, LK_QKV) && mfma_ok(m, LK_GATE_UP) && mfma_ok(m, LK_HEAD);
+            if (fold) {
+                p.epi = EPI_PARTIAL;
+                p.splits = p.K >= 8192 ? 8 : 4;
+            }
+        } else {
+            p.rows = 64;
+        }
         return p;
     }
-    p.path = !multi ? PATH_GEMV : (rows <= 4 ? PATH_VALU4 : PATH_VALU16);
+    p.path = rows == 1 ? PATH_GEMV : (rows <= 2 ? PATH_VALU2 : PATH_VALU16);
+    // weight rows per work-group: 8 for the wide layers of the one-row GEMV,
+    // 4 otherwise (the QKV tile also holds whole rotary pairs)
+    const int wide = rows == 1 ? 8 : 4;
     if (kind == LK_QKV) {
-        p.rows = qkv_gemv_rows(c.head_dim);
+        p.rows = qkv_gemv_rows(c.head_dim, rows <= 2 ? 8 : 4);
         p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
     } else if (kind == LK_GATE_UP) {
-        p.rows = 4;
-        p.n_tiles = cdiv(c.ffn_dim, 2);
-    } else if (kind == LK_HEAD && !multi) {
-        p.rows = 16;
-        p.n_tiles = cdiv(p.N, 16);
+        p.rows = wide;
+        p.n_tiles = cdiv(c.ffn_dim, wide / 2);
+    } else if (kind == LK_HEAD) {
+        p.rows = wide;
+        p.n_tiles = cdiv(p.N, wide);
     } else {
         p.rows = 4;
-        p.n_tiles = cdiv(p.N, 4);
+        p.n_tiles = cdiv(p.N, p.rows);
     }
     return p;
 }
@@ -292,6 +309,8 @@ sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, 
     a.ctl = m->ctl;
     a.epi = epi;
     a.waves = p.waves;
+    a.splits = p.splits;
+    a.part = m->part;
     a.n_tiles = p.n_tiles;
     SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer"));
     if (p.epi == EPI_HEAD)
@@ -299,13 +318,16 @@ sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, 
     return SD_OK;
 }
 
-// RMSNorm of h with gain into the hi/lo pair a (MFMA path only).
-sd_status prep_norm(sd_model *m, const Plan &p, const void *gain) {
+// RMSNorm of h with gain into the hi/lo pair a (MFMA path only), after
+// folding the pending split-K partials of the last output projection.
+sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
     if (p.path != PATH_MFMA)
         return SD_OK;
-    return launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa_h,
-                                   m->xa_l, m->xld, m->stream),
-                  "norm");
+    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa_h,
+                                   m->xa_l, m->xld, m->part, pending, m->stream),
+                  "norm"));
+    pending = 0;
+    return SD_OK;
 }
 
 struct HeadSpec {
@@ -320,7 +342,8 @@ struct HeadSpec {
 sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
                           const HeadSpec &hs) {
     const sd_config &c = m->cfg;
-    const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 4 ? m->plan4 : m->planm);
+    const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
+    int pending = 0;  // split-K partials not yet folded into h
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
@@ -340,7 +363,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             e.n_kv_heads = c.n_kv_heads;
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
-            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l]));
+            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l], pending));
             SD_TRY(run_linear(m, P[LK_QKV], m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa_h, m->xa_l));
             AttnArgs at{};
             at.q = m->q;
@@ -362,11 +385,13 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             at.head_dim = c.head_dim;
             at.splits = cdiv(cap, ATTN_CHUNK);
             at.ctl = m->ctl;
-            SD_TRY(launch(launch_attention(at, m->bf16, m->stream), "attention"));
+            SD_TRY(launch(launch_attention(at, m->bf16, max_rows, m->stream), "attention"));
             EpiArgs eo{};
             eo.out = m->h;
             eo.ld_out = ldh;
             SD_TRY(run_linear(m, P[LK_O], m->w_o[l], m->o, ldq, nullptr, eo, m->xa_h, m->xa_l));
+            if (P[LK_O].epi == EPI_PARTIAL)
+                pending = P[LK_O].splits;
         }
         if (!(skip && skip[2 * l + 1])) {
             EpiArgs eg{};
@@ -378,12 +403,14 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
                 eg.out_lo = m->xb_l;
                 eg.ld_out = m->xld;
             }
-            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l]));
+            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l], pending));
             SD_TRY(run_linear(m, P[LK_GATE_UP], m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa_h, m->xa_l));
             EpiArgs ed{};
             ed.out = m->h;
             ed.ld_out = ldh;
             SD_TRY(run_linear(m, P[LK_DOWN], m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb_h, m->xb_l));
+            if (P[LK_DOWN].epi == EPI_PARTIAL)
+                pending = P[LK_DOWN].splits;
         }
     }
     if (hs.run) {
@@ -397,7 +424,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.out_tokens = m->d_out;
         eh.head.stage_log = m->d_log;
         eh.head.stage_log_cap = m->d_log_cap / 2;
-        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm));
+        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending));
         SD_TRY(run_linear(m, P[LK_HEAD], m->lm_head, m->h, ldh, m->final_norm, eh, m->xa_h, m->xa_l));
     }
     return SD_OK;
@@ -412,10 +439,11 @@ sd_status check_config(const sd_config *c) {
     if (!c)
         return fail(SD_ERR_INVALID_ARG, "config is null");
     if (c->n_layers < 1 || c->d_model < 8 || c->d_model % 8 || c->n_heads < 1 || c->n_kv_heads < 1 ||
-        c->n_heads % c->n_kv_heads || c->head_dim < 8 || c->head_dim % 8 || c->head_dim > MAX_HEAD_DIM ||
+        c->n_heads % c->n_kv_heads || c->head_dim < 16 || (c->head_dim & (c->head_dim - 1)) ||
+        c->head_dim > MAX_HEAD_DIM ||
         c->ffn_dim < 8 || c->ffn_dim % 8 || c->vocab < 2 || (c->n_heads * c->head_dim) % 8)
-        return fail(SD_ERR_INVALID_ARG, "unsupported model shape (need d_model, ffn_dim, head_dim multiples of 8, "
-                                        "head_dim <= 128, n_heads a multiple of n_kv_heads)");
+        return fail(SD_ERR_INVALID_ARG, "unsupported model shape (need d_model and ffn_dim multiples of 8, head_dim "
+                                        "a power of two in [16, 128], n_heads a multiple of n_kv_heads)");
     if (c->dtype != SD_F32 && c->dtype != SD_BF16)
         return fail(SD_ERR_INVALID_ARG, "dtype must be SD_F32 or SD_BF16");
     if (!(c->rms_eps > 0.0f) || !(c->rope_base > 0.0f))
@@ -716,6 +744,7 @@ void destroy_model(sd_model *m) {
     dev_free(m->q);
     dev_free(m->o);
     dev_free(m->mbuf);
+    dev_free(m->part);
     dev_free(m->xa_h);
     dev_free(m->xa_l);
     dev_free(m->xb_h);
@@ -774,9 +803,9 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     int max_head_tiles = 1;
     for (int k = 0; k < LK_COUNT; ++k) {
         m->plan1[k] = make_plan(m, (LinearKind)k, 1);
-        m->plan4[k] = make_plan(m, (LinearKind)k, 4);
+        m->plan2[k] = make_plan(m, (LinearKind)k, 2);
         m->planm[k] = make_plan(m, (LinearKind)k, 16);
-        for (const Plan *p : {&m->plan1[k], &m->plan4[k], &m->planm[k]}) {
+        for (const Plan *p : {&m->plan1[k], &m->plan2[k], &m->planm[k]}) {
             if (k == LK_HEAD)
                 max_head_tiles = std::max(max_head_tiles, head_tiles(*p));
         }
@@ -791,6 +820,7 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->q, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
     chain(dev_alloc(&m->o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
     chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
+    chain(dev_alloc(&m->part, (size_t)8 * MAX_ROWS * c.d_model));
     m->xld = std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
     chain(dev_alloc(&m->xa_h, (size_t)MAX_ROWS * m->xld));
     chain(dev_alloc(&m->xa_l, (size_t)MAX_ROWS * m->xld));

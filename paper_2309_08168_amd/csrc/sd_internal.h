@@ -54,7 +54,9 @@ struct Mailbox {
 
 enum HeadMode : int32_t { HEAD_NONE = 0, HEAD_AR = 1, HEAD_DRAFT = 2, HEAD_VERIFY = 3 };
 
-enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_HEAD = 4 };
+// EPI_PARTIAL: split-K partial sums [split][row][N], folded into the
+// residual stream by the next k_prep_norm (MFMA path only).
+enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_HEAD = 4, EPI_PARTIAL = 5 };
 
 struct HeadArgs {
     int32_t mode;
@@ -92,6 +94,8 @@ struct LinearArgs {
     const DevCtl *ctl;
     EpiArgs epi;
     int32_t waves;         // MFMA path: waves per work-group splitting the reduction
+    int32_t splits;        // EPI_PARTIAL: work-groups splitting the reduction per tile group
+    float *part;           // EPI_PARTIAL: [splits][MAX_ROWS][N]
     int32_t n_tiles;       // tiles in the layer (set by launch_linear)
 };
 
@@ -110,17 +114,19 @@ struct AttnArgs {
 };
 
 // Kernel paths of the linear layers.
-enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3 };
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4 };
 
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s);
 // Normalised (gain != null) or plain copy of h split into bf16 hi/lo for the MFMA path.
-hipError_t launch_prep_norm(const float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, hipStream_t s);
+// First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
+hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
+                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, const float *part,
+                            int n_part, hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
-hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s);
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);
 hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *dev_tokens, hipStream_t s);
