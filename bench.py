@@ -11,11 +11,24 @@ library on the same inputs is reported beside it.
 Default workload: LLaMA-2-13B shape (40 layers, d 5120, 40 heads x 128,
 FFN 13824, vocab 32000, bf16), prompt 1024 uniform-random ids, 512 new
 tokens, 20 random sublayers skipped in the draft, K_max 12, gamma 0.6.
+
+Other modes:
+  --verify-micro        verification-forward latency, GB/s and MFMA use at
+                        the 13B shape for M in {1, 4, 8, 13, 16} rows over a
+                        KV cache of 512 / 2048 / 4096 N(0, 1) positions
+  --supplementary       labelled planted-redundancy runs (skipped sublayers'
+                        output projections scaled down, lm-head scaled up)
+  --calibrate-copy      a plain device copy of known size, for scaling the
+                        FETCH_SIZE / WRITE_SIZE profiler counters
+  --summarize-stats / --summarize-pmc   write profiles/ summaries from
+                        rocprofv3 CSV output
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -29,9 +42,16 @@ import numpy as np  # noqa: E402
 import sd_synth as S  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2309_08168_amd", "csrc", "kernels_linear.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_verify2_13b.json")
 
 
-def step_bytes(cfg, skip, ctx: float, rows: int = 1):
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def step_bytes(cfg, skip, ctx: float, rows: float = 1):
     """Algorithmic HBM bytes of one forward: weights of the sublayers run,
     read once whatever the row count, plus the KV read at ctx positions and
     written for `rows` new positions in the attention sublayers run."""
@@ -50,11 +70,27 @@ def step_bytes(cfg, skip, ctx: float, rows: int = 1):
     return total
 
 
-def linear_bytes(cfg, kind: str) -> int:
-    es = 2 if cfg.dtype == "bf16" else 4
-    d, F = cfg.d_model, cfg.ffn_dim
-    return {"qkv": cfg.qkv_rows * d, "o": d * cfg.n_heads * cfg.head_dim, "gate_up": 2 * F * d,
-            "down": d * F, "head": cfg.vocab * d}[kind] * es
+def kernel_bytes(n: int, k: int, rows: float, es: int = 2) -> float:
+    """Algorithmic bytes of one linear launch: the n x k weights once, the
+    float32 input rows and output rows."""
+    return n * k * es + rows * k * 4 + rows * n * 4
+
+
+def source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(kernel: str):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    e = t.get("kernels", {}).get(kernel)
+    if not e or t.get("source_hash") != source_hash():
+        return None
+    return e["bytes_per_launch"]
 
 
 def cpu_baseline(cfg, weights, prompt, wl, skip, sample_prompt=16, sample_new=4):
@@ -72,40 +108,32 @@ def cpu_baseline(cfg, weights, prompt, wl, skip, sample_prompt=16, sample_new=4)
     }
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="13b", choices=sorted(S.WORKLOADS))
-    ap.add_argument("--max-new", type=int, default=None, help="override the workload's generated tokens")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-ar", action="store_true", help="skip the autoregressive comparison")
-    args = ap.parse_args()
-
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU: --gpus {args.gpus} is not supported (the decode path is "
-              "batch-1 on a single MI355X; see DESIGN.md for how it would shard)", file=sys.stderr)
-        sys.exit(2)
-
+def load_model(cfg, seed):
     import torch
 
     from paper_2309_08168_amd import binding
 
-    torch.cuda.set_device(0)
-    wl = S.WORKLOADS[args.workload]
-    cfg = S.MODELS[wl.model]
-    max_new = args.max_new or wl.max_new
     t0 = time.perf_counter()
-    host = S.make_weights(cfg, args.seed)
+    host = S.make_weights(cfg, seed)
     t_gen = time.perf_counter() - t0
     dw = binding.DeviceWeights(cfg, host)
     torch.cuda.synchronize()
-    t_up = time.perf_counter() - t0 - t_gen
-    print(f"[bench] {cfg.name}: {cfg.param_count() / 1e9:.2f} B params, generated in {t_gen:.1f} s, "
-          f"uploaded in {t_up:.1f} s", file=sys.stderr, flush=True)
-    model = binding.Model(cfg, dw)
+    log(f"{cfg.name}: {cfg.param_count() / 1e9:.2f} B params, generated in {t_gen:.1f} s, uploaded in "
+        f"{time.perf_counter() - t0 - t_gen:.1f} s")
+    return host, binding.Model(cfg, dw)
+
+
+# ---------------------------------------------------------------------------
+# main benchmark
+
+
+def run_bench(args):
+    import torch
+
+    wl = S.WORKLOADS[args.workload]
+    cfg = S.MODELS[wl.model]
+    max_new = args.max_new or wl.max_new
+    host, model = load_model(cfg, args.seed)
     prompt = S.prompt(cfg, wl.prompt_len, args.seed)
     skip = S.skip_mask(cfg, wl.mask, args.seed)
 
@@ -115,11 +143,18 @@ def main():
     def run_ar():
         return model.generate_ar(prompt, max_new)
 
+    warm = None
     for i in range(args.warmup):
-        run_sd()
+        _, warm = run_sd()
         if not args.no_ar:
             run_ar()
-        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+        log(f"warmup {i + 1}/{args.warmup} done")
+
+    # the dominant kernel of the step: the gate/up projection at the row
+    # count the verification forwards run at (timed live with HIP events)
+    mean_rows = 1 + warm["n_drafted"] / max(warm["n_stages"], 1) if warm else 2.0
+    regime = 2 if mean_rows <= 2.0 else 16
+    model.time_kernel("gate_up", regime)
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -128,10 +163,12 @@ def main():
     for i in range(args.steps):
         sd_tokens, st = run_sd()
         sd_stats.append(st)
-        print(f"[bench] step {i + 1}/{args.steps}: decode {st['decode_ms']:.1f} ms, stages {st['n_stages']}, "
-              f"acceptance {st['n_accepted']}/{st['n_drafted']}", file=sys.stderr, flush=True)
+        log(f"step {i + 1}/{args.steps}: decode {st['decode_ms']:.1f} ms, stages {st['n_stages']}, "
+            f"acceptance {st['n_accepted']}/{st['n_drafted']}")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    kt = model.kernel_time()
+    model.time_kernel(None)
 
     ar_stats = []
     ar_tokens = None
@@ -151,8 +188,8 @@ def main():
     verify_ms = sum(s["verify_ms"] for s in sd_stats) / max(stages, 1)
     ctx = wl.prompt_len + max_new / 2
     b_draft = step_bytes(cfg, skip, ctx, 1)
-    mean_rows = 1 + drafted / max(stages, 1)
-    b_verify = step_bytes(cfg, None, ctx, mean_rows)
+    vrows = 1 + drafted / max(stages, 1)
+    b_verify = step_bytes(cfg, None, ctx, vrows)
     extra = {
         "acceptance": round(accepted / drafted, 4) if drafted else None,
         "tokens_per_stage": round(args.steps * max_new / max(stages, 1), 4),
@@ -160,7 +197,7 @@ def main():
         "draft_step_GBps": round(b_draft / (draft_ms / 1e3) / 1e9, 1),
         "draft_step_frac_hbm": round(b_draft / (draft_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
         "verify_step_ms": round(verify_ms, 4),
-        "verify_mean_rows": round(mean_rows, 3),
+        "verify_mean_rows": round(vrows, 3),
         "verify_step_GBps": round(b_verify / (verify_ms / 1e3) / 1e9, 1),
         "verify_step_frac_hbm": round(b_verify / (verify_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
         "prefill_ms": round(sum(s["prefill_ms"] for s in sd_stats) / args.steps, 2),
@@ -169,23 +206,33 @@ def main():
         ar_ms = sum(s["decode_ms"] for s in ar_stats)
         ar_tps = args.steps * max_new / (ar_ms / 1e3)
         b_ar = step_bytes(cfg, None, ctx, 1)
+        per = ar_ms / (args.steps * max_new)
         extra.update({
             "ar_tokens_per_s": round(ar_tps, 2),
             "speedup_vs_ar": round(value / ar_tps, 4),
-            "ar_step_ms": round(ar_ms / (args.steps * max_new), 4),
-            "ar_step_GBps": round(b_ar / (ar_ms / (args.steps * max_new) / 1e3) / 1e9, 1),
-            "ar_step_frac_hbm": round(b_ar / (ar_ms / (args.steps * max_new) / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
-            "sd_equals_ar_tokens": int(np.sum(np.asarray(sd_tokens) == np.asarray(ar_tokens))),
+            "ar_step_ms": round(per, 4),
+            "ar_step_GBps": round(b_ar / (per / 1e3) / 1e9, 1),
+            "ar_step_frac_hbm": round(b_ar / (per / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "sd_tokens_equal_ar": int(np.sum(np.asarray(sd_tokens) == np.asarray(ar_tokens))),
         })
+        # break-even acceptance with one draft per stage: a* = c_draft + c_verify - 1
+        extra["break_even_acceptance_1draft"] = round(draft_ms / per + verify_ms / per - 1.0, 3)
 
-    roofline = {
-        "bound": "hbm", "achieved": extra["draft_step_GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-        "frac": extra["draft_step_frac_hbm"], "traffic": None,
-        "kernel": "whole draft step (first measurement)",
-    }
+    roofline = None
+    if kt["launches"]:
+        avg_ms = kt["total_ms"] / kt["launches"]
+        rows = regime if regime == 2 else vrows
+        nbytes = kernel_bytes(kt["n"], kt["k"], rows)
+        achieved = nbytes / (avg_ms / 1e3) / 1e9
+        roofline = {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_for(kt["kernel"]),
+            "kernel": kt["kernel"], "layer": f"gate_up, verification of <= {regime} rows",
+            "bytes_per_launch": int(nbytes), "avg_launch_us": round(avg_ms * 1e3, 2), "launches": kt["launches"],
+        }
     cpu = None
     if not args.no_cpu_baseline:
-        print("[bench] timing the oracle on a bounded sample", file=sys.stderr, flush=True)
+        log("timing the oracle on a bounded sample")
         cpu = cpu_baseline(cfg, host, prompt, wl, skip)
 
     line = {
@@ -210,6 +257,216 @@ def main():
     }
     print(json.dumps(line), flush=True)
     model.close()
+
+
+# ---------------------------------------------------------------------------
+# verification-forward microbenchmark (13B stack over an N(0, 1) KV cache)
+
+
+def run_verify_micro(args):
+    import torch
+
+    cfg = S.MODELS["13b"]
+    host, model = load_model(cfg, args.seed)
+    del host
+    es = 2
+    rows_list = [int(x) for x in args.micro_rows.split(",")]
+    ctx_list = [int(x) for x in args.micro_ctx.split(",")]
+    params = cfg.param_count() - cfg.vocab * cfg.d_model  # embedding table is gathered, not streamed
+    results = []
+    for ctx in ctx_list:
+        cap = ctx + max(rows_list)
+        buf = torch.empty(model.kv_cache_bytes(cap) // 2, dtype=torch.int16, device="cuda")
+        # fill positions [0, ctx) of every (layer, K/V, head) with N(0, 1)
+        view = buf.view(cfg.n_layers * 2 * cfg.n_kv_heads, cap, cfg.head_dim)
+        fill = S.kv_fill(cfg, cfg.n_layers * 2 * cfg.n_kv_heads * ctx * cfg.head_dim, args.seed)
+        view[:, :ctx].copy_(torch.from_numpy(fill.view(np.int16)).view(-1, ctx, cfg.head_dim).to("cuda"))
+        del fill
+        cache = model.cache(cap, device_buf=buf)
+        for M in rows_list:
+            toks = S.prompt(cfg, M, args.seed + M)
+            logits = torch.empty((M, cfg.vocab), dtype=torch.float32, device="cuda")
+            times = []
+            for it in range(args.micro_iters + 1):
+                cache.set_length(ctx)
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record()
+                model.forward(toks, cache, logits=logits)
+                b.record()
+                b.synchronize()
+                if it:
+                    times.append(a.elapsed_time(b))
+            ms = float(np.median(times))
+            nbytes = step_bytes(cfg, None, ctx, M)
+            useful = 2.0 * params * M
+            issued = 2.0 * params * 16 * 2 if M > 2 else 0.0  # MFMA path: 16 padded rows, hi + lo
+            r = {"rows": M, "ctx": ctx, "ms": round(ms, 4), "GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
+                 "frac_hbm": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+                 "mfma_useful_frac": round(useful / (ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
+                 "mfma_issued_frac": round(issued / (ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5)}
+            results.append(r)
+            log(json.dumps(r))
+        cache.close()
+        del buf
+    print(json.dumps({"mode": "verify-micro", "model": "13b stack (40 layers + lm-head)", "results": results}))
+
+
+# ---------------------------------------------------------------------------
+# supplementary planted-redundancy runs (labelled; not the headline value)
+
+
+def run_supplementary(args):
+    import torch  # noqa: F401
+
+    from paper_2309_08168_amd import binding
+
+    wl = S.WORKLOADS[args.workload]
+    cfg = S.MODELS[wl.model]
+    max_new = args.max_new or wl.max_new
+    host = S.make_weights(cfg, args.seed)
+    prompt = S.prompt(cfg, wl.prompt_len, args.seed)
+    skip = S.skip_mask(cfg, wl.mask, args.seed)
+    out = []
+    for rho, gain, gamma in [(float(x.split(":")[0]), float(x.split(":")[1]), float(x.split(":")[2]))
+                             for x in args.planted.split(",")]:
+        w = S.plant_redundancy(cfg, host, skip, rho, gain)
+        model = binding.Model(cfg, binding.DeviceWeights(cfg, w))
+        model.generate_sd(prompt, max_new, skip, wl.k_max, gamma)
+        model.generate_ar(prompt, max_new)
+        sd_tok, sd = model.generate_sd(prompt, max_new, skip, wl.k_max, gamma)
+        ar_tok, ar = model.generate_ar(prompt, max_new)
+        r = {"rho": rho, "head_gain": gain, "gamma": gamma,
+             "sd_tokens_per_s": round(max_new / (sd["decode_ms"] / 1e3), 2),
+             "ar_tokens_per_s": round(max_new / (ar["decode_ms"] / 1e3), 2),
+             "speedup": round(ar["decode_ms"] / sd["decode_ms"], 4),
+             "acceptance": round(sd["n_accepted"] / max(sd["n_drafted"], 1), 4),
+             "tokens_per_stage": round(max_new / max(sd["n_stages"], 1), 3),
+             "tokens_equal": int(np.sum(sd_tok == ar_tok))}
+        out.append(r)
+        log(json.dumps(r))
+        model.close()
+        del w
+    print(json.dumps({"mode": "supplementary (planted redundancy)", "workload": wl.name, "results": out}))
+
+
+# ---------------------------------------------------------------------------
+# profiler helpers
+
+
+def run_calibrate_copy(args):
+    import torch
+
+    n = args.copy_bytes
+    a = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "calibrate-copy", "bytes_read": n, "bytes_written": n}))
+
+
+def _read_csv(path):
+    return list(csv.DictReader(open(path)))
+
+
+def run_summarize_stats(args):
+    rows = _read_csv(args.summarize_stats)
+    lines = [f"# rocprofv3 --kernel-trace --stats summary", f"# command: {args.command}", "",
+             f"{'calls':>7} {'avg_us':>9} {'total_ms':>10} {'pct':>6}  kernel"]
+    for r in rows[: args.top]:
+        lines.append(f"{int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f} {float(r['TotalDurationNs']) / 1e6:10.2f} "
+                     f"{float(r['Percentage']):6.2f}  {r['Name']}")
+    os.makedirs(os.path.dirname(args.out), exist_ok=True)
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _counter_per_kernel(path, counter):
+    per = {}
+    for r in _read_csv(path):
+        name = r.get("Kernel_Name") or r.get("Kernel-Name")
+        if r.get("Counter_Name", counter) != counter:
+            continue
+        per.setdefault(name, []).append(float(r["Counter_Value"]))
+    return per
+
+
+def run_summarize_pmc(args):
+    fetch_csv, write_csv = args.summarize_pmc
+    fetch = _counter_per_kernel(fetch_csv, "FETCH_SIZE")
+    write = _counter_per_kernel(write_csv, "WRITE_SIZE")
+    # calibration: the device-to-device copy of --copy-bytes (--with-copy)
+    # runs as the runtime's copy kernel; the largest median among copy kernels
+    # (the largest copy dispatch; smaller copies share the kernel name)
+    copy_names = [k for k in fetch if "copybuffer" in k.lower()]
+    calib_f = calib_w = None
+    if copy_names:
+        k = copy_names[0]
+        calib_f = args.copy_bytes / (max(fetch[k]) * 1024.0)
+        if k in write:
+            calib_w = args.copy_bytes / (max(write[k]) * 1024.0)
+    kernels = {}
+    for name in args.kernels.split(";"):
+        if name in fetch and name in write:
+            f = float(np.median(fetch[name])) * 1024.0 * (calib_f or 1.0)
+            w = float(np.median(write[name])) * 1024.0 * (calib_w or 1.0)
+            kernels[name] = {"fetch_bytes": f, "write_bytes": w, "bytes_per_launch": f + w}
+    out = {"source_hash": source_hash(), "copy_scale_fetch": calib_f, "copy_scale_write": calib_w,
+           "commands": args.command, "kernels": kernels}
+    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    print(json.dumps(out, indent=1))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="13b", choices=sorted(S.WORKLOADS))
+    ap.add_argument("--max-new", type=int, default=None, help="override the workload's generated tokens")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ar", action="store_true", help="skip the autoregressive comparison")
+    ap.add_argument("--verify-micro", action="store_true")
+    ap.add_argument("--micro-rows", default="1,4,8,13,16")
+    ap.add_argument("--micro-ctx", default="512,2048,4096")
+    ap.add_argument("--micro-iters", type=int, default=5)
+    ap.add_argument("--supplementary", action="store_true")
+    ap.add_argument("--planted", default="0.05:8:0.6,0.05:8:0.0,0.02:16:0.6",
+                    help="rho:head_gain:gamma triples for --supplementary")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--with-copy", action="store_true", help="also run the calibration copy after the bench")
+    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--summarize-stats", default=None, help="rocprofv3 kernel_stats.csv to summarize")
+    ap.add_argument("--summarize-pmc", nargs=2, default=None, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--kernels", default="", help="';'-separated kernel symbols for --summarize-pmc")
+    ap.add_argument("--out", default=os.path.join(ROOT, "profiles", "kernel_stats.txt"))
+    ap.add_argument("--top", type=int, default=20)
+    ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
+    args = ap.parse_args()
+
+    if args.summarize_stats:
+        return run_summarize_stats(args)
+    if args.summarize_pmc:
+        return run_summarize_pmc(args)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: --gpus {args.gpus} is not supported (the decode path is "
+              "batch-1 on a single MI355X; DESIGN.md describes how it would shard)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        return run_calibrate_copy(args)
+    if args.verify_micro:
+        run_verify_micro(args)
+    elif args.supplementary:
+        run_supplementary(args)
+    else:
+        run_bench(args)
+    if args.with_copy:
+        run_calibrate_copy(args)
 
 
 if __name__ == "__main__":

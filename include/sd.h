@@ -152,6 +152,22 @@ sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t 
 sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                      int32_t *out_tokens, sd_stats *stats);
 
+/* Measurement hook.  Selects one linear-layer class whose launches the
+ * library brackets with HIP events on its stream: layer 0 = QKV, 1 = attention
+ * output, 2 = gate/up, 3 = down, 4 = lm-head; rows = 1, 2 or 16 selects the
+ * kernel family used for forwards of one row, up to two rows, or more rows.
+ * layer = -1 turns timing off.  Timing adds a little host and GPU time per
+ * timed launch; at most 65536 launches per call are timed.  Resets the
+ * totals.  Errors: INVALID_ARG. */
+sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows);
+
+/* Totals of the timed class since sd_model_time_kernel: launches, summed
+ * GPU milliseconds, the kernel symbol as a profiler prints it (written to
+ * kernel_name, NUL-terminated, truncated to name_cap), and the weight
+ * matrix shape n x k of one launch.  Any output pointer may be NULL. */
+sd_status sd_model_kernel_time(sd_model *model, int64_t *launches, double *total_ms, char *kernel_name,
+                               int32_t name_cap, int64_t *n, int64_t *k);
+
 /* Message of the last non-OK status returned to this thread ("" if none). */
 const char *sd_last_error(void);
 

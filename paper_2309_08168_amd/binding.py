@@ -23,7 +23,8 @@ SD_F32, SD_BF16 = 0, 1
 EXPORTS = (
     "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
-    "sd_self_spec_generate", "sd_autoregressive_generate", "sd_last_error", "sd_version",
+    "sd_self_spec_generate", "sd_autoregressive_generate", "sd_model_time_kernel", "sd_model_kernel_time",
+    "sd_last_error", "sd_version",
 )
 
 
@@ -83,6 +84,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_forward": ([vp, vp, i32, vp, vp, vp], ctypes.c_int),
         "sd_self_spec_generate": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_stats)], ctypes.c_int),
         "sd_autoregressive_generate": ([vp, vp, i32, i32, vp, p(sd_stats)], ctypes.c_int),
+        "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
+        "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
+                                  p(ctypes.c_int64), p(ctypes.c_int64)], ctypes.c_int),
         "sd_last_error": ([], ctypes.c_char_p),
         "sd_version": ([], ctypes.c_char_p),
     }
@@ -175,6 +179,22 @@ class Model:
             self.close()
         except Exception:
             pass
+
+    # linear-layer classes of sd_model_time_kernel
+    LAYERS = {"qkv": 0, "o": 1, "gate_up": 2, "down": 3, "head": 4}
+
+    def time_kernel(self, layer: Optional[str], rows: int = 1):
+        """Bracket launches of one layer class with HIP events (None: off)."""
+        check(load().sd_model_time_kernel(self._h, -1 if layer is None else self.LAYERS[layer], rows))
+
+    def kernel_time(self) -> dict:
+        n_l, ms = ctypes.c_int64(), ctypes.c_double()
+        n, k = ctypes.c_int64(), ctypes.c_int64()
+        name = ctypes.create_string_buffer(256)
+        check(load().sd_model_kernel_time(self._h, ctypes.byref(n_l), ctypes.byref(ms), name, 256, ctypes.byref(n),
+                                          ctypes.byref(k)))
+        return {"launches": n_l.value, "total_ms": ms.value, "kernel": name.value.decode(), "n": n.value,
+                "k": k.value}
 
     def kv_cache_bytes(self, capacity: int) -> int:
         return int(load().sd_kv_cache_bytes(ctypes.byref(self._cfg), capacity))

@@ -50,7 +50,9 @@ enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4
 
 // How one linear layer is launched for one row regime.
 struct Plan {
-    int path;     // PATH_GEMV, PATH_VALU16 or PATH_MFMA
+    int kind;     // LinearKind
+    int regime;   // 1, 2 or 16: the row counts the plan serves
+    int path;     // PATH_GEMV, PATH_VALU2, PATH_VALU16 or PATH_MFMA
     int rows;     // weight rows per work-group
     int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
     int waves;    // MFMA: waves per work-group splitting the reduction
@@ -104,6 +106,12 @@ struct sd_model {
     int d_log_cap = 0;         // int32 elements
     sd_kv_cache *gen_cache = nullptr;
     hipEvent_t ev[6] = {};
+    // measurement hook (sd_model_time_kernel)
+    int timed_kind = -1, timed_regime = 0;
+    std::vector<hipEvent_t> tev;  // pairs
+    size_t tev_used = 0;
+    int64_t timed_launches = 0;
+    double timed_ms = 0.0;
 };
 
 namespace {
@@ -130,6 +138,8 @@ bool mfma_ok(const sd_model *m, LinearKind kind) {
 Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
     const sd_config &c = m->cfg;
     Plan p{};
+    p.kind = kind;
+    p.regime = rows;
     p.waves = 4;
     p.splits = 1;
     switch (kind) {
@@ -312,7 +322,22 @@ sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, 
     a.splits = p.splits;
     a.part = m->part;
     a.n_tiles = p.n_tiles;
+    const bool timed = p.kind == m->timed_kind && p.regime == m->timed_regime && m->tev_used + 2 <= 2 * 65536;
+    if (timed) {
+        if (m->tev_used + 2 > m->tev.size()) {
+            for (int i = 0; i < 256; ++i) {
+                hipEvent_t e;
+                SD_HIP(hipEventCreate(&e));
+                m->tev.push_back(e);
+            }
+        }
+        SD_HIP(hipEventRecord(m->tev[m->tev_used], m->stream));
+    }
     SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer"));
+    if (timed) {
+        SD_HIP(hipEventRecord(m->tev[m->tev_used + 1], m->stream));
+        m->tev_used += 2;
+    }
     if (p.epi == EPI_HEAD)
         SD_TRY(launch(launch_head_finalize(a, p.n_tiles, m->stream), "head finalize"));
     return SD_OK;
@@ -544,6 +569,17 @@ sd_status wait_mailbox(sd_model *m, int32_t seq) {
     }
 }
 
+float elapsed(hipEvent_t a, hipEvent_t b);
+
+// Adds up the timed launches of the finished call (the stream is idle).
+void collect_timing(sd_model *m) {
+    for (size_t i = 0; i + 1 < m->tev_used; i += 2) {
+        m->timed_ms += elapsed(m->tev[i], m->tev[i + 1]);
+        m->timed_launches += 1;
+    }
+    m->tev_used = 0;
+}
+
 float elapsed(hipEvent_t a, hipEvent_t b) {
     float ms = 0.0f;
     if (hipEventElapsedTime(&ms, a, b) != hipSuccess)
@@ -566,6 +602,7 @@ sd_status copy_results(sd_model *m, int32_t max_new, int32_t *out_tokens, sd_sta
                               m->stream));
     }
     SD_HIP(hipStreamSynchronize(m->stream));
+    collect_timing(m);
     if (stats) {
         stats->n_stages = st.n_stages;
         stats->n_drafted = st.n_drafted;
@@ -730,6 +767,7 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
         SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, rows, hs));
     }
     SD_HIP(hipStreamSynchronize(m->stream));
+    collect_timing(m);
     kc->len += n;
     return SD_OK;
 }
@@ -763,6 +801,8 @@ void destroy_model(sd_model *m) {
     for (hipEvent_t &e : m->ev)
         if (e)
             (void)hipEventDestroy(e);
+    for (hipEvent_t e : m->tev)
+        (void)hipEventDestroy(e);
     delete m;
 }
 
@@ -863,6 +903,30 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     return SD_OK;
 }
 
+// The kernel symbol of a plan as the profiler prints it.
+std::string kernel_symbol(const sd_model *m, const Plan &p) {
+    const char *tw = m->bf16 ? "unsigned short" : "float";
+    const bool norm = p.kind == LK_QKV || p.kind == LK_GATE_UP || p.kind == LK_HEAD;
+    if (p.path == PATH_MFMA)
+        return "void sdk::k_linear_mfma<" + std::to_string(p.epi) + ", " + std::to_string(p.rows / 16) + ", " +
+               std::to_string(p.waves) + ">(sdk::LinearArgs)";
+    const int mr = p.path == PATH_GEMV ? 1 : (p.path == PATH_VALU2 ? 2 : (p.path == PATH_VALU4 ? 4 : 16));
+    return std::string("void sdk::k_linear_valu<") + tw + ", " + std::to_string(mr) + ", " + std::to_string(p.rows) +
+           ", " + std::to_string(p.epi) + ", " + (norm ? "true" : "false") + ">(sdk::LinearArgs)";
+}
+
+const Plan *find_plan(const sd_model *m, int kind, int regime) {
+    if (kind < 0 || kind >= LK_COUNT)
+        return nullptr;
+    if (regime == 1)
+        return &m->plan1[kind];
+    if (regime == 2)
+        return &m->plan2[kind];
+    if (regime == 16)
+        return &m->planm[kind];
+    return nullptr;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -937,6 +1001,30 @@ sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t 
 sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                      int32_t *out_tokens, sd_stats *stats) {
     SD_GUARD(return autoregressive(model, prompt, prompt_len, max_new, out_tokens, stats);)
+}
+
+sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows) {
+    SD_GUARD(if (!model) return fail(SD_ERR_INVALID_ARG, "model is null");
+             if (layer != -1 && !find_plan(model, layer, rows))
+                 return fail(SD_ERR_INVALID_ARG, "layer must be -1 or 0..4 and rows 1, 2 or 16");
+             model->timed_kind = layer; model->timed_regime = rows; model->tev_used = 0;
+             model->timed_launches = 0; model->timed_ms = 0.0; return SD_OK;)
+}
+
+sd_status sd_model_kernel_time(sd_model *model, int64_t *launches, double *total_ms, char *kernel_name,
+                               int32_t name_cap, int64_t *n, int64_t *k) {
+    SD_GUARD(if (!model) return fail(SD_ERR_INVALID_ARG, "model is null");
+             const Plan *p = find_plan(model, model->timed_kind, model->timed_regime);
+             if (launches) *launches = model->timed_launches;
+             if (total_ms) *total_ms = model->timed_ms;
+             if (n) *n = p ? p->N : 0;
+             if (k) *k = p ? p->K : 0;
+             if (kernel_name && name_cap > 0) {
+                 const std::string nm = p ? kernel_symbol(model, *p) : std::string();
+                 const size_t len = std::min<size_t>(nm.size(), (size_t)name_cap - 1);
+                 std::memcpy(kernel_name, nm.data(), len);
+                 kernel_name[len] = 0;
+             } return SD_OK;)
 }
 
 const char *sd_last_error(void) { return g_err.c_str(); }
