@@ -98,6 +98,9 @@ typedef struct {
  * allocates the library's device workspace (activations of up to 16 rows,
  * rotary table, reduction scratch).  Errors: INVALID_ARG, OOM, DEVICE. */
 sd_status sd_model_create(const sd_config *config, const sd_weights *weights, void *hip_stream, sd_model **out);
+/* Waits for the model's stream, then frees the model and its workspace.
+ * KV caches created on it stay valid objects but are detached: they can
+ * only be destroyed (any other use reports INVALID_ARG). */
 sd_status sd_model_destroy(sd_model *model);
 
 /* Bytes of a KV cache for capacity positions:
@@ -111,6 +114,8 @@ size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity);
  * otherwise the library allocates it.  Errors: INVALID_ARG, CAPACITY
  * (more than 65536 positions), OOM. */
 sd_status sd_kv_cache_create(sd_model *model, int32_t capacity, void *device_buf, sd_kv_cache **out);
+/* Frees the cache (and its buffer when the library allocated it), after
+ * waiting for its model's stream; allowed before or after sd_model_destroy. */
 sd_status sd_kv_cache_destroy(sd_kv_cache *cache);
 int32_t sd_kv_cache_length(const sd_kv_cache *cache); /* -1 for NULL */
 /* Rolls the cache back to len positions (0 <= len <= length). */

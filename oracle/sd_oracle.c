@@ -59,6 +59,19 @@ static void wrow(const orc_model *m, const void *p, int64_t row, int64_t ncols, 
         dst[k] = wval(m, p, row * ncols + k);
 }
 
+/* Reading: the models the paper evaluates run in bfloat16 (its adaptation
+ * appendix names bf16 the default), so their KV caches hold bfloat16
+ * values.  For bf16 models the cache stores each K/V element rounded to the
+ * nearest bfloat16 (ties to even); float32 models keep it exact. */
+static double kv_store_value(const orc_model *m, double x)
+{
+    if (m->c.wdtype != 1 || x == 0.0 || !isfinite(x))
+        return x;
+    int e;
+    const double f = frexp(x, &e);       /* x = f * 2^e, 0.5 <= |f| < 1 */
+    return ldexp(rint(ldexp(f, 8)), e - 8); /* 8 significant bits, ties to even */
+}
+
 static const void **copy_ptrs(const void *const *src, int n)
 {
     const void **dst = (const void **)malloc(sizeof(void *) * (size_t)n);
@@ -360,10 +373,12 @@ int orc_forward(orc_model *m, orc_cache *c, const int32_t *tokens, int32_t n, co
                 rope(m, row, H, start + r);
                 rope(m, row + (int64_t)H * dh, KVH, start + r);
                 for (int g = 0; g < KVH; ++g) {
-                    memcpy(c->kv + kv_index(c, l, 0, g, start + r), row + (int64_t)(H + g) * dh,
-                           sizeof(double) * (size_t)dh);
-                    memcpy(c->kv + kv_index(c, l, 1, g, start + r), row + (int64_t)(H + KVH + g) * dh,
-                           sizeof(double) * (size_t)dh);
+                    double *kd = c->kv + kv_index(c, l, 0, g, start + r);
+                    double *vd = c->kv + kv_index(c, l, 1, g, start + r);
+                    for (int e = 0; e < dh; ++e) {
+                        kd[e] = kv_store_value(m, row[(int64_t)(H + g) * dh + e]);
+                        vd[e] = kv_store_value(m, row[(int64_t)(H + KVH + g) * dh + e]);
+                    }
                 }
             }
 #pragma omp parallel

@@ -7,7 +7,10 @@
  * table or helper with the GPU path.
  *
  * Arithmetic is float64 throughout.  Weights are read as stored (float32,
- * or bfloat16 bit patterns expanded exactly) and the KV cache holds float64.
+ * or bfloat16 bit patterns expanded exactly).  The KV cache holds each
+ * element in the model's storage precision: exact for float32 models,
+ * rounded to the nearest bfloat16 for bfloat16 models (the precision the
+ * paper's models run in).
  * Every output element is a sequential reduction over its inputs in index
  * order, so a row's result does not depend on how many rows share the call
  * or on the thread count.  Argmax and the top-1 probability are decided on

@@ -347,10 +347,8 @@ __global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
         const int r = qi / G, head = g * G + (qi - r * G);
         const float y = O / L;
         const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
-        if (a.out_hi) {
-            const uint32_t bits = __float_as_uint(y);
-            a.out_hi[oi] = (uint16_t)(bits >> 16);
-            a.out_lo[oi] = (uint16_t)(__float_as_uint(y - __uint_as_float(bits & 0xffff0000u)) >> 16);
+        if (a.out_x) {
+            store_split3(a.out_x, (int64_t)MAX_ROWS * a.ld_out, oi, y);
         } else {
             a.out[oi] = y;
         }
@@ -404,10 +402,8 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
             O = fmaf(w_s[sp], a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e], O);
         const float y = O / L;
         const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
-        if (a.out_hi) {
-            const uint32_t b = __float_as_uint(y);
-            a.out_hi[oi] = (uint16_t)(b >> 16);
-            a.out_lo[oi] = (uint16_t)(__float_as_uint(y - __uint_as_float(b & 0xffff0000u)) >> 16);
+        if (a.out_x) {
+            store_split3(a.out_x, (int64_t)MAX_ROWS * a.ld_out, oi, y);
         } else {
             a.out[oi] = y;
         }

@@ -10,8 +10,8 @@
 //   - k_linear_valu, MR == 2 or 4: verification of 1 or up to 3 drafts;
 //   - k_linear_valu, MR == 16: any row count, for float32 weights;
 //   - k_linear_mfma: the verification forward over up to 16 rows (the last
-//     committed token plus the drafts, Algorithm 2), bf16 MFMA tiles with
-//     the rows padded to 16.
+//     committed token plus the drafts, Algorithm 2) on bf16 MFMA tiles, the
+//     activations split into three bf16 terms packed into the 16 columns.
 //
 // RMSNorm is folded in: y = W (g * h) / rms(h), so the kernel that reads h
 // as its input also accumulates sum(h^2) and scales its outputs at the end;
@@ -33,14 +33,6 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     uint32_t u = __float_as_uint(f);
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
-}
-
-// Split u into bf16 hi (its top 16 bits) and lo (the remainder, rounded
-// down to bf16): hi + lo keeps about 16 bits of u's mantissa.
-__device__ __forceinline__ void split_hilo(float u, uint16_t &hi, uint16_t &lo) {
-    const uint32_t b = __float_as_uint(u);
-    hi = (uint16_t)(b >> 16);
-    lo = (uint16_t)(__float_as_uint(u - __uint_as_float(b & 0xffff0000u)) >> 16);
 }
 
 __device__ __forceinline__ void unpack8(u32x4_t v, float (&w)[8]) {
@@ -300,7 +292,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                 dst[(int64_t)m * a.N + n] = fin[i * MR + m];
         }
     } else if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
-        for (int j = tid; j < R * M; j += 256) {
+        for (int j = tid; j < R * M; j += blockDim.x) {
             const int i = j % R, m = j / R, n = t * R + i;
             if (n < a.N) {
                 const float v = fin[i * MR + m] * inv[m];
@@ -313,17 +305,14 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
         }
     } else if constexpr (EPI == EPI_SWIGLU) {
         const int P = R >> 1;
-        for (int j = tid; j < P * M; j += 256) {
+        for (int j = tid; j < P * M; j += blockDim.x) {
             const int i = j % P, m = j / P, f = t * P + i;
             if (f < e.ffn) {
                 const float g = fin[i * MR + m] * inv[m];
                 const float u = fin[(i + P) * MR + m] * inv[m];
                 const float y = g / (1.0f + expf(-g)) * u;
-                if (e.out_hi) {
-                    uint16_t hb, lb;
-                    split_hilo(y, hb, lb);
-                    e.out_hi[(int64_t)m * e.ld_out + f] = hb;
-                    e.out_lo[(int64_t)m * e.ld_out + f] = lb;
+                if (e.out_x) {
+                    store_split3(e.out_x, (int64_t)MAX_ROWS * e.ld_out, (int64_t)m * e.ld_out + f, y);
                 } else {
                     e.out[(int64_t)m * e.ld_out + f] = y;
                 }
@@ -332,7 +321,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
     } else if constexpr (EPI == EPI_QKV) {
         const int P = R >> 1, dh = e.head_dim, half = dh >> 1;
         const int H = e.n_heads, KVH = e.n_kv_heads;
-        for (int j = tid; j < P * M; j += 256) {
+        for (int j = tid; j < P * M; j += blockDim.x) {
             const int i = j % P, m = j / P;
             const int n0 = tile_row<EPI>(t, i, R, e);
             const int head = n0 / dh, ei = n0 - head * dh;
@@ -361,7 +350,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
         }
     } else if constexpr (EPI == EPI_HEAD) {
         const HeadArgs &h = e.head;
-        for (int j = tid; j < R * M; j += 256) {
+        for (int j = tid; j < R * M; j += blockDim.x) {
             const int i = j % R, m = j / R, n = t * R + i;
             if (n < a.N) {
                 const float v = fin[i * MR + m] * inv[m];
@@ -521,32 +510,39 @@ __device__ __forceinline__ void mfma_load(u32x4_t (&wv)[TN][4], const uint16_t *
             wv[j][i] = *reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 32 * i);
 }
 
-// One k-step: the hi and lo activation fragments of k-step k0 against the
-// weights already in registers.
-template <int TN>
-__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const uint16_t *Xh, const uint16_t *Xl,
-                                           bool xrow, int k0, floatx4_t (&acc)[TN]) {
+// One k-step of 128: the packed activation columns against the weights
+// already in registers.
+template <int TN, int NP>
+__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const uint16_t *const (&Xp)[NP],
+                                           const bool (&xv)[NP], int k0, floatx4_t (&acc)[TN][NP]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        u32x4_t bhi = {0u, 0u, 0u, 0u}, blo = {0u, 0u, 0u, 0u};
-        if (xrow) {
-            bhi = *reinterpret_cast<const u32x4_t *>(Xh + k0 + 32 * i);
-            blo = *reinterpret_cast<const u32x4_t *>(Xl + k0 + 32 * i);
+        bf16x8_t b[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            u32x4_t v = {0u, 0u, 0u, 0u};
+            if (xv[p])
+                v = *reinterpret_cast<const u32x4_t *>(Xp[p] + k0 + 32 * i);
+            b[p] = __builtin_bit_cast(bf16x8_t, v);
         }
-        const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bhi);
-        const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, blo);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, wv[j][i]);
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bh, acc[j], 0, 0, 0);
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, bl, acc[j], 0, 0, 0);
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+                acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, b[p], acc[j][p], 0, 0, 0);
         }
     }
 }
 
-template <int EPI, int TN, int NW>
+// The 16 x NP columns of the B operand hold (term, row) pairs: column
+// c = t * M + r carries term t of activation row r, so NP = ceil(3 M / 16)
+// MFMAs per k-step cover all X_TERMS terms of M rows (one MFMA for up to 5
+// rows, two up to 10, three up to 16).  The host picks NP from its bound on
+// M (LinearArgs::max_rows).
+template <int EPI, int TN, int NW, int NP>
 __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
-    __shared__ float red[NW][TN * 16][17];
+    __shared__ float red[NW][TN * 16][NP * 16 + 1];
     __shared__ float fin[TN * 16 * 16];
     __shared__ float inv_s[16];
     const int S = EPI == EPI_PARTIAL ? a.splits : 1;
@@ -563,17 +559,27 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         const int n = nv ? tile_row<EPI>(t, r16, 16, a.epi) : 0;
         Wr[j] = reinterpret_cast<const uint16_t *>(a.W) + (int64_t)n * a.K + kg * 8;
     }
-    const uint16_t *Xh = a.Xh + (int64_t)r16 * a.ldx + kg * 8;
-    const uint16_t *Xl = a.Xl + (int64_t)r16 * a.ldx + kg * 8;
-    const bool xrow = r16 < M;
+    const int64_t plane = (int64_t)MAX_ROWS * a.ldx;
+    const uint16_t *Xp[NP];
+    bool xv[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const int c = 16 * p + r16;
+        const int t = M > 0 ? c / M : X_TERMS;
+        xv[p] = t < X_TERMS;
+        const int r = xv[p] ? c - t * M : 0;
+        Xp[p] = a.Xs + (xv[p] ? t : 0) * plane + (int64_t)r * a.ldx + kg * 8;
+    }
     // k-steps of this split, shared out among the waves
     const int KS_all = a.K >> 7;
     const int ks0 = (int)(((int64_t)KS_all * sp) / S), KS = (int)(((int64_t)KS_all * (sp + 1)) / S) - ks0;
 
-    floatx4_t acc[TN];
+    floatx4_t acc[TN][NP];
 #pragma unroll
     for (int j = 0; j < TN; ++j)
-        acc[j] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+            acc[j][p] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     // Each wave streams a contiguous range of k-steps with the weights of
     // the next k-step in flight while the current one is multiplied.
     const int q_beg = ks0 + (int)(((int64_t)KS * wave) / NW), q_end = ks0 + (int)(((int64_t)KS * (wave + 1)) / NW);
@@ -583,28 +589,38 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         int q = q_beg;
         for (; q + 2 <= q_end; q += 2) {
             mfma_load<TN>(wb, Wr, (q + 1) << 7);
-            mfma_kstep<TN>(wa, Xh, Xl, xrow, q << 7, acc);
+            mfma_kstep<TN, NP>(wa, Xp, xv, q << 7, acc);
             if (q + 2 < q_end)
                 mfma_load<TN>(wa, Wr, (q + 2) << 7);
-            mfma_kstep<TN>(wb, Xh, Xl, xrow, (q + 1) << 7, acc);
+            mfma_kstep<TN, NP>(wb, Xp, xv, (q + 1) << 7, acc);
         }
         if (q < q_end)
-            mfma_kstep<TN>(wa, Xh, Xl, xrow, q << 7, acc);
+            mfma_kstep<TN, NP>(wa, Xp, xv, q << 7, acc);
     }
 
-    // D[n_local][m]: lane l holds rows 4 (l / 16) + v, column l % 16.
+    // D[n_local][c]: lane l holds rows 4 (l / 16) + v, column l % 16.
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-            red[wave][16 * j + 4 * kg + v][r16] = acc[j][v];
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                red[wave][16 * j + 4 * kg + v][16 * p + r16] = acc[j][p][v];
     __syncthreads();
+    // fold the waves, then the terms (hi first): fin[n][m] = sum_t sum_w
     for (int o = tid; o < TN * 256; o += NW * 64) {
         const int ni = o >> 4, mi = o & 15;
         float v = 0.0f;
+        if (mi < M) {
 #pragma unroll
-        for (int w = 0; w < NW; ++w)
-            v += red[w][ni][mi];
+            for (int t = 0; t < X_TERMS; ++t) {
+                const int c = t * M + mi;
+                if (c < NP * 16)
+#pragma unroll
+                    for (int w = 0; w < NW; ++w)
+                        v += red[w][ni][c];
+            }
+        }
         fin[o] = v;
     }
     if (tid < 16)
@@ -620,12 +636,12 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 
 // ---------------------------------------------------------------------------
 // Activations for the MFMA path, once per forward: u = g * h / rms(h) (or
-// u = h without a gain), split into bf16 hi (top 16 bits) and lo (the rest,
-// rounded down to bf16).  One work-group per row.
+// u = h without a gain), split into X_TERMS bf16 planes.  One work-group per
+// row.
 
 template <typename TW>
 __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
-                                                    const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx,
+                                                    const DevCtl *ctl, uint16_t *xs, int64_t ldx,
                                                     const float *part, int n_part) {
     __shared__ float red[16];
     const int r = blockIdx.x;
@@ -671,7 +687,7 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
     for (int k = tid; k < K4; k += 1024) {
         const float4 v = hr[k];
         float u[4] = {v.x, v.y, v.z, v.w};
-        uint16_t hi[4], lo[4];
+        uint16_t t[X_TERMS][4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if (g) {
@@ -682,28 +698,33 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
                     gk = g[4 * k + e];
                 u[e] = gk * (u[e] * inv);
             }
-            split_hilo(u[e], hi[e], lo[e]);
+            const uint16_t hi = bf16_rne_bits(u[e]);
+            const float r1 = u[e] - bf2f(hi);
+            const uint16_t mid = bf16_rne_bits(r1);
+            t[0][e] = hi;
+            t[1][e] = mid;
+            t[2][e] = bf16_rne_bits(r1 - bf2f(mid));
         }
-        uint2 ph, pl;
-        ph.x = hi[0] | ((uint32_t)hi[1] << 16);
-        ph.y = hi[2] | ((uint32_t)hi[3] << 16);
-        pl.x = lo[0] | ((uint32_t)lo[1] << 16);
-        pl.y = lo[2] | ((uint32_t)lo[3] << 16);
-        *reinterpret_cast<uint2 *>(xh + (int64_t)r * ldx + 4 * k) = ph;
-        *reinterpret_cast<uint2 *>(xl + (int64_t)r * ldx + 4 * k) = pl;
+#pragma unroll
+        for (int i = 0; i < X_TERMS; ++i) {
+            uint2 pk;
+            pk.x = t[i][0] | ((uint32_t)t[i][1] << 16);
+            pk.y = t[i][2] | ((uint32_t)t[i][3] << 16);
+            *reinterpret_cast<uint2 *>(xs + (int64_t)(i * MAX_ROWS + r) * ldx + 4 * k) = pk;
+        }
     }
 }
 
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
-                            uint16_t *xh, uint16_t *xl, int64_t ldx, const float *part, int n_part, hipStream_t s) {
+                            uint16_t *xs, int64_t ldx, const float *part, int n_part, hipStream_t s) {
     if ((K & 3) || (ldh & 3) || (ldx & 3) || n_part > 8)
         return hipErrorInvalidValue;
     if (bf16)
         hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xh, xl, ldx, part, n_part);
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, ldx, part, n_part);
     else
         hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xh, xl, ldx, part, n_part);
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, ldx, part, n_part);
     return hipGetLastError();
 }
 
@@ -755,7 +776,7 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
     }
 }
 
-template <int TN, int NW>
+template <int TN, int NW, int NP>
 static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
     const int groups = (n_tiles + TN - 1) / TN;
     dim3 grid(groups * (epi == EPI_PARTIAL ? a.splits : 1)), block(NW * 64);
@@ -763,27 +784,41 @@ static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStre
     case EPI_PARTIAL:
         if (a.splits < 1 || !a.part)
             return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_linear_mfma<EPI_PARTIAL, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_PARTIAL, TN, NW, NP>), grid, block, 0, s, a);
         break;
     case EPI_STORE:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, TN, NW, NP>), grid, block, 0, s, a);
         break;
     case EPI_RESID:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, TN, NW, NP>), grid, block, 0, s, a);
         break;
     case EPI_SWIGLU:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, TN, NW, NP>), grid, block, 0, s, a);
         break;
     case EPI_QKV:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, TN, NW, NP>), grid, block, 0, s, a);
         break;
     case EPI_HEAD:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, TN, NW>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, TN, NW, NP>), grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+template <int TN, int NW>
+static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
+    switch (mfma_packs(a.max_rows)) {
+    case 1:
+        return launch_mfma<TN, NW, 1>(a, epi, n_tiles, s);
+    case 2:
+        return launch_mfma<TN, NW, 2>(a, epi, n_tiles, s);
+    case 3:
+        return launch_mfma<mfma_group_tiles(TN, 3), NW, 3>(a, epi, n_tiles, s);
+    default:
+        return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s) {
@@ -804,22 +839,12 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
             return hipErrorInvalidValue;
         LinearArgs b = a;
         b.n_tiles = n_tiles;
-        if (!a.Xh || !a.Xl)
+        if (!a.Xs || a.max_rows < 1 || a.max_rows > MAX_ROWS)
             return hipErrorInvalidValue;
-        if (TN == 1 && NW == 4)
-            return launch_mfma<1, 4>(b, epi, n_tiles, s);
-        if (TN == 1 && NW == 8)
-            return launch_mfma<1, 8>(b, epi, n_tiles, s);
-        if (TN == 1 && NW == 16)
-            return launch_mfma<1, 16>(b, epi, n_tiles, s);
         if (TN == 2 && NW == 4)
-            return launch_mfma<2, 4>(b, epi, n_tiles, s);
-        if (TN == 2 && NW == 8)
-            return launch_mfma<2, 8>(b, epi, n_tiles, s);
+            return launch_mfma_np<2, 4>(b, epi, n_tiles, s);
         if (TN == 4 && NW == 4)
-            return launch_mfma<4, 4>(b, epi, n_tiles, s);
-        if (TN == 4 && NW == 2)
-            return launch_mfma<4, 2>(b, epi, n_tiles, s);
+            return launch_mfma_np<4, 4>(b, epi, n_tiles, s);
         return hipErrorInvalidValue;
     }
     if (a.K & 7)

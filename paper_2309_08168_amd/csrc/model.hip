@@ -84,9 +84,9 @@ struct sd_model {
     float *part = nullptr;  // split-K partials of the MFMA output projections
 
     float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
-    // MFMA-path activations split into bf16 hi/lo, [MAX_ROWS][xld]: pair a holds
-    // normalised inputs and the attention output, pair b the SwiGLU output.
-    uint16_t *xa_h = nullptr, *xa_l = nullptr, *xb_h = nullptr, *xb_l = nullptr;
+    // MFMA-path activations as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][xld]:
+    // xa holds normalised inputs and the attention output, xb the SwiGLU output.
+    uint16_t *xa = nullptr, *xb = nullptr;
     int64_t xld = 0;
     float4 *head_part = nullptr;
     float *attn_o = nullptr;
@@ -105,9 +105,11 @@ struct sd_model {
     int32_t *d_log = nullptr;  // (k_e, n_e) pairs
     int d_log_cap = 0;         // int32 elements
     sd_kv_cache *gen_cache = nullptr;
+    std::vector<sd_kv_cache *> caches;  // caller-created caches, detached on destroy
     hipEvent_t ev[6] = {};
     // measurement hook (sd_model_time_kernel)
     int timed_kind = -1, timed_regime = 0;
+    int timed_rows_lo = 0, timed_rows_hi = 0;  // row bounds seen by the timed launches
     std::vector<hipEvent_t> tev;  // pairs
     size_t tev_used = 0;
     int64_t timed_launches = 0;
@@ -297,18 +299,19 @@ sd_status launch(hipError_t e, const char *what) {
     return SD_OK;
 }
 
-// One linear layer.  X (float32, with the RMSNorm gain folded in by the
-// VALU kernels) feeds the VALU paths; the MFMA path reads the bf16 hi/lo
-// pair xs (already normalised by k_prep_norm or split by the producer).
-sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, int64_t ldx, const void *gain,
-                     const EpiArgs &epi, const uint16_t *xs_h = nullptr, const uint16_t *xs_l = nullptr) {
+// One linear layer over up to max_rows rows.  X (float32, with the RMSNorm
+// gain folded in by the VALU kernels) feeds the VALU paths; the MFMA path
+// reads the bf16 term planes xs (already normalised by k_prep_norm or split
+// by the producer).
+sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, const float *X, int64_t ldx,
+                     const void *gain, const EpiArgs &epi, const uint16_t *xs) {
     LinearArgs a{};
     a.W = W;
     a.N = p.N;
     a.K = p.K;
     if (p.path == PATH_MFMA) {
-        a.Xh = xs_h;
-        a.Xl = xs_l;
+        a.Xs = xs;
+        a.max_rows = max_rows;
         a.ldx = m->xld;
     } else {
         a.X = X;
@@ -332,6 +335,8 @@ sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, 
             }
         }
         SD_HIP(hipEventRecord(m->tev[m->tev_used], m->stream));
+        m->timed_rows_lo = m->timed_rows_lo ? std::min(m->timed_rows_lo, max_rows) : max_rows;
+        m->timed_rows_hi = std::max(m->timed_rows_hi, max_rows);
     }
     SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer"));
     if (timed) {
@@ -343,13 +348,13 @@ sd_status run_linear(sd_model *m, const Plan &p, const void *W, const float *X, 
     return SD_OK;
 }
 
-// RMSNorm of h with gain into the hi/lo pair a (MFMA path only), after
+// RMSNorm of h with gain into the term planes xa (MFMA path only), after
 // folding the pending split-K partials of the last output projection.
 sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
     if (p.path != PATH_MFMA)
         return SD_OK;
-    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa_h,
-                                   m->xa_l, m->xld, m->part, pending, m->stream),
+    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa, m->xld,
+                                   m->part, pending, m->stream),
                   "norm"));
     pending = 0;
     return SD_OK;
@@ -389,7 +394,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
             SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l], pending));
-            SD_TRY(run_linear(m, P[LK_QKV], m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa_h, m->xa_l));
+            SD_TRY(run_linear(m, P[LK_QKV], max_rows, m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa));
             AttnArgs at{};
             at.q = m->q;
             at.ld_q = ldq;
@@ -401,8 +406,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             at.out = m->o;
             at.ld_out = ldq;
             if (P[LK_O].path == PATH_MFMA) {
-                at.out_hi = m->xa_h;
-                at.out_lo = m->xa_l;
+                at.out_x = m->xa;
                 at.ld_out = m->xld;
             }
             at.n_heads = c.n_heads;
@@ -414,7 +418,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             EpiArgs eo{};
             eo.out = m->h;
             eo.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_O], m->w_o[l], m->o, ldq, nullptr, eo, m->xa_h, m->xa_l));
+            SD_TRY(run_linear(m, P[LK_O], max_rows, m->w_o[l], m->o, ldq, nullptr, eo, m->xa));
             if (P[LK_O].epi == EPI_PARTIAL)
                 pending = P[LK_O].splits;
         }
@@ -424,16 +428,15 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             eg.ld_out = c.ffn_dim;
             eg.ffn = c.ffn_dim;
             if (P[LK_DOWN].path == PATH_MFMA) {
-                eg.out_hi = m->xb_h;
-                eg.out_lo = m->xb_l;
+                eg.out_x = m->xb;
                 eg.ld_out = m->xld;
             }
             SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l], pending));
-            SD_TRY(run_linear(m, P[LK_GATE_UP], m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa_h, m->xa_l));
+            SD_TRY(run_linear(m, P[LK_GATE_UP], max_rows, m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa));
             EpiArgs ed{};
             ed.out = m->h;
             ed.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_DOWN], m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb_h, m->xb_l));
+            SD_TRY(run_linear(m, P[LK_DOWN], max_rows, m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb));
             if (P[LK_DOWN].epi == EPI_PARTIAL)
                 pending = P[LK_DOWN].splits;
         }
@@ -450,7 +453,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.stage_log = m->d_log;
         eh.head.stage_log_cap = m->d_log_cap / 2;
         SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending));
-        SD_TRY(run_linear(m, P[LK_HEAD], m->lm_head, m->h, ldh, m->final_norm, eh, m->xa_h, m->xa_l));
+        SD_TRY(run_linear(m, P[LK_HEAD], max_rows, m->lm_head, m->h, ldh, m->final_norm, eh, m->xa));
     }
     return SD_OK;
 }
@@ -524,6 +527,25 @@ void destroy_cache(sd_kv_cache *c) {
     if (c->owns)
         dev_free(c->buf);
     delete c;
+}
+
+// Caches the caller creates are registered with their model; destroying the
+// model detaches them (model = nullptr) so that they can still be destroyed.
+sd_status create_user_cache(sd_model *m, int32_t cap, void *buf, sd_kv_cache **out) {
+    m->caches.reserve(m->caches.size() + 1);  // registration below cannot throw
+    SD_TRY(create_cache(m, cap, buf, out));
+    m->caches.push_back(*out);
+    return SD_OK;
+}
+
+void destroy_user_cache(sd_kv_cache *c) {
+    if (sd_model *m = c->model) {
+        (void)hipStreamSynchronize(m->stream);
+        auto it = std::find(m->caches.begin(), m->caches.end(), c);
+        if (it != m->caches.end())
+            m->caches.erase(it);
+    }
+    destroy_cache(c);
 }
 
 sd_status ensure_gen_cache(sd_model *m, int32_t cap) {
@@ -777,16 +799,16 @@ void destroy_model(sd_model *m) {
         return;
     if (m->stream)
         (void)hipStreamSynchronize(m->stream);
+    for (sd_kv_cache *c : m->caches)
+        c->model = nullptr;
     destroy_cache(m->gen_cache);
     dev_free(m->h);
     dev_free(m->q);
     dev_free(m->o);
     dev_free(m->mbuf);
     dev_free(m->part);
-    dev_free(m->xa_h);
-    dev_free(m->xa_l);
-    dev_free(m->xb_h);
-    dev_free(m->xb_l);
+    dev_free(m->xa);
+    dev_free(m->xb);
     dev_free(m->head_part);
     dev_free(m->attn_o);
     dev_free(m->attn_ml);
@@ -862,10 +884,8 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
     chain(dev_alloc(&m->part, (size_t)8 * MAX_ROWS * c.d_model));
     m->xld = std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
-    chain(dev_alloc(&m->xa_h, (size_t)MAX_ROWS * m->xld));
-    chain(dev_alloc(&m->xa_l, (size_t)MAX_ROWS * m->xld));
-    chain(dev_alloc(&m->xb_h, (size_t)MAX_ROWS * m->xld));
-    chain(dev_alloc(&m->xb_l, (size_t)MAX_ROWS * m->xld));
+    chain(dev_alloc(&m->xa, (size_t)X_TERMS * MAX_ROWS * m->xld));
+    chain(dev_alloc(&m->xb, (size_t)X_TERMS * MAX_ROWS * m->xld));
     chain(dev_alloc(&m->head_part, (size_t)max_head_tiles * MAX_ROWS));
     chain(dev_alloc(&m->ctl, 1));
     chain(dev_alloc(&m->st, 1));
@@ -907,9 +927,18 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
 std::string kernel_symbol(const sd_model *m, const Plan &p) {
     const char *tw = m->bf16 ? "unsigned short" : "float";
     const bool norm = p.kind == LK_QKV || p.kind == LK_GATE_UP || p.kind == LK_HEAD;
-    if (p.path == PATH_MFMA)
-        return "void sdk::k_linear_mfma<" + std::to_string(p.epi) + ", " + std::to_string(p.rows / 16) + ", " +
-               std::to_string(p.waves) + ">(sdk::LinearArgs)";
+    if (p.path == PATH_MFMA) {
+        // the packing count follows the row bound of each launch; name the
+        // widest one the timed launches used
+        const int hi = m->timed_rows_hi ? m->timed_rows_hi : MAX_ROWS;
+        const int np = mfma_packs(hi);
+        std::string nm = "void sdk::k_linear_mfma<" + std::to_string(p.epi) + ", " +
+                         std::to_string(mfma_group_tiles(p.rows / 16, np)) + ", " + std::to_string(p.waves) + ", " +
+                         std::to_string(np) + ">(sdk::LinearArgs)";
+        if (m->timed_rows_lo && mfma_packs(m->timed_rows_lo) != mfma_packs(hi))
+            nm += " (mixed packings)";
+        return nm;
+    }
     const int mr = p.path == PATH_GEMV ? 1 : (p.path == PATH_VALU2 ? 2 : (p.path == PATH_VALU4 ? 4 : 16));
     return std::string("void sdk::k_linear_valu<") + tw + ", " + std::to_string(mr) + ", " + std::to_string(p.rows) +
            ", " + std::to_string(p.epi) + ", " + (norm ? "true" : "false") + ">(sdk::LinearArgs)";
@@ -959,12 +988,12 @@ size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity) {
 
 sd_status sd_kv_cache_create(sd_model *model, int32_t capacity, void *device_buf, sd_kv_cache **out) {
     SD_GUARD(if (!model || !out) return fail(SD_ERR_INVALID_ARG, "model or out is null");
-             *out = nullptr; return create_cache(model, capacity, device_buf, out);)
+             *out = nullptr; return create_user_cache(model, capacity, device_buf, out);)
 }
 
 sd_status sd_kv_cache_destroy(sd_kv_cache *cache) {
     SD_GUARD(if (!cache) return fail(SD_ERR_INVALID_ARG, "cache is null");
-             (void)hipStreamSynchronize(cache->model->stream); destroy_cache(cache); return SD_OK;)
+             destroy_user_cache(cache); return SD_OK;)
 }
 
 int32_t sd_kv_cache_length(const sd_kv_cache *cache) { return cache ? cache->len : -1; }
@@ -1008,6 +1037,7 @@ sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows) {
              if (layer != -1 && !find_plan(model, layer, rows))
                  return fail(SD_ERR_INVALID_ARG, "layer must be -1 or 0..4 and rows 1, 2 or 16");
              model->timed_kind = layer; model->timed_regime = rows; model->tev_used = 0;
+             model->timed_rows_lo = 0; model->timed_rows_hi = 0;
              model->timed_launches = 0; model->timed_ms = 0.0; return SD_OK;)
 }
 

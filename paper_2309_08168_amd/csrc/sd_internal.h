@@ -20,6 +20,39 @@ constexpr int MAX_SPLITS = 1024;
 // Where and what the current forward computes.  Device resident: the
 // greedy head of one step writes the control block of the next step, so
 // the host never needs token ids or positions during decoding.
+// Activations of the MFMA path: a float32 value u is held as X_TERMS
+// bfloat16 terms hi + mid + lo, each the round-to-nearest-even of what the
+// previous terms leave; the remainders are exact in float32, so the three
+// terms reproduce every normal float32 value exactly.  A two-term split
+// (about 17 bits) lets the few-ulp differences it leaves in K/V flip their
+// bfloat16 rounding in the cache, and the flips compound with depth.
+constexpr int X_TERMS = 3;
+
+__device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// MFMAs per k-step (16 packed columns each) for up to max_rows rows.
+__host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * max_rows + 15) / 16; }
+
+// 16-row tiles per MFMA work-group for a plan's tn at a packing count: with
+// three packings four tiles of accumulators and double-buffered weights
+// leave one wave per SIMD, so those launches take two.
+__host__ __device__ constexpr int mfma_group_tiles(int tn, int np) { return np >= 3 && tn > 2 ? 2 : tn; }
+
+// Stores u as X_TERMS bf16 terms at x[t * plane + i].
+__device__ __forceinline__ void store_split3(uint16_t *x, int64_t plane, int64_t i, float u) {
+    const uint16_t hi = bf16_rne_bits(u);
+    const float r1 = u - __uint_as_float((uint32_t)hi << 16);
+    const uint16_t mid = bf16_rne_bits(r1);
+    const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
+    x[i] = hi;
+    x[plane + i] = mid;
+    x[2 * plane + i] = bf16_rne_bits(r2);
+}
+
 struct DevCtl {
     int32_t pos;               // position of row 0
     int32_t m;                 // rows in this forward, 1..MAX_ROWS
@@ -73,7 +106,7 @@ struct HeadArgs {
 struct EpiArgs {
     float *out;            // STORE/RESID: [m][ld_out]; SWIGLU: [m][ffn]
     int64_t ld_out;
-    uint16_t *out_hi, *out_lo;  // SWIGLU: when set, the output as split bf16 hi/lo [m][ld_out]
+    uint16_t *out_x;       // SWIGLU: when set, the output as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][ld_out]
     float *q;              // QKV: rotated queries [m][n_heads * head_dim]
     int64_t ld_q;
     void *kcache, *vcache; // QKV: this layer's K and V: [n_kv_heads][cap][head_dim]
@@ -87,7 +120,8 @@ struct LinearArgs {
     const void *W;         // [N][K] row-major, weight dtype
     int32_t N, K;
     const float *X;        // VALU paths: activations [m][ldx] float32
-    const uint16_t *Xh, *Xl;  // MFMA path: activations split into bf16 hi/lo [m][ldx]
+    const uint16_t *Xs;    // MFMA path: activations as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][ldx]
+    int32_t max_rows;      // MFMA path: host bound on ctl->m, sets the MFMAs per k-step
     int64_t ldx;
     const void *gain;      // RMSNorm gain [K] (weight dtype), or null: no norm
     float eps;
@@ -107,7 +141,7 @@ struct AttnArgs {
     float *part_o;         // [splits][n_heads][MAX_ROWS][head_dim]
     float2 *part_ml;       // [splits][n_heads][MAX_ROWS]: (running max, sum of exp)
     float *out;            // [m][n_heads * head_dim]
-    uint16_t *out_hi, *out_lo;  // when set, the output as split bf16 hi/lo instead
+    uint16_t *out_x;       // when set, the output as X_TERMS bf16 planes instead
     int64_t ld_out;
     int32_t n_heads, n_kv_heads, head_dim, splits;
     const DevCtl *ctl;
@@ -119,11 +153,11 @@ enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s);
-// Normalised (gain != null) or plain copy of h split into bf16 hi/lo for the MFMA path.
-// First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
+// Normalised (gain != null) or plain copy of h split into X_TERMS bf16 planes for the
+// MFMA path.  First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xh, uint16_t *xl, int64_t ldx, const float *part,
-                            int n_part, hipStream_t s);
+                            const DevCtl *ctl, uint16_t *xs, int64_t ldx, const float *part, int n_part,
+                            hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s);

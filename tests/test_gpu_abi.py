@@ -66,3 +66,19 @@ def test_caller_owned_cache_buffer(dm):
     kv = buf.view(cfg.n_layers, 2, cfg.n_kv_heads, 20, cfg.head_dim)
     assert torch.count_nonzero(kv[:, :, :, :6]).item() > 0
     assert torch.count_nonzero(kv[:, :, :, 6:]).item() == 0
+
+
+def test_cache_outlives_model():
+    """Destroying a model first detaches its caches; they can still be destroyed."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cfg = S.MODELS["tiny"]
+    m = U.device_model(cfg, S.make_weights(cfg, 0))
+    c = m.cache(8)
+    m.forward([1, 2], c)
+    m2 = U.device_model(cfg, S.make_weights(cfg, 0))
+    assert _status(m2.forward, [3], c) == binding.SD_ERR_INVALID_ARG  # another model's cache
+    m.close()
+    assert c.length == 2
+    c.close()  # after its model: must not touch the freed model
+    m2.close()

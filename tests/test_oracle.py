@@ -40,7 +40,7 @@ def test_forward_matches_library_built_model(cfg):
     assert _rel(got, ref) < 1e-10
 
 
-@pytest.mark.parametrize("cfg", [MICRO_GQA, S.MODELS["tiny"]], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [MICRO_GQA, MICRO_BF16, S.MODELS["tiny"]], ids=lambda c: c.name)
 def test_skipped_forward_matches_library_built_model(cfg):
     m, w = _model(cfg, seed=1)
     z = S.skip_mask(cfg, "random3", seed=5)

@@ -35,6 +35,8 @@ MUTATIONS = {
     "kcap": ("if (kcap > max_new - emitted - 1)\n            kcap = max_new - emitted - 1;",
              "if (kcap > max_new - emitted - 2)\n            kcap = max_new - emitted - 2 > 0 ? max_new - emitted - 2 : 0;"),
     "draft_input": ("int32_t in = j == 0 ? last : draft[j - 1];", "int32_t in = last;"),
+    "kv_not_rounded": ("if (m->c.wdtype != 1 || x == 0.0 || !isfinite(x))", "if (1)"),
+    "kv_round_7bits": ("return ldexp(rint(ldexp(f, 8)), e - 8);", "return ldexp(rint(ldexp(f, 7)), e - 7);"),
 }
 
 
@@ -48,6 +50,13 @@ def _pins_hold(lib_path) -> bool:
         got = m.score(toks)["logits"]
         ref = torch_ref.forward(cfg, S.weights_as_f64(cfg, w), toks)
         if not np.max(np.abs(got - ref)) <= 1e-10 * np.max(np.abs(ref)):  # NaN fails too
+            return False
+        cb = S.micro_config(n_layers=3, d_model=48, n_heads=2, n_kv_heads=1, head_dim=24, ffn_dim=80,
+                            vocab=61, dtype="bf16", name="micro_bf16")
+        wb = S.make_weights(cb, 0)
+        got = oracle.Model(cb, wb, lib_path=lib_path).score(toks[:15] % cb.vocab)["logits"]
+        ref = torch_ref.forward(cb, S.weights_as_f64(cb, wb), toks[:15] % cb.vocab)
+        if not np.max(np.abs(got - ref)) <= 1e-10 * np.max(np.abs(ref)):
             return False
         tiny = S.MODELS["tiny"]
         mt = oracle.Model(tiny, S.make_weights(tiny, 0), lib_path=lib_path)

@@ -55,6 +55,9 @@ def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0):
             q = rope(qkv[:, : H * dh].reshape(T, H, dh))
             k = rope(qkv[:, H * dh: (H + KVH) * dh].reshape(T, KVH, dh))
             v = qkv[:, (H + KVH) * dh:].reshape(T, KVH, dh)
+            if cfg.dtype == "bf16":  # the KV cache of a bf16 model holds bf16 values
+                k = k.to(torch.bfloat16).to(torch.float64)
+                v = v.to(torch.bfloat16).to(torch.float64)
             k = k.repeat_interleave(grp, dim=1)
             v = v.repeat_interleave(grp, dim=1)
             o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
