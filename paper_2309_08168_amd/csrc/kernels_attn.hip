@@ -44,14 +44,18 @@ __device__ __forceinline__ float wave_add(float v) {
     return v;
 }
 
-// One wave per (key chunk of CH keys, kv head g): flash-decoding without
-// LDS or barriers.  Lanes form 4 groups of 16; group j holds keys j, j + 4,
-// ..., j + CH - 4 of the chunk, and lane e16 of a group holds head_dim / 16
-// consecutive elements of q, K and V, so each K or V row is one coalesced
-// load by 16 lanes.  All K and V of the chunk are loaded into registers up
-// front; every group then scores its 16 keys for up to QB query vectors,
-// and the four groups' softmax states are merged by shuffles.  The chunk
-// leaves a partial state per (query, split) for the ordered combine.
+// One work-group per (chunk of ATTN_CHUNK keys, kv head g), split-KV
+// flash decoding.  Each of the AW waves takes 16 consecutive keys; its lanes
+// form 4 groups of 16, group j holds keys j, j + 4, j + 8, j + 12 and lane
+// e16 of a group holds head_dim / 16 consecutive elements of q, K and V, so
+// each K or V row is one coalesced load by 16 lanes.  A wave keeps its K and
+// V in registers (32 VGPRs for bf16 at head_dim 128), which leaves room for
+// several waves per SIMD: a decode step has only c * head_dim * 4 bytes of
+// KV per kv head to read, and small work-groups spread it over every CU.
+// For up to QB query vectors at a time, every group scores its 4 keys, the
+// four groups' softmax states merge by shuffles, the AW waves' states merge
+// in LDS in wave order, and the chunk leaves one partial state per (query,
+// split) for the ordered combine.
 template <typename TK, int ED>
 struct KvFrag {
     float v[ED];
@@ -87,33 +91,38 @@ struct KvFrag<uint16_t, 8> {
     }
 };
 
+constexpr int AW = 8;                  // waves per chunk
+constexpr int AKW = ATTN_CHUNK / AW;   // keys per wave
+static_assert(AKW == 16, "a wave holds 4 keys per lane group");
+
 template <typename TK, int ED>
-__global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
-    constexpr int CH = ATTN_CHUNK;
-    constexpr int KPG = CH / 4;  // keys per lane group
+__global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
+    constexpr int KPG = AKW / 4;  // keys per lane group
     constexpr int QB = 4;
+    __shared__ float red_o[AW][QB][MAX_HEAD_DIM];
+    __shared__ float2 red_ml[AW][QB];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int split = blockIdx.x * 4 + wave, g = blockIdx.y;
+    const int split = blockIdx.x, g = blockIdx.y;
     const int pos = a.ctl->pos, M = a.ctl->m;
     const int ctx = pos + M;
-    const int c0 = split * CH;
+    const int c0 = split * ATTN_CHUNK;
     if (c0 >= ctx)
-        return;
-    const int nk = min(CH, ctx - c0);
+        return;  // uniform over the work-group
     const int dh = a.head_dim, H = a.n_heads;
     const int G = H / a.n_kv_heads;
     const int Q = G * M;
     const int ks = lane >> 4, e16 = lane & 15;
-    const TK *Kg = reinterpret_cast<const TK *>(a.kcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh + e16 * ED;
-    const TK *Vg = reinterpret_cast<const TK *>(a.vcache) + (int64_t)g * a.kv_head_stride + (int64_t)c0 * dh + e16 * ED;
+    const int cw = c0 + wave * AKW;  // first key of this wave
+    const TK *Kg = reinterpret_cast<const TK *>(a.kcache) + (int64_t)g * a.kv_head_stride + (int64_t)cw * dh + e16 * ED;
+    const TK *Vg = reinterpret_cast<const TK *>(a.vcache) + (int64_t)g * a.kv_head_stride + (int64_t)cw * dh + e16 * ED;
     const float scale = 1.0f / sqrtf((float)dh);
 
     KvFrag<TK, ED> kf[KPG], vf[KPG];
 #pragma unroll
     for (int j = 0; j < KPG; ++j) {
         const int c = ks + 4 * j;
-        kf[j].load(Kg + (int64_t)c * dh, c < nk);
-        vf[j].load(Vg + (int64_t)c * dh, c < nk);
+        kf[j].load(Kg + (int64_t)c * dh, cw + c < ctx);
+        vf[j].load(Vg + (int64_t)c * dh, cw + c < ctx);
     }
 
     for (int qg = 0; qg < Q; qg += QB) {
@@ -128,7 +137,7 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < ED; ++e)
                 qv[e] = qs[e] * scale;
-            const int lim = pos + r - c0;  // last key row r sees, relative to the chunk
+            const int lim = pos + r - cw;  // last key row r sees, relative to the wave
             float s[KPG];
             float mx = -INFINITY;
 #pragma unroll
@@ -142,7 +151,7 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
                 t += __shfl_xor(t, 4, 64);
                 t += __shfl_xor(t, 8, 64);
                 const int c = ks + 4 * j;
-                s[j] = (c < nk && c <= lim) ? t : -INFINITY;
+                s[j] = (cw + c < ctx && c <= lim) ? t : -INFINITY;
                 mx = fmaxf(mx, s[j]);
             }
             float l = 0.0f, o[ED];
@@ -178,14 +187,40 @@ __global__ __launch_bounds__(256) void k_attn_split(AttnArgs a) {
                 }
             }
             if (ks == 0) {
-                const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
 #pragma unroll
                 for (int e = 0; e < ED; ++e)
-                    a.part_o[slot * dh + e16 * ED + e] = o[e];
+                    red_o[wave][qi][e16 * ED + e] = o[e];
                 if (e16 == 0)
-                    a.part_ml[slot] = make_float2(mx, l);
+                    red_ml[wave][qi] = make_float2(mx, l);
             }
         }
+        __syncthreads();
+        // merge the waves in wave order; one (query, element) per thread
+        for (int t = threadIdx.x; t < nq * dh; t += AW * 64) {
+            const int qi = t / dh, e = t - qi * dh;
+            float m = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < AW; ++w)
+                m = fmaxf(m, red_ml[w][qi].x);
+            float L = 0.0f, O = 0.0f;
+            if (m != -INFINITY) {
+#pragma unroll
+                for (int w = 0; w < AW; ++w) {
+                    const float2 ml = red_ml[w][qi];
+                    if (ml.x != -INFINITY) {
+                        const float wt = expf(ml.x - m);
+                        L = fmaf(wt, ml.y, L);
+                        O = fmaf(wt, red_o[w][qi][e], O);
+                    }
+                }
+            }
+            const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
+            const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
+            a.part_o[slot * dh + e] = O;
+            if (e == 0)
+                a.part_ml[slot] = make_float2(m, L);
+        }
+        __syncthreads();
     }
 }
 
@@ -412,7 +447,7 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
 
 template <typename TK>
 static hipError_t launch_attn_split(const AttnArgs &a, hipStream_t s) {
-    dim3 grid((a.splits + 3) / 4, a.n_kv_heads), block(256);
+    dim3 grid(a.splits, a.n_kv_heads), block(AW * 64);
     switch (a.head_dim) {
     case 16:
         hipLaunchKernelGGL((k_attn_split<TK, 1>), grid, block, 0, s, a);
@@ -460,7 +495,7 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
     const int G = a.n_heads / a.n_kv_heads;
     // one work-group per kv head while the context is short and the query
     // vectors per head fit; otherwise split the keys over work-groups
-    if (G * max_rows <= QH && a.splits <= 4)
+    if (G * max_rows <= QH && a.splits * ATTN_CHUNK <= 256)
         return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
     const hipError_t e = bf16 ? launch_attn_split<uint16_t>(a, s) : launch_attn_split<float>(a, s);
     if (e != hipSuccess)
@@ -537,12 +572,9 @@ __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc
     ctl->pos = lc;
     ctl->m = 1;
     ctl->tokens[0] = tok;
-    if (mb) {
-        __hip_atomic_store(&mb->phase, st->phase, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        __hip_atomic_store(&mb->gen_done, st->gen_done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        __hip_atomic_store(&mb->emitted, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        __hip_atomic_store(&mb->seq, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-    }
+    if (mb)
+        __hip_atomic_store(&mb->word, mb_pack(0, st->phase, st->gen_done, 0), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,

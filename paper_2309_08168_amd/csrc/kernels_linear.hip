@@ -139,10 +139,8 @@ __device__ __forceinline__ HeadPart head_comb(HeadPart a, HeadPart b) {
 
 __device__ void post_mailbox(DevState *st, Mailbox *mb) {
     st->seq += 1;
-    __hip_atomic_store(&mb->phase, st->phase, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    __hip_atomic_store(&mb->gen_done, st->gen_done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    __hip_atomic_store(&mb->emitted, st->emitted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    __hip_atomic_store(&mb->seq, st->seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->word, mb_pack(st->seq, st->phase, st->gen_done, st->emitted), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // The decoding decision after one step, taken by one thread once the
@@ -487,19 +485,16 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
 
 // ---------------------------------------------------------------------------
 // MFMA main loop (bf16 weights, up to 16 rows).  A work-group owns TN tiles
-// of 16 weight rows and the whole reduction dimension; its NW waves each
-// stream a contiguous range of 128-element k-steps and are summed in LDS at
-// the end, so no work-group depends on another.  A k-step is four 16x16x32
-// MFMAs per tile; for MFMA i, lane l supplies the 8 weights of row l % 16 at
-// k offset 32 i + 8 (l / 16), so one load instruction reads 64 contiguous
-// bytes of each of the 16 rows, and the next instruction the following 64
-// bytes of the same cache lines.  Lane l supplies the same 8 activations of
-// input row l % 16.  The k order inside an MFMA is a permutation shared by
-// both operands, so the dot products are unchanged.  Activations arrive
-// pre-split into a hi + lo pair of bf16 (k_prep_norm, or the producing
-// epilogue), two MFMAs per k-block, which keeps about 16 bits of their
-// mantissa; the weights are exact in bf16.  The loop body is loads and
-// MFMAs only.
+// of 16 weight rows and the whole reduction dimension (or one of S slices of
+// it); its NW waves each stream a contiguous range of 128-element k-steps
+// and are summed in LDS at the end, so no work-group depends on another.  A
+// k-step is four 16x16x32 MFMAs per tile and packing; for MFMA i, lane l
+// supplies the 8 weights of row l % 16 at k offset 32 i + 8 (l / 16), so one
+// load instruction reads 64 contiguous bytes of each of the 16 rows, and the
+// next instruction the following 64 bytes of the same cache lines.  The k
+// order inside an MFMA is a permutation shared by both operands, so the dot
+// products are unchanged.  Activations arrive as X_TERMS bf16 planes
+// (k_prep_norm, or the producing epilogue); the weights are exact in bf16.
 
 template <int TN>
 __device__ __forceinline__ void mfma_load(u32x4_t (&wv)[TN][4], const uint16_t *const (&Wr)[TN], int k0) {
@@ -510,29 +505,31 @@ __device__ __forceinline__ void mfma_load(u32x4_t (&wv)[TN][4], const uint16_t *
             wv[j][i] = *reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 32 * i);
 }
 
-// One k-step of 128: the packed activation columns against the weights
-// already in registers.
+// Activation fragments of one k-step of 128: for each packing p, this
+// lane's 8 bf16 of its (term, row) column at the four 32-wide slices.
+template <int NP>
+__device__ __forceinline__ void mfma_xload(u32x4_t (&xv4)[NP][4], const uint16_t *const (&Xp)[NP],
+                                           const bool (&xv)[NP], int k0) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            xv4[p][i] = xv[p] ? *reinterpret_cast<const u32x4_t *>(Xp[p] + k0 + 32 * i) : u32x4_t{0u, 0u, 0u, 0u};
+}
+
+// One k-step: TN x NP x 4 MFMAs on fragments already in registers.
 template <int TN, int NP>
-__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const uint16_t *const (&Xp)[NP],
-                                           const bool (&xv)[NP], int k0, floatx4_t (&acc)[TN][NP]) {
+__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const u32x4_t (&xv4)[NP][4],
+                                           floatx4_t (&acc)[TN][NP]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        bf16x8_t b[NP];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            u32x4_t v = {0u, 0u, 0u, 0u};
-            if (xv[p])
-                v = *reinterpret_cast<const u32x4_t *>(Xp[p] + k0 + 32 * i);
-            b[p] = __builtin_bit_cast(bf16x8_t, v);
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const bf16x8_t wb = __builtin_bit_cast(bf16x8_t, wv[j][i]);
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int p = 0; p < NP; ++p)
-                acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, b[p], acc[j][p], 0, 0, 0);
-        }
-    }
+                acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[j][i]),
+                                                                    __builtin_bit_cast(bf16x8_t, xv4[p][i]),
+                                                                    acc[j][p], 0, 0, 0);
 }
 
 // The 16 x NP columns of the B operand hold (term, row) pairs: column
@@ -580,22 +577,29 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 #pragma unroll
         for (int p = 0; p < NP; ++p)
             acc[j][p] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    // Each wave streams a contiguous range of k-steps with the weights of
-    // the next k-step in flight while the current one is multiplied.
+    // Each wave streams a contiguous range of k-steps with the weights and
+    // activations of the next k-step in flight while the current one is
+    // multiplied.  Both are issued together: loads complete in issue order,
+    // so activations requested after the next step's weights would make
+    // every step wait for those weights.
     const int q_beg = ks0 + (int)(((int64_t)KS * wave) / NW), q_end = ks0 + (int)(((int64_t)KS * (wave + 1)) / NW);
     if (q_beg < q_end) {
-        u32x4_t wa[TN][4], wb[TN][4];
+        u32x4_t wa[TN][4], wb[TN][4], xa[NP][4], xb[NP][4];
         mfma_load<TN>(wa, Wr, q_beg << 7);
+        mfma_xload<NP>(xa, Xp, xv, q_beg << 7);
         int q = q_beg;
         for (; q + 2 <= q_end; q += 2) {
             mfma_load<TN>(wb, Wr, (q + 1) << 7);
-            mfma_kstep<TN, NP>(wa, Xp, xv, q << 7, acc);
-            if (q + 2 < q_end)
+            mfma_xload<NP>(xb, Xp, xv, (q + 1) << 7);
+            mfma_kstep<TN, NP>(wa, xa, acc);
+            if (q + 2 < q_end) {
                 mfma_load<TN>(wa, Wr, (q + 2) << 7);
-            mfma_kstep<TN, NP>(wb, Xp, xv, (q + 1) << 7, acc);
+                mfma_xload<NP>(xa, Xp, xv, (q + 2) << 7);
+            }
+            mfma_kstep<TN, NP>(wb, xb, acc);
         }
         if (q < q_end)
-            mfma_kstep<TN, NP>(wa, Xp, xv, q << 7, acc);
+            mfma_kstep<TN, NP>(wa, xa, acc);
     }
 
     // D[n_local][c]: lane l holds rows 4 (l / 16) + v, column l % 16.
@@ -807,15 +811,29 @@ static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStre
     return hipGetLastError();
 }
 
-template <int TN, int NW>
+// The work-group shape follows the output kind and the packing count
+// (mfma_shape_tn / mfma_shape_nw).
 static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
-    switch (mfma_packs(a.max_rows)) {
+    const int np = mfma_packs(a.max_rows);
+    if (epi == EPI_PARTIAL) {
+        switch (np) {
+        case 1:
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 1), mfma_shape_nw(EPI_PARTIAL, 1), 1>(a, epi, n_tiles, s);
+        case 2:
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 2), mfma_shape_nw(EPI_PARTIAL, 2), 2>(a, epi, n_tiles, s);
+        case 3:
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 3), mfma_shape_nw(EPI_PARTIAL, 3), 3>(a, epi, n_tiles, s);
+        default:
+            return hipErrorInvalidValue;
+        }
+    }
+    switch (np) {
     case 1:
-        return launch_mfma<TN, NW, 1>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 1), mfma_shape_nw(EPI_STORE, 1), 1>(a, epi, n_tiles, s);
     case 2:
-        return launch_mfma<TN, NW, 2>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 2), mfma_shape_nw(EPI_STORE, 2), 2>(a, epi, n_tiles, s);
     case 3:
-        return launch_mfma<mfma_group_tiles(TN, 3), NW, 3>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 3), mfma_shape_nw(EPI_STORE, 3), 3>(a, epi, n_tiles, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -833,19 +851,15 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
     if (n_tiles <= 0)
         return hipSuccess;
     if (path == PATH_MFMA) {
-        // rows_per_tile = 16 * TN; n_tiles counts 16-row tiles.
-        const int TN = rows_per_tile / 16, NW = a.waves;
-        if (!bf16 || (a.K & 127) || rows_per_tile != 16 * TN)
+        // n_tiles counts 16-row tiles; the work-group shape is chosen here
+        (void)rows_per_tile;
+        if (!bf16 || (a.K & 127))
+            return hipErrorInvalidValue;
+        if (!a.Xs || a.max_rows < 1 || a.max_rows > MAX_ROWS)
             return hipErrorInvalidValue;
         LinearArgs b = a;
         b.n_tiles = n_tiles;
-        if (!a.Xs || a.max_rows < 1 || a.max_rows > MAX_ROWS)
-            return hipErrorInvalidValue;
-        if (TN == 2 && NW == 4)
-            return launch_mfma_np<2, 4>(b, epi, n_tiles, s);
-        if (TN == 4 && NW == 4)
-            return launch_mfma_np<4, 4>(b, epi, n_tiles, s);
-        return hipErrorInvalidValue;
+        return launch_mfma_np(b, epi, n_tiles, s);
     }
     if (a.K & 7)
         return hipErrorInvalidValue;

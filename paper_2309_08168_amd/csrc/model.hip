@@ -179,19 +179,19 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
             p.n_tiles = cdiv(c.ffn_dim, 8);
         else
             p.n_tiles = cdiv(p.N, 16);
+        // 16-row tiles; the work-group shape is picked per launch from the
+        // packing count (mfma_shape_tn / mfma_shape_nw)
+        p.rows = 16;
         if (kind == LK_O || kind == LK_DOWN) {
-            // Narrow outputs: two tiles per work-group and the reduction split
-            // over work-groups, the partial sums folded into the residual
-            // stream by the norm that reads it next (all readers of the
-            // residual stream must then be MFMA layers).
-            p.rows = 32;
+            // Narrow outputs: the reduction is split over work-groups and the
+            // partial sums are folded into the residual stream by the norm
+            // that reads it next (all readers of the residual stream must
+            // then be MFMA layers).
             const bool fold = mfma_ok(m, LK_QKV) && mfma_ok(m, LK_GATE_UP) && mfma_ok(m, LK_HEAD);
             if (fold) {
                 p.epi = EPI_PARTIAL;
                 p.splits = p.K >= 8192 ? 8 : 4;
             }
-        } else {
-            p.rows = 64;
         }
         return p;
     }
@@ -568,17 +568,23 @@ sd_status enqueue_prefill(sd_model *m, sd_kv_cache *kc, const int32_t *dev_token
     return SD_OK;
 }
 
-sd_status wait_mailbox(sd_model *m, int32_t seq) {
+// Waits until the mailbox shows step seq; *word receives what it holds.
+sd_status wait_mailbox(sd_model *m, int32_t seq, uint64_t *word) {
     uint64_t spins = 0;
     for (;;) {
-        const int32_t v = __atomic_load_n(&m->mb_host->seq, __ATOMIC_ACQUIRE);
-        if (v == seq)
+        const uint64_t w = __atomic_load_n(&m->mb_host->word, __ATOMIC_ACQUIRE);
+        if (mb_seq(w) == seq) {
+            *word = w;
             return SD_OK;
+        }
         if ((++spins & 1023u) == 0) {
             const hipError_t e = hipStreamQuery(m->stream);
             if (e == hipSuccess) {
-                if (__atomic_load_n(&m->mb_host->seq, __ATOMIC_ACQUIRE) == seq)
+                const uint64_t w2 = __atomic_load_n(&m->mb_host->word, __ATOMIC_ACQUIRE);
+                if (mb_seq(w2) == seq) {
+                    *word = w2;
                     return SD_OK;
+                }
                 return fail(SD_ERR_DEVICE, "decode step " + std::to_string(seq) +
                                                " finished without posting its result");
             }
@@ -669,7 +675,7 @@ sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     SD_TRY(enqueue_prefill(m, m->gen_cache, m->d_tokens, prompt_len - 1, 0));
     m->gen_cache->len = prompt_len - 1;
     SD_HIP(hipEventRecord(m->ev[1], m->stream));
-    __atomic_store_n(&m->mb_host->seq, -1, __ATOMIC_RELEASE);
+    __atomic_store_n(&m->mb_host->word, mb_pack(-1, 0, 0, 0), __ATOMIC_RELEASE);
     SD_TRY(launch(launch_init_decode(m->st, m->ctl, m->mb_dev, prompt_len - 1, m->d_tokens + prompt_len - 1,
                                      max_new, k_max, gamma, m->stream),
                   "decode setup"));
@@ -712,7 +718,8 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
         }
         SD_HIP(hipEventRecord(e1, m->stream));
         ++seq;
-        SD_TRY(wait_mailbox(m, seq));
+        uint64_t word = 0;
+        SD_TRY(wait_mailbox(m, seq, &word));
         // the previous step's events have completed: account for them
         if (prev_phase >= 0) {
             const float ms = elapsed(m->ev[2 + 2 * (1 - cur)], m->ev[3 + 2 * (1 - cur)]);
@@ -720,8 +727,8 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
         }
         prev_phase = phase;
         cur = 1 - cur;
-        phase = __atomic_load_n(&m->mb_host->phase, __ATOMIC_ACQUIRE);
-        done = __atomic_load_n(&m->mb_host->gen_done, __ATOMIC_ACQUIRE) != 0;
+        phase = mb_phase(word);
+        done = mb_done(word);
     }
     SD_TRY(copy_results(m, max_new, out_tokens, stats));
     if (prev_phase >= 0) {
@@ -933,8 +940,8 @@ std::string kernel_symbol(const sd_model *m, const Plan &p) {
         const int hi = m->timed_rows_hi ? m->timed_rows_hi : MAX_ROWS;
         const int np = mfma_packs(hi);
         std::string nm = "void sdk::k_linear_mfma<" + std::to_string(p.epi) + ", " +
-                         std::to_string(mfma_group_tiles(p.rows / 16, np)) + ", " + std::to_string(p.waves) + ", " +
-                         std::to_string(np) + ">(sdk::LinearArgs)";
+                         std::to_string(mfma_shape_tn(p.epi, np)) + ", " + std::to_string(mfma_shape_nw(p.epi, np)) +
+                         ", " + std::to_string(np) + ">(sdk::LinearArgs)";
         if (m->timed_rows_lo && mfma_packs(m->timed_rows_lo) != mfma_packs(hi))
             nm += " (mixed packings)";
         return nm;

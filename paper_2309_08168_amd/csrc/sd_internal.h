@@ -10,49 +10,16 @@ namespace sdk {
 // Rows of one forward: the verification of K_max <= 15 drafts plus the last
 // committed token, one 16-row MFMA tile, and the prefill chunk size.
 constexpr int MAX_ROWS = 16;
-// Keys per attention work-group (split-KV chunk).
-constexpr int ATTN_CHUNK = 64;
+// Keys per attention work-group (split-KV chunk): 8 waves of 16 keys.
+constexpr int ATTN_CHUNK = 128;
 // Largest head_dim the attention kernel stages in LDS.
 constexpr int MAX_HEAD_DIM = 128;
 // Most key chunks one attention call combines: 65536 positions.
-constexpr int MAX_SPLITS = 1024;
+constexpr int MAX_SPLITS = 512;
 
 // Where and what the current forward computes.  Device resident: the
 // greedy head of one step writes the control block of the next step, so
 // the host never needs token ids or positions during decoding.
-// Activations of the MFMA path: a float32 value u is held as X_TERMS
-// bfloat16 terms hi + mid + lo, each the round-to-nearest-even of what the
-// previous terms leave; the remainders are exact in float32, so the three
-// terms reproduce every normal float32 value exactly.  A two-term split
-// (about 17 bits) lets the few-ulp differences it leaves in K/V flip their
-// bfloat16 rounding in the cache, and the flips compound with depth.
-constexpr int X_TERMS = 3;
-
-__device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-// MFMAs per k-step (16 packed columns each) for up to max_rows rows.
-__host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * max_rows + 15) / 16; }
-
-// 16-row tiles per MFMA work-group for a plan's tn at a packing count: with
-// three packings four tiles of accumulators and double-buffered weights
-// leave one wave per SIMD, so those launches take two.
-__host__ __device__ constexpr int mfma_group_tiles(int tn, int np) { return np >= 3 && tn > 2 ? 2 : tn; }
-
-// Stores u as X_TERMS bf16 terms at x[t * plane + i].
-__device__ __forceinline__ void store_split3(uint16_t *x, int64_t plane, int64_t i, float u) {
-    const uint16_t hi = bf16_rne_bits(u);
-    const float r1 = u - __uint_as_float((uint32_t)hi << 16);
-    const uint16_t mid = bf16_rne_bits(r1);
-    const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
-    x[i] = hi;
-    x[plane + i] = mid;
-    x[2 * plane + i] = bf16_rne_bits(r2);
-}
-
 struct DevCtl {
     int32_t pos;               // position of row 0
     int32_t m;                 // rows in this forward, 1..MAX_ROWS
@@ -80,16 +47,68 @@ struct DevState {
     int64_t n_stages, n_drafted, n_accepted, n_draft_steps;
 };
 
-// Pinned host memory the GPU writes after every self-speculative step.
+// Pinned host memory the GPU writes after every self-speculative step: one
+// 64-bit word (step sequence number in bits 0-31, phase in 32-35, the
+// generation-done flag in bit 36, tokens emitted in 40-63), written by a
+// single relaxed store, so the host never sees a torn state and the GPU
+// needs no release fence (which would write back the whole L2).
 struct Mailbox {
-    int32_t seq, phase, gen_done, emitted;
+    uint64_t word;
 };
+
+__host__ __device__ inline uint64_t mb_pack(int32_t seq, int32_t phase, int32_t gen_done, int32_t emitted) {
+    return (uint64_t)(uint32_t)seq | ((uint64_t)(phase & 15) << 32) | ((uint64_t)(gen_done & 1) << 36) |
+           ((uint64_t)(emitted & 0xffffff) << 40);
+}
+__host__ __device__ inline int32_t mb_seq(uint64_t w) { return (int32_t)(uint32_t)(w & 0xffffffffu); }
+__host__ __device__ inline int32_t mb_phase(uint64_t w) { return (int32_t)((w >> 32) & 15); }
+__host__ __device__ inline bool mb_done(uint64_t w) { return ((w >> 36) & 1) != 0; }
 
 enum HeadMode : int32_t { HEAD_NONE = 0, HEAD_AR = 1, HEAD_DRAFT = 2, HEAD_VERIFY = 3 };
 
 // EPI_PARTIAL: split-K partial sums [split][row][N], folded into the
 // residual stream by the next k_prep_norm (MFMA path only).
 enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_HEAD = 4, EPI_PARTIAL = 5 };
+
+// Activations of the MFMA path: a float32 value u is held as X_TERMS
+// bfloat16 terms hi + mid + lo, each the round-to-nearest-even of what the
+// previous terms leave; the remainders are exact in float32, so the three
+// terms reproduce every normal float32 value exactly.  A two-term split
+// (about 17 bits) lets the few-ulp differences it leaves in K/V flip their
+// bfloat16 rounding in the cache, and the flips compound with depth.
+constexpr int X_TERMS = 3;
+
+__device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// MFMAs per k-step (16 packed columns each) for up to max_rows rows.
+__host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * max_rows + 15) / 16; }
+
+// MFMA work-group shape (16-row tiles per work-group, waves per work-group)
+// by output kind and packing count, from a sweep at the 13B shapes: the
+// split-K output projections take 2 tiles and 4 waves; the others take one
+// tile with 4 waves for one packing, four tiles with 4 waves for two, and
+// four tiles with 2 waves for three.
+__host__ __device__ constexpr int mfma_shape_tn(int epi, int np) {
+    return epi == EPI_PARTIAL ? 2 : (np == 1 ? 1 : 4);
+}
+__host__ __device__ constexpr int mfma_shape_nw(int epi, int np) {
+    return epi == EPI_PARTIAL ? 4 : (np == 3 ? 2 : 4);
+}
+
+// Stores u as X_TERMS bf16 terms at x[t * plane + i].
+__device__ __forceinline__ void store_split3(uint16_t *x, int64_t plane, int64_t i, float u) {
+    const uint16_t hi = bf16_rne_bits(u);
+    const float r1 = u - __uint_as_float((uint32_t)hi << 16);
+    const uint16_t mid = bf16_rne_bits(r1);
+    const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
+    x[i] = hi;
+    x[plane + i] = mid;
+    x[2 * plane + i] = bf16_rne_bits(r2);
+}
 
 struct HeadArgs {
     int32_t mode;
