@@ -24,3 +24,17 @@ def _built_helpers():
     if not os.path.exists(sd_synth._LIB_PATH):
         sd_synth.build()
     yield
+
+
+_MODEL_ORDER = {"7b": 0, "13b": 1, "70b": 2}
+
+
+def pytest_collection_modifyitems(config, items):
+    """Full-shape tests run grouped by model, so each model is built once."""
+    big = [i for i, it in enumerate(items) if it.get_closest_marker("big")]
+    if not big:
+        return
+    group = [items[i] for i in big]
+    group.sort(key=lambda it: _MODEL_ORDER.get(getattr(getattr(it, "callspec", None), "params", {}).get("name"), 9))
+    for i, it in zip(big, group):
+        items[i] = it
