@@ -383,7 +383,7 @@ __global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
         const float y = O / L;
         const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
         if (a.out_x) {
-            store_split3(a.out_x, (int64_t)MAX_ROWS * a.ld_out, oi, y);
+            store_split3(a.out_x, r, head * dh + e, M, y);
         } else {
             a.out[oi] = y;
         }
@@ -438,7 +438,7 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
         const float y = O / L;
         const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
         if (a.out_x) {
-            store_split3(a.out_x, (int64_t)MAX_ROWS * a.ld_out, oi, y);
+            store_split3(a.out_x, r, head * dh + e, M, y);
         } else {
             a.out[oi] = y;
         }

@@ -310,7 +310,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                 const float u = fin[(i + P) * MR + m] * inv[m];
                 const float y = g / (1.0f + expf(-g)) * u;
                 if (e.out_x) {
-                    store_split3(e.out_x, (int64_t)MAX_ROWS * e.ld_out, (int64_t)m * e.ld_out + f, y);
+                    store_split3(e.out_x, m, f, M, y);
                 } else {
                     e.out[(int64_t)m * e.ld_out + f] = y;
                 }
@@ -486,51 +486,21 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
 // ---------------------------------------------------------------------------
 // MFMA main loop (bf16 weights, up to 16 rows).  A work-group owns TN tiles
 // of 16 weight rows and the whole reduction dimension (or one of S slices of
-// it); its NW waves each stream a contiguous range of 128-element k-steps
-// and are summed in LDS at the end, so no work-group depends on another.  A
-// k-step is four 16x16x32 MFMAs per tile and packing; for MFMA i, lane l
-// supplies the 8 weights of row l % 16 at k offset 32 i + 8 (l / 16), so one
-// load instruction reads 64 contiguous bytes of each of the 16 rows, and the
-// next instruction the following 64 bytes of the same cache lines.  The k
-// order inside an MFMA is a permutation shared by both operands, so the dot
-// products are unchanged.  Activations arrive as X_TERMS bf16 planes
-// (k_prep_norm, or the producing epilogue); the weights are exact in bf16.
-
-template <int TN>
-__device__ __forceinline__ void mfma_load(u32x4_t (&wv)[TN][4], const uint16_t *const (&Wr)[TN], int k0) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            wv[j][i] = *reinterpret_cast<const u32x4_t *>(Wr[j] + k0 + 32 * i);
-}
-
-// Activation fragments of one k-step of 128: for each packing p, this
-// lane's 8 bf16 of its (term, row) column at the four 32-wide slices.
-template <int NP>
-__device__ __forceinline__ void mfma_xload(u32x4_t (&xv4)[NP][4], const uint16_t *const (&Xp)[NP],
-                                           const bool (&xv)[NP], int k0) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            xv4[p][i] = xv[p] ? *reinterpret_cast<const u32x4_t *>(Xp[p] + k0 + 32 * i) : u32x4_t{0u, 0u, 0u, 0u};
-}
-
-// One k-step: TN x NP x 4 MFMAs on fragments already in registers.
-template <int TN, int NP>
-__device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const u32x4_t (&xv4)[NP][4],
-                                           floatx4_t (&acc)[TN][NP]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int p = 0; p < NP; ++p)
-                acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv[j][i]),
-                                                                    __builtin_bit_cast(bf16x8_t, xv4[p][i]),
-                                                                    acc[j][p], 0, 0, 0);
-}
+// it); its NW waves take every NW-th 128-element k-step, so at any time the
+// work-group reads adjacent pieces of its rows, and are summed in LDS at the
+// end: no work-group depends on another.
+//
+// The MFMA operand layout puts weight row l % 16 in lane l, so loading it
+// straight from memory gives every lane its own cache line and defeats the
+// coalescing of neighbouring lanes (one L1 access per lane instead of one
+// per four).  Weights are therefore loaded coalesced (16 lanes per 256-byte
+// row slice), non-temporal (they are read once), and transposed through a
+// wave-private LDS tile whose 16-byte chunks are XOR-swizzled by row, which
+// keeps both the writes and the fragment reads free of bank conflicts.
+// The activations come pre-split (three bf16 terms) in fragment order
+// (xfrag_off), so each B operand is one contiguous 1 KB load.  A k-step is
+// four 16x16x32 MFMAs per tile and packing; the k order inside an MFMA is a
+// permutation shared by both operands, so the dot products are unchanged.
 
 // The 16 x NP columns of the B operand hold (term, row) pairs: column
 // c = t * M + r carries term t of activation row r, so NP = ceil(3 M / 16)
@@ -539,7 +509,10 @@ __device__ __forceinline__ void mfma_kstep(const u32x4_t (&wv)[TN][4], const u32
 // M (LinearArgs::max_rows).
 template <int EPI, int TN, int NW, int NP>
 __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
-    __shared__ float red[NW][TN * 16][NP * 16 + 1];
+    constexpr int WL = TN * 16 * 128;                // bf16 staging per wave
+    constexpr int RC = NP * 16 + 1;                  // reduction row length
+    constexpr size_t SMEM_W = (size_t)NW * WL * 2, SMEM_R = (size_t)NW * TN * 16 * RC * 4;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM_W > SMEM_R ? SMEM_W : SMEM_R];
     __shared__ float fin[TN * 16 * 16];
     __shared__ float inv_s[16];
     const int S = EPI == EPI_PARTIAL ? a.splits : 1;
@@ -548,28 +521,24 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     const int r16 = lane & 15, kg = lane >> 4;
     const int M = a.ctl->m;
     const int n_tiles = a.n_tiles;
-    const uint16_t *Wr[TN];
+    uint16_t *wl = reinterpret_cast<uint16_t *>(smem) + wave * WL;
+    // coalesced loads: instruction ii of tile j reads rows 4 ii + lane / 16,
+    // 16-byte chunk lane % 16 of the k-step's 256-byte slice
+    const int lrow = lane >> 4, lch = lane & 15;
+    uint32_t woff[TN][4];
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int t = grp * TN + j;
-        const bool nv = t < n_tiles && row_valid<EPI>(t, r16, 16, a.N, a.epi);
-        const int n = nv ? tile_row<EPI>(t, r16, 16, a.epi) : 0;
-        Wr[j] = reinterpret_cast<const uint16_t *>(a.W) + (int64_t)n * a.K + kg * 8;
-    }
-    const int64_t plane = (int64_t)MAX_ROWS * a.ldx;
-    const uint16_t *Xp[NP];
-    bool xv[NP];
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-        const int c = 16 * p + r16;
-        const int t = M > 0 ? c / M : X_TERMS;
-        xv[p] = t < X_TERMS;
-        const int r = xv[p] ? c - t * M : 0;
-        Xp[p] = a.Xs + (xv[p] ? t : 0) * plane + (int64_t)r * a.ldx + kg * 8;
-    }
-    // k-steps of this split, shared out among the waves
+        for (int ii = 0; ii < 4; ++ii) {
+            const int t = grp * TN + j, row = 4 * ii + lrow;
+            const bool nv = t < n_tiles && row_valid<EPI>(t, row, 16, a.N, a.epi);
+            woff[j][ii] = (uint32_t)(nv ? tile_row<EPI>(t, row, 16, a.epi) : 0) * (uint32_t)a.K + lch * 8;
+        }
+    const uint16_t *W = reinterpret_cast<const uint16_t *>(a.W);
+    const uint16_t *X = a.Xs + lane * 8;
+    // k-steps of this split, dealt out to the waves in turn
     const int KS_all = a.K >> 7;
-    const int ks0 = (int)(((int64_t)KS_all * sp) / S), KS = (int)(((int64_t)KS_all * (sp + 1)) / S) - ks0;
+    const int ks0 = (int)(((int64_t)KS_all * sp) / S), ks1 = (int)(((int64_t)KS_all * (sp + 1)) / S);
 
     floatx4_t acc[TN][NP];
 #pragma unroll
@@ -577,39 +546,70 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 #pragma unroll
         for (int p = 0; p < NP; ++p)
             acc[j][p] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    // Each wave streams a contiguous range of k-steps with the weights and
-    // activations of the next k-step in flight while the current one is
-    // multiplied.  Both are issued together: loads complete in issue order,
-    // so activations requested after the next step's weights would make
-    // every step wait for those weights.
-    const int q_beg = ks0 + (int)(((int64_t)KS * wave) / NW), q_end = ks0 + (int)(((int64_t)KS * (wave + 1)) / NW);
-    if (q_beg < q_end) {
-        u32x4_t wa[TN][4], wb[TN][4], xa[NP][4], xb[NP][4];
-        mfma_load<TN>(wa, Wr, q_beg << 7);
-        mfma_xload<NP>(xa, Xp, xv, q_beg << 7);
-        int q = q_beg;
-        for (; q + 2 <= q_end; q += 2) {
-            mfma_load<TN>(wb, Wr, (q + 1) << 7);
-            mfma_xload<NP>(xb, Xp, xv, (q + 1) << 7);
-            mfma_kstep<TN, NP>(wa, xa, acc);
-            if (q + 2 < q_end) {
-                mfma_load<TN>(wa, Wr, (q + 2) << 7);
-                mfma_xload<NP>(xa, Xp, xv, (q + 2) << 7);
+    u32x4_t wv[TN][4], xv[NP][4];
+    auto load = [&](int q) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii)
+                wv[j][ii] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(W + woff[j][ii] + (q << 7)));
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                xv[p][i] = *reinterpret_cast<const u32x4_t *>(X + ((((int64_t)q * X_PACKS_MAX + p) * 4 + i) << 9));
+    };
+    int q = ks0 + wave;
+    if (q < ks1)
+        load(q);
+    for (; q < ks1; q += NW) {
+        // this k-step's weights into the staging tile; its activations stay
+        // in registers while the next k-step's loads go out
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                const int row = 4 * ii + lrow;
+                *reinterpret_cast<u32x4_t *>(wl + j * 2048 + row * 128 + ((lch ^ row) << 3)) = wv[j][ii];
             }
-            mfma_kstep<TN, NP>(wb, xb, acc);
+        u32x4_t xc[NP][4];
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                xc[p][i] = xv[p][i];
+        if (q + NW < ks1)
+            load(q + NW);
+        // the staging tile is private to this wave, whose LDS accesses run in
+        // program order; the fences only keep the compiler from reordering them
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ch = (4 * i + kg) ^ r16;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const u32x4_t w = *reinterpret_cast<const u32x4_t *>(wl + j * 2048 + r16 * 128 + (ch << 3));
+#pragma unroll
+                for (int p = 0; p < NP; ++p)
+                    acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
+                                                                        __builtin_bit_cast(bf16x8_t, xc[p][i]),
+                                                                        acc[j][p], 0, 0, 0);
+            }
         }
-        if (q < q_end)
-            mfma_kstep<TN, NP>(wa, xa, acc);
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
 
-    // D[n_local][c]: lane l holds rows 4 (l / 16) + v, column l % 16.
+    // D[n_local][c]: lane l holds rows 4 (l / 16) + v, column l % 16.  The
+    // reduction reuses the staging memory once every wave is done with it.
+    __syncthreads();
+    float *red = reinterpret_cast<float *>(smem);
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int p = 0; p < NP; ++p)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                red[wave][16 * j + 4 * kg + v][16 * p + r16] = acc[j][p][v];
+                red[(wave * TN * 16 + 16 * j + 4 * kg + v) * RC + 16 * p + r16] = acc[j][p][v];
     __syncthreads();
     // fold the waves, then the terms (hi first): fin[n][m] = sum_t sum_w
     for (int o = tid; o < TN * 256; o += NW * 64) {
@@ -622,7 +622,7 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
                 if (c < NP * 16)
 #pragma unroll
                     for (int w = 0; w < NW; ++w)
-                        v += red[w][ni][c];
+                        v += red[(w * TN * 16 + ni) * RC + c];
             }
         }
         fin[o] = v;
@@ -640,16 +640,16 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 
 // ---------------------------------------------------------------------------
 // Activations for the MFMA path, once per forward: u = g * h / rms(h) (or
-// u = h without a gain), split into X_TERMS bf16 planes.  One work-group per
-// row.
+// u = h without a gain), split into X_TERMS bf16 terms in fragment layout.
+// One work-group per row.
 
 template <typename TW>
 __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
-                                                    const DevCtl *ctl, uint16_t *xs, int64_t ldx,
-                                                    const float *part, int n_part) {
+                                                    const DevCtl *ctl, uint16_t *xs, const float *part,
+                                                    int n_part) {
     __shared__ float red[16];
-    const int r = blockIdx.x;
-    if (r >= ctl->m)
+    const int r = blockIdx.x, M = ctl->m;
+    if (r >= M)
         return;
     const int tid = threadIdx.x;
     float4 *hr = reinterpret_cast<float4 *>(h + (int64_t)r * ldh);
@@ -709,26 +709,27 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
             t[1][e] = mid;
             t[2][e] = bf16_rne_bits(r1 - bf2f(mid));
         }
+        // four consecutive k stay contiguous in the fragment layout
 #pragma unroll
         for (int i = 0; i < X_TERMS; ++i) {
             uint2 pk;
             pk.x = t[i][0] | ((uint32_t)t[i][1] << 16);
             pk.y = t[i][2] | ((uint32_t)t[i][3] << 16);
-            *reinterpret_cast<uint2 *>(xs + (int64_t)(i * MAX_ROWS + r) * ldx + 4 * k) = pk;
+            *reinterpret_cast<uint2 *>(xs + xfrag_off(i, r, 4 * k, M)) = pk;
         }
     }
 }
 
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
-                            uint16_t *xs, int64_t ldx, const float *part, int n_part, hipStream_t s) {
-    if ((K & 3) || (ldh & 3) || (ldx & 3) || n_part > 8)
+                            uint16_t *xs, const float *part, int n_part, hipStream_t s) {
+    if ((K & 127) || (ldh & 3) || n_part > 8)
         return hipErrorInvalidValue;
     if (bf16)
         hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, ldx, part, n_part);
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part);
     else
         hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, ldx, part, n_part);
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part);
     return hipGetLastError();
 }
 
@@ -856,6 +857,8 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
         if (!bf16 || (a.K & 127))
             return hipErrorInvalidValue;
         if (!a.Xs || a.max_rows < 1 || a.max_rows > MAX_ROWS)
+            return hipErrorInvalidValue;
+        if ((int64_t)a.N * a.K >= ((int64_t)1 << 32))  // 32-bit weight offsets
             return hipErrorInvalidValue;
         LinearArgs b = a;
         b.n_tiles = n_tiles;

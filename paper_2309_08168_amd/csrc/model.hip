@@ -84,8 +84,9 @@ struct sd_model {
     float *part = nullptr;  // split-K partials of the MFMA output projections
 
     float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
-    // MFMA-path activations as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][xld]:
-    // xa holds normalised inputs and the attention output, xb the SwiGLU output.
+    // MFMA-path activations split into X_TERMS bf16 terms in fragment layout
+    // (48 xld elements each): xa holds normalised inputs and the attention
+    // output, xb the SwiGLU output.
     uint16_t *xa = nullptr, *xb = nullptr;
     int64_t xld = 0;
     float4 *head_part = nullptr;
@@ -353,8 +354,8 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
 sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
     if (p.path != PATH_MFMA)
         return SD_OK;
-    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa, m->xld,
-                                   m->part, pending, m->stream),
+    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa, m->part,
+                                   pending, m->stream),
                   "norm"));
     pending = 0;
     return SD_OK;

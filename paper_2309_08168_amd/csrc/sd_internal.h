@@ -88,26 +88,42 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
 __host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * max_rows + 15) / 16; }
 
 // MFMA work-group shape (16-row tiles per work-group, waves per work-group)
-// by output kind and packing count, from a sweep at the 13B shapes: the
-// split-K output projections take 2 tiles and 4 waves; the others take one
-// tile with 4 waves for one packing, four tiles with 4 waves for two, and
-// four tiles with 2 waves for three.
+// by output kind and packing count, from a sweep at the 13B shapes: two
+// tiles for one packing and for the split-K output projections, four tiles
+// for two or three packings; four waves throughout.
 __host__ __device__ constexpr int mfma_shape_tn(int epi, int np) {
-    return epi == EPI_PARTIAL ? 2 : (np == 1 ? 1 : 4);
+    return epi == EPI_PARTIAL ? 2 : (np == 1 ? 2 : 4);
 }
-__host__ __device__ constexpr int mfma_shape_nw(int epi, int np) {
-    return epi == EPI_PARTIAL ? 4 : (np == 3 ? 2 : 4);
+__host__ __device__ constexpr int mfma_shape_nw(int epi, int np) { return (void)epi, (void)np, 4; }
+
+// Fragment layout of the MFMA-path activations.  For k-step q = k / 128,
+// packing p and 32-wide slice i = (k % 128) / 32, the 16 columns x 32 k of
+// one MFMA B operand are 512 contiguous bf16 in lane order: lane
+// column + 16 ((k % 32) / 8) holds 8 consecutive k.  Column c = t M + r
+// carries term t of row r (M rows in this forward).  X_PACKS_MAX packings
+// are reserved per k-step, so a buffer holds 48 K elements for any M, and
+// an MFMA operand is one coalesced 1 KB load.
+constexpr int X_PACKS_MAX = 3;
+__host__ __device__ inline int64_t xfrag_off(int t, int r, int k, int M) {
+    const int c = t * M + r, p = c >> 4, lane = (c & 15) + 16 * ((k & 31) >> 3);
+    return ((((int64_t)(k >> 7) * X_PACKS_MAX + p) * 4 + ((k & 127) >> 5)) << 9) + lane * 8 + (k & 7);
 }
 
-// Stores u as X_TERMS bf16 terms at x[t * plane + i].
-__device__ __forceinline__ void store_split3(uint16_t *x, int64_t plane, int64_t i, float u) {
-    const uint16_t hi = bf16_rne_bits(u);
-    const float r1 = u - __uint_as_float((uint32_t)hi << 16);
-    const uint16_t mid = bf16_rne_bits(r1);
-    const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
-    x[i] = hi;
-    x[plane + i] = mid;
-    x[2 * plane + i] = bf16_rne_bits(r2);
+// Splits u into X_TERMS bf16 terms.
+__device__ __forceinline__ void split3(float u, uint16_t (&t)[X_TERMS]) {
+    t[0] = bf16_rne_bits(u);
+    const float r1 = u - __uint_as_float((uint32_t)t[0] << 16);
+    t[1] = bf16_rne_bits(r1);
+    t[2] = bf16_rne_bits(r1 - __uint_as_float((uint32_t)t[1] << 16));
+}
+
+// Stores the terms of activation (row r, index k) of an M-row forward.
+__device__ __forceinline__ void store_split3(uint16_t *x, int r, int k, int M, float u) {
+    uint16_t t[X_TERMS];
+    split3(u, t);
+#pragma unroll
+    for (int i = 0; i < X_TERMS; ++i)
+        x[xfrag_off(i, r, k, M)] = t[i];
 }
 
 struct HeadArgs {
@@ -125,7 +141,7 @@ struct HeadArgs {
 struct EpiArgs {
     float *out;            // STORE/RESID: [m][ld_out]; SWIGLU: [m][ffn]
     int64_t ld_out;
-    uint16_t *out_x;       // SWIGLU: when set, the output as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][ld_out]
+    uint16_t *out_x;       // SWIGLU: when set, the output split into bf16 terms in fragment layout (xfrag_off)
     float *q;              // QKV: rotated queries [m][n_heads * head_dim]
     int64_t ld_q;
     void *kcache, *vcache; // QKV: this layer's K and V: [n_kv_heads][cap][head_dim]
@@ -139,7 +155,7 @@ struct LinearArgs {
     const void *W;         // [N][K] row-major, weight dtype
     int32_t N, K;
     const float *X;        // VALU paths: activations [m][ldx] float32
-    const uint16_t *Xs;    // MFMA path: activations as X_TERMS bf16 planes [X_TERMS][MAX_ROWS][ldx]
+    const uint16_t *Xs;    // MFMA path: activations split into bf16 terms in fragment layout (xfrag_off)
     int32_t max_rows;      // MFMA path: host bound on ctl->m, sets the MFMAs per k-step
     int64_t ldx;
     const void *gain;      // RMSNorm gain [K] (weight dtype), or null: no norm
@@ -160,7 +176,7 @@ struct AttnArgs {
     float *part_o;         // [splits][n_heads][MAX_ROWS][head_dim]
     float2 *part_ml;       // [splits][n_heads][MAX_ROWS]: (running max, sum of exp)
     float *out;            // [m][n_heads * head_dim]
-    uint16_t *out_x;       // when set, the output as X_TERMS bf16 planes instead
+    uint16_t *out_x;       // when set, the output split into bf16 terms in fragment layout instead
     int64_t ld_out;
     int32_t n_heads, n_kv_heads, head_dim, splits;
     const DevCtl *ctl;
@@ -172,11 +188,10 @@ enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s);
-// Normalised (gain != null) or plain copy of h split into X_TERMS bf16 planes for the
-// MFMA path.  First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
+// Normalised (gain != null) or plain copy of h split into X_TERMS bf16 terms in
+// fragment layout for the MFMA path (K a multiple of 128).  First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xs, int64_t ldx, const float *part, int n_part,
-                            hipStream_t s);
+                            const DevCtl *ctl, uint16_t *xs, const float *part, int n_part, hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s);
