@@ -300,7 +300,8 @@ def run_verify_micro(args):
             ms = float(np.median(times))
             nbytes = step_bytes(cfg, None, ctx, M)
             useful = 2.0 * params * M
-            issued = 2.0 * params * 16 * 2 if M > 2 else 0.0  # MFMA path: 16 padded rows, hi + lo
+            # MFMA path: ceil(3 M / 16) packings of 16 columns (three bf16 terms per row)
+            issued = 2.0 * params * 16 * ((3 * M + 15) // 16) if M > 2 else 0.0
             r = {"rows": M, "ctx": ctx, "ms": round(ms, 4), "GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
                  "frac_hbm": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
                  "mfma_useful_frac": round(useful / (ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
@@ -336,13 +337,36 @@ def run_supplementary(args):
         model.generate_ar(prompt, max_new)
         sd_tok, sd = model.generate_sd(prompt, max_new, skip, wl.k_max, gamma)
         ar_tok, ar = model.generate_ar(prompt, max_new)
+        n_st, n_dr = max(sd["n_stages"], 1), max(sd["n_draft_steps"], 1)
         r = {"rho": rho, "head_gain": gain, "gamma": gamma,
              "sd_tokens_per_s": round(max_new / (sd["decode_ms"] / 1e3), 2),
              "ar_tokens_per_s": round(max_new / (ar["decode_ms"] / 1e3), 2),
              "speedup": round(ar["decode_ms"] / sd["decode_ms"], 4),
              "acceptance": round(sd["n_accepted"] / max(sd["n_drafted"], 1), 4),
-             "tokens_per_stage": round(max_new / max(sd["n_stages"], 1), 3),
+             "tokens_per_stage": round(max_new / n_st, 3),
+             "draft_steps": sd["n_draft_steps"], "stages": sd["n_stages"],
+             "draft_step_ms": round(sd["draft_ms"] / n_dr, 4),
+             "verify_step_ms": round(sd["verify_ms"] / n_st, 4),
+             "verify_mean_rows": round((sd["n_drafted"] + sd["n_stages"]) / n_st, 3),
+             "host_gap_ms_per_step": round((sd["decode_ms"] - sd["draft_ms"] - sd["verify_ms"]) /
+                                           (sd["n_stages"] + sd["n_draft_steps"]), 4),
+             "ar_step_ms": round(ar["decode_ms"] / max_new, 4),
              "tokens_equal": int(np.sum(sd_tok == ar_tok))}
+        d = np.nonzero(sd_tok != ar_tok)[0]
+        if d.size:
+            # the two agree up to d; the GPU's own logits there decide whether
+            # the split is a near-tie (the tolerance of the parity tests)
+            d = int(d[0])
+            seq = np.concatenate([prompt, ar_tok[:d]]).astype(np.int32)
+            c = model.cache(len(seq) + 1)
+            model.forward(seq[:-1], c)
+            lg = torch.empty((1, cfg.vocab), dtype=torch.float32, device="cuda")
+            model.forward(seq[-1:], c, logits=lg)
+            lg = lg[0].cpu().numpy()
+            top2 = np.sort(lg)[-2:]
+            c.close()
+            r.update({"first_divergence": d, "gpu_top2_margin": round(float(top2[1] - top2[0]), 5),
+                      "near_tie_tau": round(float(2 * 3e-2 * lg.std()), 5)})
         out.append(r)
         log(json.dumps(r))
         model.close()

@@ -46,6 +46,17 @@ class _Weights(ctypes.Structure):
     ]
 
 
+class Adaptive(ctypes.Structure):
+    """Adaptive draft-exit parameters (Sec. 3.4, Eqs. 2-4)."""
+
+    _fields_ = [(n, ctypes.c_double) for n in ("gamma0", "alpha", "epsilon", "beta1", "beta2")]
+
+
+# The paper's settings (appendix table of hyperparameters): gamma0 0.6,
+# epsilon 0.01, beta1 0.5, beta2 0.9; alpha 0.90 for LLaMA-2-13B on CNN/DM.
+PAPER_ADAPTIVE = dict(gamma0=0.6, alpha=0.9, epsilon=0.01, beta1=0.5, beta2=0.9)
+
+
 class SDStats(ctypes.Structure):
     _fields_ = [
         ("n_stages", ctypes.c_int64), ("n_drafted", ctypes.c_int64), ("n_accepted", ctypes.c_int64),
@@ -73,7 +84,10 @@ def _load(path: str = LIB_PATH):
         lib.orc_forward.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, vp]
         lib.orc_generate_ar.argtypes = [vp, vp, i32, i32, vp, vp]
         lib.orc_generate_sd.argtypes = [vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, vp, p(SDStats), vp, vp]
-        for fn in ("orc_cache_truncate", "orc_cache_load", "orc_forward", "orc_generate_ar", "orc_generate_sd"):
+        lib.orc_generate_sd_adaptive.argtypes = [vp, vp, i32, i32, vp, i32, p(Adaptive), vp, vp, p(SDStats), vp,
+                                                 vp, vp]
+        for fn in ("orc_cache_truncate", "orc_cache_load", "orc_forward", "orc_generate_ar", "orc_generate_sd",
+                   "orc_generate_sd_adaptive"):
             getattr(lib, fn).restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
@@ -168,6 +182,29 @@ class Model:
             "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
             "draft_pmax": pm[: st.n_draft_steps].copy(), "n_stages": st.n_stages, "n_drafted": st.n_drafted,
             "n_accepted": st.n_accepted, "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
+        }
+
+    def generate_sd_adaptive(self, prompt, max_new: int, skip, k_max: int, **params):
+        """Self-speculative decoding with the adaptive threshold; params are
+        gamma0, alpha, epsilon, beta1, beta2 (defaults: PAPER_ADAPTIVE)."""
+        ad = Adaptive(**{**PAPER_ADAPTIVE, **params})
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        out = np.empty(max_new, np.int32)
+        margin = np.empty(max_new, np.float64)
+        log = np.zeros((max(max_new, 1), 2), np.int32)
+        pm = np.zeros(max(max_new * max(k_max, 1), 1), np.float32)
+        glog = np.zeros(max(max_new, 1), np.float32)
+        st = SDStats()
+        _check(self._lib.orc_generate_sd_adaptive(self._h, pr.ctypes.data, pr.size, max_new, _ptr(sk), k_max,
+                                                ctypes.byref(ad), out.ctypes.data, margin.ctypes.data,
+                                                ctypes.byref(st), log.ctypes.data, pm.ctypes.data,
+                                                glog.ctypes.data), "orc_generate_sd_adaptive")
+        return {
+            "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
+            "draft_pmax": pm[: st.n_draft_steps].copy(), "gammas": glog[: st.n_stages].copy(),
+            "n_stages": st.n_stages, "n_drafted": st.n_drafted, "n_accepted": st.n_accepted,
+            "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
         }
 
 

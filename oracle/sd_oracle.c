@@ -479,12 +479,21 @@ int orc_generate_ar(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_
     return rc;
 }
 
-int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new, const uint8_t *skip,
-                    int32_t k_max, float gamma, int32_t *out, double *margin, orc_sd_stats *stats,
-                    int32_t *stage_log, float *draft_pmax)
+/* Self-speculative decoding; ad == NULL keeps the threshold fixed at gamma,
+ * otherwise it starts at ad->gamma0 and follows Eqs. 2-4. */
+static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new, const uint8_t *skip,
+                       int32_t k_max, float gamma, const orc_adaptive *ad, int32_t *out, double *margin,
+                       orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax, float *gamma_log)
 {
     if (!m || max_new < 0 || (max_new > 0 && !out) || k_max < 0 || gamma != gamma || check_prompt(m, prompt, t))
         return -1;
+    /* threshold state of the adaptive rule: gamma_d is the threshold in
+     * float64, the exit test uses it rounded to float32 */
+    double gamma_d = ad ? ad->gamma0 : (double)gamma;
+    double ar = 0.0;
+    int64_t n_updates = 0;
+    if (ad)
+        gamma = (float)gamma_d;
     if (skip)
         for (int i = 0; i < 2 * m->c.n_layers; ++i)
             if (skip[i] > 1)
@@ -577,9 +586,27 @@ int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_
             stage_log[2 * st.n_stages] = k;
             stage_log[2 * st.n_stages + 1] = na;
         }
+        if (gamma_log)
+            gamma_log[st.n_stages] = gamma;
         st.n_stages++;
         st.n_drafted += k;
         st.n_accepted += na;
+
+        /* Adaptive threshold, after the verification stage (Eqs. 2-4): the
+         * stage's acceptance rate AR_e = n_e / k_e is smoothed into AR
+         * (AR = AR_e at the first stage), the threshold moves by epsilon up
+         * when AR is at most the target alpha and down otherwise, and the
+         * move is smoothed by beta2.  Reading: a stage without drafts
+         * (k_e = 0, only at the end of generation or with K = 0) says
+         * nothing about acceptance and leaves AR and gamma as they are. */
+        if (ad && k > 0) {
+            const double ar_e = (double)na / (double)k;
+            ar = n_updates == 0 ? ar_e : ad->beta1 * ar + (1.0 - ad->beta1) * ar_e;
+            n_updates++;
+            const double gamma_t = ar <= ad->alpha ? gamma_d + ad->epsilon : gamma_d - ad->epsilon;
+            gamma_d = ad->beta2 * gamma_d + (1.0 - ad->beta2) * gamma_t;
+            gamma = (float)gamma_d;
+        }
     }
     st.n_emitted = emitted;
     if (stats)
@@ -590,4 +617,24 @@ int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_
     free(y);
     free(ymargin);
     return rc;
+}
+
+int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new, const uint8_t *skip,
+                    int32_t k_max, float gamma, int32_t *out, double *margin, orc_sd_stats *stats,
+                    int32_t *stage_log, float *draft_pmax)
+{
+    return generate_sd(m, prompt, t, max_new, skip, k_max, gamma, NULL, out, margin, stats, stage_log, draft_pmax,
+                       NULL);
+}
+
+int orc_generate_sd_adaptive(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                             const uint8_t *skip, int32_t k_max, const orc_adaptive *ad, int32_t *out,
+                             double *margin, orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax,
+                             float *gamma_log)
+{
+    if (!ad || ad->gamma0 != ad->gamma0 || ad->alpha != ad->alpha || ad->epsilon != ad->epsilon ||
+        ad->beta1 != ad->beta1 || ad->beta2 != ad->beta2)
+        return -1;
+    return generate_sd(m, prompt, t, max_new, skip, k_max, 0.0f, ad, out, margin, stats, stage_log, draft_pmax,
+                       gamma_log);
 }

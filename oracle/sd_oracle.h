@@ -101,6 +101,24 @@ int orc_generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_
                     const uint8_t *skip, int32_t k_max, float gamma, int32_t *out, double *margin,
                     orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax);
 
+/* Adaptive draft exit (Sec. 3.4, Eqs. 2-4), updated after every
+ * verification stage. */
+typedef struct {
+    double gamma0;  /* initial threshold */
+    double alpha;   /* target acceptance rate */
+    double epsilon; /* step of the threshold update */
+    double beta1;   /* smoothing of the acceptance rate */
+    double beta2;   /* smoothing of the threshold */
+} orc_adaptive;
+
+/* Greedy self-speculative decoding with the adaptive threshold; arguments as
+ * for orc_generate_sd.  gamma_log float32 [max_new] optional: the threshold
+ * each stage drafted with. */
+int orc_generate_sd_adaptive(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                             const uint8_t *skip, int32_t k_max, const orc_adaptive *ad, int32_t *out,
+                             double *margin, orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax,
+                             float *gamma_log);
+
 #ifdef __cplusplus
 }
 #endif
