@@ -17,7 +17,10 @@ Other modes:
                         the 13B shape for M in {1, 4, 8, 13, 16} rows over a
                         KV cache of 512 / 2048 / 4096 N(0, 1) positions
   --supplementary       labelled planted-redundancy runs (skipped sublayers'
-                        output projections scaled down, lm-head scaled up)
+                        output projections scaled down, lm-head scaled up),
+                        static and adaptive draft exit; --supp-mask picks
+                        another skip set (e.g. random36, the paper's 13B
+                        skip count)
   --calibrate-copy      a plain device copy of known size, for scaling the
                         FETCH_SIZE / WRITE_SIZE profiler counters
   --summarize-stats / --summarize-pmc   write profiles/ summaries from
@@ -327,7 +330,8 @@ def run_supplementary(args):
     max_new = args.max_new or wl.max_new
     host = S.make_weights(cfg, args.seed)
     prompt = S.prompt(cfg, wl.prompt_len, args.seed)
-    skip = S.skip_mask(cfg, wl.mask, args.seed)
+    mask = args.supp_mask or wl.mask
+    skip = S.skip_mask(cfg, mask, args.seed)
     out = []
     for rho, gain, gamma in [(float(x.split(":")[0]), float(x.split(":")[1]), float(x.split(":")[2]))
                              for x in args.planted.split(",")]:
@@ -352,6 +356,15 @@ def run_supplementary(args):
                                            (sd["n_stages"] + sd["n_draft_steps"]), 4),
              "ar_step_ms": round(ar["decode_ms"] / max_new, 4),
              "tokens_equal": int(np.sum(sd_tok == ar_tok))}
+        # the same planted model with the adaptive exit (the paper's settings)
+        model.generate_sd_adaptive(prompt, max_new, skip, wl.k_max)
+        ad_tok, ad = model.generate_sd_adaptive(prompt, max_new, skip, wl.k_max)
+        r.update({"adaptive_sd_tokens_per_s": round(max_new / (ad["decode_ms"] / 1e3), 2),
+                  "adaptive_speedup": round(ar["decode_ms"] / ad["decode_ms"], 4),
+                  "adaptive_acceptance": round(ad["n_accepted"] / max(ad["n_drafted"], 1), 4),
+                  "adaptive_tokens_per_stage": round(max_new / max(ad["n_stages"], 1), 3),
+                  "adaptive_gamma_last": round(float(ad["gammas"][-1]), 4) if len(ad["gammas"]) else None,
+                  "adaptive_tokens_equal": int(np.sum(ad_tok == ar_tok))})
         d = np.nonzero(sd_tok != ar_tok)[0]
         if d.size:
             # the two agree up to d; the GPU's own logits there decide whether
@@ -371,7 +384,8 @@ def run_supplementary(args):
         log(json.dumps(r))
         model.close()
         del w
-    print(json.dumps({"mode": "supplementary (planted redundancy)", "workload": wl.name, "results": out}))
+    print(json.dumps({"mode": "supplementary (planted redundancy)", "workload": wl.name, "mask": mask,
+                      "skipped_sublayers": int(np.sum(skip)), "adaptive": binding.PAPER_ADAPTIVE, "results": out}))
 
 
 # ---------------------------------------------------------------------------
@@ -457,6 +471,8 @@ def main():
     ap.add_argument("--micro-ctx", default="512,2048,4096")
     ap.add_argument("--micro-iters", type=int, default=5)
     ap.add_argument("--supplementary", action="store_true")
+    ap.add_argument("--supp-mask", default=None,
+                    help="skip mask for --supplementary (default: the workload's; e.g. random36)")
     ap.add_argument("--planted", default="0.05:8:0.6,0.05:8:0.0,0.02:16:0.6",
                     help="rho:head_gain:gamma triples for --supplementary")
     ap.add_argument("--calibrate-copy", action="store_true")

@@ -91,7 +91,20 @@ typedef struct {
     double total_ms;       /* GPU time of the whole call */
     int32_t *stage_log;
     int32_t stage_log_cap;
+    float *gamma_log;      /* HOST float [stage_log_cap] or NULL: the threshold each stage drafted with */
 } sd_stats;
+
+/* Parameters of the adaptive draft exit (Sec. 3.4, Eqs. 2-4).  After every
+ * verification stage e with k_e > 0 drafts, AR <- beta1 AR + (1 - beta1) AR_e
+ * with AR_e = n_e / k_e (AR = AR_e at the first such stage); the threshold
+ * moves to gamma + epsilon when AR <= alpha and to gamma - epsilon otherwise,
+ * smoothed: gamma <- beta2 gamma + (1 - beta2) (gamma +- epsilon).  The
+ * update runs in float64 in that order; the exit test compares the top-1
+ * probability with the threshold rounded to float32.  The paper's settings:
+ * gamma0 0.6, epsilon 0.01, beta1 0.5, beta2 0.9, alpha 0.70-0.90. */
+typedef struct {
+    double gamma0, alpha, epsilon, beta1, beta2;
+} sd_adaptive;
 
 /* Creates a model over borrowed device weights.  hip_stream is a
  * hipStream_t (NULL = the default stream).  Validates the shape and
@@ -151,6 +164,14 @@ sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const ui
 sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                 const uint8_t *skip_mask, int32_t K_max, float gamma, int32_t *out_tokens,
                                 sd_stats *stats);
+
+/* sd_self_spec_generate with the adaptive threshold of Sec. 3.4 (Eqs. 2-4)
+ * in place of a fixed gamma; params is a HOST sd_adaptive (no NaN fields).
+ * The update runs on the device after each verification, with no extra
+ * synchronisation.  Errors: INVALID_ARG, OOM, DEVICE. */
+sd_status sd_self_spec_generate_adaptive(sd_model *model, const int32_t *prompt, int32_t prompt_len,
+                                         int32_t max_new, const uint8_t *skip_mask, int32_t K_max,
+                                         const sd_adaptive *params, int32_t *out_tokens, sd_stats *stats);
 
 /* Greedy autoregressive decoding (Algorithm 1) with the same prefill
  * convention; one full-model forward per token, no per-token host sync. */

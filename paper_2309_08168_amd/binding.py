@@ -23,7 +23,8 @@ SD_F32, SD_BF16 = 0, 1
 EXPORTS = (
     "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
-    "sd_self_spec_generate", "sd_autoregressive_generate", "sd_model_time_kernel", "sd_model_kernel_time",
+    "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
+    "sd_model_time_kernel", "sd_model_kernel_time",
     "sd_last_error", "sd_version",
 )
 
@@ -57,7 +58,17 @@ class sd_stats(ctypes.Structure):
         ("prefill_ms", ctypes.c_double), ("draft_ms", ctypes.c_double), ("verify_ms", ctypes.c_double),
         ("decode_ms", ctypes.c_double), ("total_ms", ctypes.c_double),
         ("stage_log", ctypes.POINTER(ctypes.c_int32)), ("stage_log_cap", ctypes.c_int32),
+        ("gamma_log", ctypes.POINTER(ctypes.c_float)),
     ]
+
+
+class sd_adaptive(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("gamma0", "alpha", "epsilon", "beta1", "beta2")]
+
+
+# The paper's adaptive-exit settings (gamma0, epsilon, beta1, beta2; alpha
+# for LLaMA-2-13B on CNN/DM).
+PAPER_ADAPTIVE = dict(gamma0=0.6, alpha=0.9, epsilon=0.01, beta1=0.5, beta2=0.9)
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -83,6 +94,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_kv_cache_set_length": ([vp, i32], ctypes.c_int),
         "sd_forward": ([vp, vp, i32, vp, vp, vp], ctypes.c_int),
         "sd_self_spec_generate": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_stats)], ctypes.c_int),
+        "sd_self_spec_generate_adaptive": ([vp, vp, i32, i32, vp, i32, p(sd_adaptive), vp, p(sd_stats)],
+                                           ctypes.c_int),
         "sd_autoregressive_generate": ([vp, vp, i32, i32, vp, p(sd_stats)], ctypes.c_int),
         "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
         "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
@@ -210,18 +223,32 @@ class Model:
         check(load().sd_forward(self._h, _ptr(tok), tok.size, _ptr(sk), cache._h, lp))
         return logits
 
-    def generate_sd(self, prompt, max_new: int, skip, k_max: int, gamma: float, log_cap: Optional[int] = None):
+    def _sd_call(self, fn, prompt, max_new, skip, k_max, rule, log_cap):
         pr = np.ascontiguousarray(prompt, dtype=np.int32)
         sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
         out = np.zeros(max(max_new, 1), np.int32)
         cap = max(max_new, 1) if log_cap is None else log_cap
         log = np.zeros((cap, 2), np.int32)
+        glog = np.zeros(cap, np.float32)
         st = sd_stats()
         st.stage_log = log.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        st.gamma_log = glog.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
         st.stage_log_cap = cap
-        check(load().sd_self_spec_generate(self._h, _ptr(pr), pr.size, max_new, _ptr(sk), k_max,
-                                           ctypes.c_float(gamma), _ptr(out), ctypes.byref(st)))
-        return out[:max_new], _stats(st, log)
+        check(fn(self._h, _ptr(pr), pr.size, max_new, _ptr(sk), k_max, rule, _ptr(out), ctypes.byref(st)))
+        return out[:max_new], _stats(st, log, glog)
+
+    def generate_sd(self, prompt, max_new: int, skip, k_max: int, gamma: float, log_cap: Optional[int] = None):
+        """sd_self_spec_generate (fixed threshold gamma)."""
+        return self._sd_call(load().sd_self_spec_generate, prompt, max_new, skip, k_max, ctypes.c_float(gamma),
+                             log_cap)
+
+    def generate_sd_adaptive(self, prompt, max_new: int, skip, k_max: int, log_cap: Optional[int] = None,
+                             **params):
+        """sd_self_spec_generate_adaptive; params: gamma0, alpha, epsilon, beta1,
+        beta2 (defaults: PAPER_ADAPTIVE)."""
+        ad = sd_adaptive(**{**PAPER_ADAPTIVE, **params})
+        return self._sd_call(load().sd_self_spec_generate_adaptive, prompt, max_new, skip, k_max,
+                             ctypes.byref(ad), log_cap)
 
     def generate_ar(self, prompt, max_new: int):
         pr = np.ascontiguousarray(prompt, dtype=np.int32)
@@ -231,10 +258,12 @@ class Model:
         return out[:max_new], _stats(st, None)
 
 
-def _stats(st: sd_stats, log) -> dict:
-    d = {k: getattr(st, k) for k, _ in sd_stats._fields_ if k not in ("stage_log", "stage_log_cap")}
+def _stats(st: sd_stats, log, glog=None) -> dict:
+    d = {k: getattr(st, k) for k, _ in sd_stats._fields_ if k not in ("stage_log", "stage_log_cap", "gamma_log")}
     if log is not None:
         d["stages"] = log[: min(st.n_stages, log.shape[0])].copy()
+    if glog is not None:
+        d["gammas"] = glog[: min(st.n_stages, glog.shape[0])].copy()
     return d
 
 

@@ -552,7 +552,7 @@ hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *de
 // State at the start of decoding: the cache holds the prompt minus its last
 // token; the first stage drafts from that last token.
 __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *last,
-                              int32_t max_new, int32_t k_max, float gamma) {
+                              int32_t max_new, int32_t k_max, ExitRule rule) {
     if (threadIdx.x != 0)
         return;
     const int tok = *last;
@@ -567,7 +567,15 @@ __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc
     st->phase = kcap > 0 ? PHASE_DRAFT : PHASE_VERIFY;
     st->gen_done = max_new <= 0;
     st->seq = 0;
-    st->gamma = gamma;
+    st->adaptive = rule.adaptive;
+    st->gamma_d = rule.adaptive ? rule.gamma0 : (double)rule.gamma;
+    st->gamma = rule.adaptive ? __double2float_rn(rule.gamma0) : rule.gamma;
+    st->n_updates = 0;
+    st->ar = 0.0;
+    st->alpha = rule.alpha;
+    st->epsilon = rule.epsilon;
+    st->beta1 = rule.beta1;
+    st->beta2 = rule.beta2;
     st->n_stages = st->n_drafted = st->n_accepted = st->n_draft_steps = 0;
     ctl->pos = lc;
     ctl->m = 1;
@@ -578,8 +586,8 @@ __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc
 }
 
 hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,
-                              int32_t max_new, int32_t k_max, float gamma, hipStream_t s) {
-    hipLaunchKernelGGL(k_init_decode, dim3(1), dim3(64), 0, s, st, ctl, mb, lc, dev_last, max_new, k_max, gamma);
+                              int32_t max_new, int32_t k_max, const ExitRule &rule, hipStream_t s) {
+    hipLaunchKernelGGL(k_init_decode, dim3(1), dim3(64), 0, s, st, ctl, mb, lc, dev_last, max_new, k_max, rule);
     return hipGetLastError();
 }
 

@@ -153,7 +153,7 @@ __device__ void post_mailbox(DevState *st, Mailbox *mb) {
 //           to the model's own tokens is accepted, followed by the model's
 //           token at the first mismatch (or the bonus token); the committed
 //           length advances past them, which rolls back the KV positions of
-//           rejected drafts.
+//           rejected drafts; then the adaptive threshold update, if on.
 __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, const float *p) {
     DevState *st = h.st;
     if (h.mode == HEAD_AR) {
@@ -198,10 +198,27 @@ __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, co
         if (h.stage_log && st->n_stages < h.stage_log_cap) {
             h.stage_log[2 * st->n_stages] = k;
             h.stage_log[2 * st->n_stages + 1] = n;
+            h.gamma_log[st->n_stages] = st->gamma;
         }
         st->n_stages += 1;
         st->n_drafted += k;
         st->n_accepted += n;
+        // Adaptive threshold (Sec. 3.4, Eqs. 2-4): smooth the stage's
+        // acceptance rate into AR (the first stage sets it), step the
+        // threshold up when AR is at most the target and down otherwise,
+        // and smooth the step.  Float64, each operation rounded on its own
+        // in the order of the equations (contraction into FMAs is off, so
+        // the host-side definition gives the same bits); a stage without
+        // drafts carries no acceptance rate and leaves both unchanged.
+        if (st->adaptive && k > 0) {
+#pragma clang fp contract(off)
+            const double ar_e = (double)n / (double)k;
+            st->ar = st->n_updates == 0 ? ar_e : st->beta1 * st->ar + (1.0 - st->beta1) * ar_e;
+            st->n_updates += 1;
+            const double gt = st->ar <= st->alpha ? st->gamma_d + st->epsilon : st->gamma_d - st->epsilon;
+            st->gamma_d = st->beta2 * st->gamma_d + (1.0 - st->beta2) * gt;
+            st->gamma = __double2float_rn(st->gamma_d);
+        }
         st->lc += n + 1;
         st->last = y[n];
         if (e >= st->max_new) {

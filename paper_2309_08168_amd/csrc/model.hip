@@ -105,6 +105,8 @@ struct sd_model {
     int d_out_cap = 0;
     int32_t *d_log = nullptr;  // (k_e, n_e) pairs
     int d_log_cap = 0;         // int32 elements
+    float *d_glog = nullptr;   // threshold of each stage
+    int d_glog_cap = 0;
     sd_kv_cache *gen_cache = nullptr;
     std::vector<sd_kv_cache *> caches;  // caller-created caches, detached on destroy
     hipEvent_t ev[6] = {};
@@ -282,11 +284,12 @@ sd_status ensure_attn(sd_model *m, int cap) {
     return SD_OK;
 }
 
-sd_status ensure_i32(sd_model *m, int32_t **buf, int *cap, int need) {
+template <typename T>
+sd_status ensure_buf(sd_model *m, T **buf, int *cap, int need) {
     if (need <= *cap)
         return SD_OK;
     SD_HIP(hipStreamSynchronize(m->stream));
-    int32_t *nb = nullptr;
+    T *nb = nullptr;
     SD_TRY(dev_alloc(&nb, (size_t)need));
     dev_free(*buf);
     *buf = nb;
@@ -452,7 +455,8 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.mb = m->mb_dev;
         eh.head.out_tokens = m->d_out;
         eh.head.stage_log = m->d_log;
-        eh.head.stage_log_cap = m->d_log_cap / 2;
+        eh.head.gamma_log = m->d_glog;
+        eh.head.stage_log_cap = std::min(m->d_log_cap / 2, m->d_glog_cap);
         SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending));
         SD_TRY(run_linear(m, P[LK_HEAD], max_rows, m->lm_head, m->h, ldh, m->final_norm, eh, m->xa));
     }
@@ -623,11 +627,15 @@ sd_status copy_results(sd_model *m, int32_t max_new, int32_t *out_tokens, sd_sta
     DevState st{};
     SD_HIP(hipMemcpyAsync(&st, m->st, sizeof st, hipMemcpyDeviceToHost, m->stream));
     std::vector<int32_t> log;
+    std::vector<float> glog;
     int64_t nlog = 0;
-    if (stats && stats->stage_log && stats->stage_log_cap > 0) {
-        nlog = std::min<int64_t>(stats->stage_log_cap, m->d_log_cap / 2);
+    if (stats && (stats->stage_log || stats->gamma_log) && stats->stage_log_cap > 0) {
+        nlog = std::min<int64_t>(stats->stage_log_cap, std::min(m->d_log_cap / 2, m->d_glog_cap));
         log.resize((size_t)nlog * 2);
+        glog.resize((size_t)nlog);
         SD_HIP(hipMemcpyAsync(log.data(), m->d_log, sizeof(int32_t) * 2 * (size_t)nlog, hipMemcpyDeviceToHost,
+                              m->stream));
+        SD_HIP(hipMemcpyAsync(glog.data(), m->d_glog, sizeof(float) * (size_t)nlog, hipMemcpyDeviceToHost,
                               m->stream));
     }
     SD_HIP(hipStreamSynchronize(m->stream));
@@ -640,7 +648,10 @@ sd_status copy_results(sd_model *m, int32_t max_new, int32_t *out_tokens, sd_sta
         stats->n_draft_steps = st.n_draft_steps;
         if (nlog) {
             const int64_t n = std::min<int64_t>(nlog, st.n_stages);
-            std::memcpy(stats->stage_log, log.data(), sizeof(int32_t) * 2 * (size_t)n);
+            if (stats->stage_log)
+                std::memcpy(stats->stage_log, log.data(), sizeof(int32_t) * 2 * (size_t)n);
+            if (stats->gamma_log)
+                std::memcpy(stats->gamma_log, glog.data(), sizeof(float) * (size_t)n);
         }
     }
     return SD_OK;
@@ -664,11 +675,12 @@ sd_status check_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len,
 // Shared start of both generate calls: buffers, prompt upload, prefill,
 // decode-state setup.
 sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new, int32_t k_max,
-                         float gamma) {
+                         const ExitRule &rule) {
     SD_TRY(ensure_gen_cache(m, prompt_len + max_new + k_max + 1));
-    SD_TRY(ensure_i32(m, &m->d_tokens, &m->d_tokens_cap, prompt_len));
-    SD_TRY(ensure_i32(m, &m->d_out, &m->d_out_cap, std::max(max_new, 1)));
-    SD_TRY(ensure_i32(m, &m->d_log, &m->d_log_cap, 2 * std::max(max_new, 1)));
+    SD_TRY(ensure_buf(m, &m->d_tokens, &m->d_tokens_cap, prompt_len));
+    SD_TRY(ensure_buf(m, &m->d_out, &m->d_out_cap, std::max(max_new, 1)));
+    SD_TRY(ensure_buf(m, &m->d_log, &m->d_log_cap, 2 * std::max(max_new, 1)));
+    SD_TRY(ensure_buf(m, &m->d_glog, &m->d_glog_cap, std::max(max_new, 1)));
     SD_HIP(hipMemcpyAsync(m->d_tokens, prompt, sizeof(int32_t) * (size_t)prompt_len, hipMemcpyHostToDevice,
                           m->stream));
     SD_HIP(hipEventRecord(m->ev[0], m->stream));
@@ -678,20 +690,23 @@ sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     SD_HIP(hipEventRecord(m->ev[1], m->stream));
     __atomic_store_n(&m->mb_host->word, mb_pack(-1, 0, 0, 0), __ATOMIC_RELEASE);
     SD_TRY(launch(launch_init_decode(m->st, m->ctl, m->mb_dev, prompt_len - 1, m->d_tokens + prompt_len - 1,
-                                     max_new, k_max, gamma, m->stream),
+                                     max_new, k_max, rule, m->stream),
                   "decode setup"));
     return SD_OK;
 }
 
 sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new, const uint8_t *skip,
-                    int32_t k_max, float gamma, int32_t *out_tokens, sd_stats *stats) {
+                    int32_t k_max, const ExitRule &rule, int32_t *out_tokens, sd_stats *stats) {
     SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
     if (k_max < 0 || k_max > MAX_ROWS - 1)
         return fail(SD_ERR_INVALID_ARG, "K_max must be in [0, 15]");
-    if (std::isnan(gamma))
+    if (std::isnan(rule.gamma))
         return fail(SD_ERR_INVALID_ARG, "gamma is NaN");
+    if (rule.adaptive && (std::isnan(rule.gamma0) || std::isnan(rule.alpha) || std::isnan(rule.epsilon) ||
+                          std::isnan(rule.beta1) || std::isnan(rule.beta2)))
+        return fail(SD_ERR_INVALID_ARG, "adaptive parameters must not be NaN");
     SD_TRY(check_mask(m, skip));
-    SD_TRY(start_generate(m, prompt, prompt_len, max_new, k_max, gamma));
+    SD_TRY(start_generate(m, prompt, prompt_len, max_new, k_max, rule));
     sd_kv_cache *kc = m->gen_cache;
 
     // The host mirrors the phase and waits for each step's decision in the
@@ -750,7 +765,7 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
 sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                          int32_t *out_tokens, sd_stats *stats) {
     SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
-    SD_TRY(start_generate(m, prompt, prompt_len, max_new, 0, 0.0f));
+    SD_TRY(start_generate(m, prompt, prompt_len, max_new, 0, ExitRule{}));
     sd_kv_cache *kc = m->gen_cache;
     HeadSpec hs;
     hs.run = true;
@@ -785,7 +800,7 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
         return fail(SD_ERR_CAPACITY, "cache of capacity " + std::to_string(kc->cap) + " holds " +
                                          std::to_string(kc->len) + " positions; " + std::to_string(n) +
                                          " more do not fit");
-    SD_TRY(ensure_i32(m, &m->d_tokens, &m->d_tokens_cap, n));
+    SD_TRY(ensure_buf(m, &m->d_tokens, &m->d_tokens_cap, n));
     SD_HIP(hipMemcpyAsync(m->d_tokens, tokens, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, m->stream));
     for (int32_t c = 0; c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
@@ -826,6 +841,7 @@ void destroy_model(sd_model *m) {
     dev_free(m->d_tokens);
     dev_free(m->d_out);
     dev_free(m->d_log);
+    dev_free(m->d_glog);
     if (m->mb_host)
         (void)hipHostFree(m->mb_host);
     for (hipEvent_t &e : m->ev)
@@ -1032,7 +1048,18 @@ sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const ui
 sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                 const uint8_t *skip_mask, int32_t K_max, float gamma, int32_t *out_tokens,
                                 sd_stats *stats) {
-    SD_GUARD(return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, gamma, out_tokens, stats);)
+    SD_GUARD(ExitRule rule{}; rule.gamma = gamma;
+             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, out_tokens, stats);)
+}
+
+sd_status sd_self_spec_generate_adaptive(sd_model *model, const int32_t *prompt, int32_t prompt_len,
+                                         int32_t max_new, const uint8_t *skip_mask, int32_t K_max,
+                                         const sd_adaptive *params, int32_t *out_tokens, sd_stats *stats) {
+    SD_GUARD(if (!params) return fail(SD_ERR_INVALID_ARG, "params is null"); ExitRule rule{};
+             rule.adaptive = 1; rule.gamma = (float)params->gamma0; rule.gamma0 = params->gamma0;
+             rule.alpha = params->alpha; rule.epsilon = params->epsilon; rule.beta1 = params->beta1;
+             rule.beta2 = params->beta2;
+             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, out_tokens, stats);)
 }
 
 sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,

@@ -40,8 +40,13 @@ struct DevState {
     int32_t phase;     // what the next step is
     int32_t gen_done;
     int32_t seq;       // steps finished (mirrors the mailbox)
-    float gamma;
+    float gamma;       // draft-exit threshold of the current stage
+    int32_t adaptive;  // 1: gamma follows the adaptive rule after each verification
+    int32_t n_updates; // stages that updated the threshold
     int32_t pad;
+    double ar;         // smoothed acceptance rate
+    double gamma_d;    // threshold in float64; gamma is its float32 rounding
+    double alpha, epsilon, beta1, beta2;
     int32_t drafts[MAX_ROWS];
     float dpmax[MAX_ROWS];
     int64_t n_stages, n_drafted, n_accepted, n_draft_steps;
@@ -135,6 +140,7 @@ struct HeadArgs {
     Mailbox *mb;         // device view of the pinned mailbox (HEAD_DRAFT / HEAD_VERIFY)
     int32_t *out_tokens;
     int32_t *stage_log;  // [stage_log_cap][2]
+    float *gamma_log;    // [stage_log_cap]: threshold each stage drafted with
     int32_t stage_log_cap;
 };
 
@@ -198,8 +204,15 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);
 hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *dev_tokens, hipStream_t s);
+// Threshold rule of a generate call: fixed gamma (adaptive = 0) or the
+// adaptive rule starting at gamma0.
+struct ExitRule {
+    int32_t adaptive;
+    float gamma;
+    double gamma0, alpha, epsilon, beta1, beta2;
+};
 hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,
-                              int32_t max_new, int32_t k_max, float gamma, hipStream_t s);
+                              int32_t max_new, int32_t k_max, const ExitRule &rule, hipStream_t s);
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 
 }  // namespace sdk

@@ -16,6 +16,7 @@ import pytest
 
 import oracle
 import sd_synth as S
+from paper_2309_08168_amd import binding
 from tests import gpu_util as U
 
 pytestmark = pytest.mark.gpu
@@ -151,6 +152,67 @@ def test_generate_matches_oracle(name, mask, k_max, gamma, t, max_new):
         assert np.array_equal(st[:, 0], st[:, 1])
     print(f"{name}: AR agrees for {n_ar}/{max_new}, SD for {n_sd}/{max_new}; stages {len(st)}, "
           f"acceptance {sd_st['n_accepted']}/{sd_st['n_drafted']}")
+
+
+_planted = {}
+
+
+def _planted_pair(name, mask, rho, gain):
+    """A model whose masked sublayers are nearly redundant (long, confident drafts)."""
+    key = (name, mask, rho, gain)
+    if key not in _planted:
+        cfg = MODELS[name]
+        w = S.plant_redundancy(cfg, S.make_weights(cfg, 0), S.skip_mask(cfg, mask, seed=11), rho, gain)
+        _planted[key] = (cfg, w, oracle.Model(cfg, w), U.device_model(cfg, w))
+    return _planted[key]
+
+
+ADAPT_CASES = [
+    # model, mask, K_max, adaptive parameters, planted (rho, gain) or None, prompt, new tokens
+    ("tiny", "tiny", 4, dict(gamma0=0.003, alpha=0.5), None, 16, 48),
+    ("tiny", "none", 4, dict(), None, 16, 40),
+    ("tiny", "tiny", 8, dict(gamma0=0.6, alpha=0.8), (0.05, 30.0), 16, 64),
+    ("tiny", "tiny", 8, dict(gamma0=0.3, alpha=0.9, beta1=0.8), (0.05, 30.0), 16, 64),
+    ("mini_bf16", "0,3", 12, dict(gamma0=0.002, alpha=0.3), None, 24, 40),
+    ("mini_bf16", "0,3", 8, dict(gamma0=0.6, alpha=0.8), (0.02, 60.0), 24, 64),
+]
+# A draft's top-1 probability within this of the threshold may exit on the
+# other side on the GPU: the logits differ by up to the parity tolerance,
+# which moves p_max by ~1e-6 for float32 models and by a few 1e-3 for bf16.
+GAMMA_TIE = {"f32": 1e-4, "bf16": 0.02}
+
+
+@pytest.mark.parametrize("name,mask,k_max,params,planted,t,max_new", ADAPT_CASES)
+def test_generate_adaptive_matches_oracle(name, mask, k_max, params, planted, t, max_new):
+    """Adaptive draft exit (Sec. 3.4, Eqs. 2-4): tokens, stage trace and the
+    threshold of every stage equal the oracle's."""
+    cfg, w, om, dm = _pair(name) if planted is None else _planted_pair(name, mask, *planted)
+    pr = S.prompt(cfg, t, seed=t)
+    z = S.skip_mask(cfg, mask, seed=11)
+    ref = om.generate_sd_adaptive(pr, max_new, z, k_max, **params)
+    ar_ref, _ = om.generate_ar(pr, max_new)
+    std = om.score(np.concatenate([pr, ar_ref])[:-1])["logits"][t - 1:].std(axis=1)
+    sd, st = dm.generate_sd_adaptive(pr, max_new, z, k_max, **params)
+    n_sd = U.check_free_running(cfg, sd, ref["tokens"], ref["margin"], std, f"{name} adaptive SD")
+    U.check_tokens_teacher_forced(cfg, om, pr, sd, f"{name} adaptive SD teacher-forced")
+    stg, g = st["stages"], st["gammas"]
+    assert int(np.sum(stg[:, 1] + 1)) == max_new and np.all((stg[:, 1] <= stg[:, 0]) & (stg[:, 0] <= k_max))
+    # the threshold moves by (1 - beta2) epsilon after every stage with drafts
+    p = {**oracle.PAPER_ADAPTIVE, **params}
+    step = (1 - p["beta2"]) * p["epsilon"]
+    d = np.round(np.diff(g.astype(np.float64)) / step)
+    assert np.all(np.abs(d[stg[:-1, 0] > 0]) == 1) and np.all(d[stg[:-1, 0] == 0] == 0)
+    if n_sd == max_new and ref["min_gamma_gap"] > GAMMA_TIE[cfg.dtype]:
+        assert np.array_equal(stg, ref["stages"]), (stg.tolist(), ref["stages"].tolist())
+        assert np.array_equal(g, ref["gammas"])  # bit-exact: same float64 steps, same rounding
+    print(f"{name}: adaptive SD agrees for {n_sd}/{max_new}; stages {len(stg)}, acceptance "
+          f"{st['n_accepted']}/{st['n_drafted']}, gamma {g[0]:.4f} -> {g[-1]:.4f}")
+
+
+def test_adaptive_rejects_bad_parameters():
+    cfg, w, om, dm = _pair("tiny")
+    with pytest.raises(binding.SDError):
+        dm.generate_sd_adaptive(S.prompt(cfg, 4), 4, None, 2, alpha=float("nan"))
 
 
 def test_generate_is_deterministic():
