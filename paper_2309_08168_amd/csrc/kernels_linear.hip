@@ -312,10 +312,23 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
             if (n < a.N) {
                 const float v = fin[i * MR + m] * inv[m];
                 float *o = e.out + (int64_t)m * e.ld_out + n;
-                if constexpr (EPI == EPI_RESID)
-                    *o += v;
-                else
+                if constexpr (EPI == EPI_RESID) {
+                    const float hn = *o + v;
+                    *o = hn;
+                    // this work-group owns element n of every row of the
+                    // residual stream: it also prepares g * h for the next
+                    // norm's MFMA consumer (which divides by rms(h) itself)
+                    if (e.out_x) {
+                        float gk;
+                        if constexpr (sizeof(TK) == 2)
+                            gk = bf2f(reinterpret_cast<const uint16_t *>(e.next_gain)[n]);
+                        else
+                            gk = reinterpret_cast<const float *>(e.next_gain)[n];
+                        store_split3(e.out_x, m, n, M, gk * hn);
+                    }
+                } else {
                     *o = v;
+                }
             }
         }
     } else if constexpr (EPI == EPI_SWIGLU) {
@@ -579,6 +592,24 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     int q = ks0 + wave;
     if (q < ks1)
         load(q);
+    // RMSNorm folded into the outputs: the fragments hold g * h, and
+    // 1/rms(h) of every row comes from h itself (L2-resident, read while the
+    // first weights are in flight), summed in a fixed order
+    __shared__ float ssw[NW][MAX_ROWS];
+    if (a.gain) {
+        const int K4 = a.K >> 2;
+        for (int m = 0; m < M; ++m) {
+            const float4 *hr = reinterpret_cast<const float4 *>(a.X + (int64_t)m * a.ldx);
+            float ss = 0.0f;
+            for (int k = tid; k < K4; k += NW * 64) {
+                const float4 v = hr[k];
+                ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+            }
+            ss = wave_sum(ss);
+            if (lane == 0)
+                ssw[wave][m] = ss;
+        }
+    }
     for (; q < ks1; q += NW) {
         // this k-step's weights into the staging tile; its activations stay
         // in registers while the next k-step's loads go out
@@ -644,8 +675,17 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         }
         fin[o] = v;
     }
-    if (tid < 16)
-        inv_s[tid] = 1.0f;
+    if (tid < 16) {
+        float v = 1.0f;
+        if (a.gain && tid < M) {
+            float ss = 0.0f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                ss += ssw[w][tid];
+            v = 1.0f / sqrtf(ss / (float)a.K + a.eps);
+        }
+        inv_s[tid] = v;
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -656,14 +696,15 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Activations for the MFMA path, once per forward: u = g * h / rms(h) (or
-// u = h without a gain), split into X_TERMS bf16 terms in fragment layout.
-// One work-group per row.
+// Activations for the MFMA path: u = g * h / rms(h), u = g * h (when the
+// consumer divides by rms(h) itself) or u = h without a gain, split into
+// X_TERMS bf16 terms in fragment layout, after folding pending split-K
+// partials into h.  One work-group per row.
 
 template <typename TW>
 __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
                                                     const DevCtl *ctl, uint16_t *xs, const float *part,
-                                                    int n_part) {
+                                                    int n_part, bool normalize) {
     __shared__ float red[16];
     const int r = blockIdx.x, M = ctl->m;
     if (r >= M)
@@ -695,7 +736,7 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
         ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
     }
     float inv = 1.0f;
-    if (g) {
+    if (g && normalize) {
         ss = wave_sum(ss);
         if ((tid & 63) == 0)
             red[tid >> 6] = ss;
@@ -738,15 +779,15 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
 }
 
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
-                            uint16_t *xs, const float *part, int n_part, hipStream_t s) {
+                            uint16_t *xs, const float *part, int n_part, bool normalize, hipStream_t s) {
     if ((K & 127) || (ldh & 3) || n_part > 8)
         return hipErrorInvalidValue;
     if (bf16)
         hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part);
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part, normalize);
     else
         hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part);
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part, normalize);
     return hipGetLastError();
 }
 
