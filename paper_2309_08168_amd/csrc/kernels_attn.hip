@@ -56,24 +56,27 @@ __device__ __forceinline__ float wave_add(float v) {
 // four groups' softmax states merge by shuffles, the AW waves' states merge
 // in LDS in wave order, and the chunk leaves one partial state per (query,
 // split) for the ordered combine.
+//
+// Loads are unconditional: the caller passes the address of a valid cache
+// row (clamped into the context) and a flag that zeroes the values after
+// the load.  A load under a branch would make the compiler wait for every
+// outstanding load where the branches join, serialising the round trips.
 template <typename TK, int ED>
 struct KvFrag {
     float v[ED];
     __device__ __forceinline__ void load(const TK *p, bool ok) {
-        if (!ok) {
-#pragma unroll
-            for (int e = 0; e < ED; ++e)
-                v[e] = 0.0f;
-            return;
-        }
         if constexpr (sizeof(TK) == 2) {
 #pragma unroll
-            for (int e = 0; e < ED; ++e)
-                v[e] = __uint_as_float(((uint32_t)reinterpret_cast<const uint16_t *>(p)[e]) << 16);
+            for (int e = 0; e < ED; ++e) {
+                const float x = __uint_as_float(((uint32_t)reinterpret_cast<const uint16_t *>(p)[e]) << 16);
+                v[e] = ok ? x : 0.0f;
+            }
         } else {
 #pragma unroll
-            for (int e = 0; e < ED; ++e)
-                v[e] = reinterpret_cast<const float *>(p)[e];
+            for (int e = 0; e < ED; ++e) {
+                const float x = reinterpret_cast<const float *>(p)[e];
+                v[e] = ok ? x : 0.0f;
+            }
         }
     }
     __device__ __forceinline__ float at(int e) const { return v[e]; }
@@ -83,7 +86,8 @@ template <>
 struct KvFrag<uint16_t, 8> {
     u32x4_t w;
     __device__ __forceinline__ void load(const uint16_t *p, bool ok) {
-        w = ok ? *reinterpret_cast<const u32x4_t *>(p) : u32x4_t{0u, 0u, 0u, 0u};
+        const u32x4_t x = *reinterpret_cast<const u32x4_t *>(p);
+        w = ok ? x : u32x4_t{0u, 0u, 0u, 0u};
     }
     __device__ __forceinline__ float at(int e) const {
         const uint32_t x = w[e >> 1];
@@ -95,10 +99,9 @@ constexpr int AW = 8;                  // waves per chunk
 constexpr int AKW = ATTN_CHUNK / AW;   // keys per wave
 static_assert(AKW == 16, "a wave holds 4 keys per lane group");
 
-template <typename TK, int ED>
+template <typename TK, int ED, int QB>
 __global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
     constexpr int KPG = AKW / 4;  // keys per lane group
-    constexpr int QB = 4;
     __shared__ float red_o[AW][QB][MAX_HEAD_DIM];
     __shared__ float2 red_ml[AW][QB];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -121,22 +124,52 @@ __global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < KPG; ++j) {
         const int c = ks + 4 * j;
-        kf[j].load(Kg + (int64_t)c * dh, cw + c < ctx);
-        vf[j].load(Vg + (int64_t)c * dh, cw + c < ctx);
+        const bool ok = cw + c < ctx;
+        const int cc = ok ? c : ctx - 1 - cw;  // a row inside the context
+        kf[j].load(Kg + (int64_t)cc * dh, ok);
+        vf[j].load(Vg + (int64_t)cc * dh, ok);
     }
+    // Query vector qidx (one past the last reads the first).  Passes of one
+    // or two vectors load them with the K/V rows; wider passes load each
+    // vector where it is used, which keeps fewer registers live.
+    auto load_q = [&](int qidx, float(&qv)[ED]) {
+        qidx = qidx < Q ? qidx : 0;
+        const int r = qidx / G, head = g * G + (qidx - r * G);
+        const float *qs = a.q + (int64_t)r * a.ld_q + (int64_t)head * dh + e16 * ED;
+#pragma unroll
+        for (int e = 0; e < ED; ++e)
+            qv[e] = qs[e] * scale;
+    };
+    constexpr bool PRELOAD = QB <= 2;
+    float qb[PRELOAD ? QB : 1][ED];
+    if constexpr (PRELOAD) {
+#pragma unroll
+        for (int qi = 0; qi < QB; ++qi)
+            load_q(qi, qb[qi]);
+    }
+    // every load above is issued before the first result is waited for
+    __builtin_amdgcn_sched_barrier(0);
 
     for (int qg = 0; qg < Q; qg += QB) {
         const int nq = min(QB, Q - qg);
+        if (PRELOAD && qg) {
+#pragma unroll
+            for (int qi = 0; qi < (PRELOAD ? QB : 1); ++qi)
+                load_q(qg + qi, qb[qi]);
+        }
 #pragma unroll
         for (int qi = 0; qi < QB; ++qi) {
             if (qi >= nq)
                 break;
-            const int qidx = qg + qi, r = qidx / G, head = g * G + (qidx - r * G);
-            const float *qs = a.q + (int64_t)r * a.ld_q + (int64_t)head * dh + e16 * ED;
+            const int qidx = qg + qi, r = qidx / G;
             float qv[ED];
+            if constexpr (PRELOAD) {
 #pragma unroll
-            for (int e = 0; e < ED; ++e)
-                qv[e] = qs[e] * scale;
+                for (int e = 0; e < ED; ++e)
+                    qv[e] = qb[qi][e];
+            } else {
+                load_q(qidx, qv);
+            }
             const int lim = pos + r - cw;  // last key row r sees, relative to the wave
             float s[KPG];
             float mx = -INFINITY;
@@ -221,6 +254,235 @@ __global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
                 a.part_ml[slot] = make_float2(m, L);
         }
         __syncthreads();
+    }
+}
+
+// The same split-KV attention on matrix cores, for bfloat16 caches and any
+// number of query vectors: one work-group per (128-key chunk, kv head, tile
+// of 16 query vectors), each of its 4 waves taking 32 keys.
+//
+// Scores S^T[key][q] = sum_e K[key][e] q[e] are 16x16x32 bf16 MFMAs with K
+// rows as the A operand, read straight from the cache, and q (float32, times
+// 1/sqrt(head_dim)) as the B operand, split into three bf16 terms that add
+// up to it exactly, so every product is exact and only the float32
+// accumulation rounds.  Row i of score tile t holds key 16 t + 4 (i % 4) +
+// i / 4 of the wave: after the MFMA, lane group G (lanes 16 G..16 G + 15)
+// then holds, for its query column, the keys 16 t + 4 v + G (v = 0..3), which
+// are exactly the eight reduction slots 8 G + 4 t + v the output MFMA takes
+// from that lane, so softmax weights never move between lanes.
+//
+// Outputs O^T[e][q] = sum_key V[key][e] P[q][key] are 16x16x32 MFMAs with
+// P (split into three bf16 terms likewise) as the B operand and V^T as the A
+// operand: the wave's 32 V rows are stored to a wave-private LDS tile with
+// coalesced 16-byte loads and read back transposed, 2 bytes a lane, from rows
+// padded by 32 bytes so the four lane groups hit disjoint banks.  The softmax
+// of a wave's 32 keys needs one cross-lane max and sum (lanes 16 apart); the
+// four waves merge in LDS in wave order and the chunk leaves one partial per
+// (query, split) for the ordered combine.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+constexpr int MW = 4;                  // waves per work-group
+constexpr int MKW = ATTN_CHUNK / MW;   // keys per wave
+static_assert(MKW == 32, "a wave's keys are two 16-key score tiles");
+
+__device__ __forceinline__ u32x4_t pack_bf16x8(const uint16_t (&h)[8]) {
+    u32x4_t v;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        v[j] = (uint32_t)h[2 * j] | ((uint32_t)h[2 * j + 1] << 16);
+    return v;
+}
+
+// Three bf16 terms of 8 float32 values, packed as MFMA operands.
+__device__ __forceinline__ void split3x8(const float (&x)[8], u32x4_t (&t)[X_TERMS]) {
+    uint16_t h[X_TERMS][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        uint16_t s[X_TERMS];
+        split3(x[u], s);
+#pragma unroll
+        for (int i = 0; i < X_TERMS; ++i)
+            h[i][u] = s[i];
+    }
+#pragma unroll
+    for (int i = 0; i < X_TERMS; ++i)
+        t[i] = pack_bf16x8(h[i]);
+}
+
+__device__ __forceinline__ f32x4_t mfma_bf16(u32x4_t a, u32x4_t b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+}
+
+template <int DH>
+__global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
+    constexpr int ES = DH / 32;            // 32-wide slices of head_dim (score MFMAs)
+    constexpr int ET = DH / 16;            // 16-wide tiles of head_dim (output MFMAs)
+    constexpr int VP = DH + 16;            // LDS pitch of a V row, bf16 elements
+    constexpr int LPR = DH / 8;            // lanes per V row in 16-byte loads
+    constexpr int RPI = 64 / LPR;          // V rows per load instruction
+    constexpr int NVJ = MKW / RPI;         // V loads per lane
+    constexpr int OP = 17;                 // LDS pitch of the merged output, floats per e
+    constexpr int WB_V = MKW * VP * 2, WB_O = DH * OP * 4;
+    constexpr int WS = (WB_V > WB_O ? WB_V : WB_O) / 4;  // words of one wave's LDS tile
+    __shared__ uint32_t tile[MW][WS];
+    __shared__ float2 red_ml[MW][16];
+
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int split = blockIdx.x, g = blockIdx.y, qt = blockIdx.z;
+    const int pos = a.ctl->pos, M = a.ctl->m;
+    const int ctx = pos + M;
+    const int H = a.n_heads, G = H / a.n_kv_heads, Q = G * M;
+    const int c0 = split * ATTN_CHUNK;
+    if (c0 >= ctx || qt * 16 >= Q)
+        return;  // uniform over the work-group
+    const int cw = c0 + wave * MKW;  // first key of this wave
+    const int col = lane & 15, grp = lane >> 4;
+    const uint16_t *Kg = reinterpret_cast<const uint16_t *>(a.kcache) + (int64_t)g * a.kv_head_stride;
+    const uint16_t *Vg = reinterpret_cast<const uint16_t *>(a.vcache) + (int64_t)g * a.kv_head_stride;
+
+    // query column col of this tile: row r of head g G + (qi mod G)
+    const int qi = qt * 16 + col;
+    const bool qok = qi < Q;
+    const int r = qok ? qi / G : 0;
+    const int head = g * G + (qi - r * G);
+    // a column past the query vectors reads the first one and scores zero
+    f32x4_t qraw[ES][2];
+    {
+        const float *qs = a.q + (qok ? (int64_t)r * a.ld_q + (int64_t)head * DH : (int64_t)g * G * DH) + 8 * grp;
+#pragma unroll
+        for (int s = 0; s < ES; ++s) {
+            qraw[s][0] = reinterpret_cast<const f32x4_t *>(qs + 32 * s)[0];
+            qraw[s][1] = reinterpret_cast<const f32x4_t *>(qs + 32 * s)[1];
+        }
+    }
+    // K operands (A of the score MFMAs) and the wave's V rows.  Keys past the
+    // context read the last row inside it: their scores are masked and their
+    // weights are zero, and the row read is a finite one.
+    u32x4_t kf[2][ES], vr[NVJ];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const int key = min(cw + 16 * t + 4 * (col & 3) + (col >> 2), ctx - 1);
+        const uint16_t *kp = Kg + (int64_t)key * DH + 8 * grp;
+#pragma unroll
+        for (int s = 0; s < ES; ++s)
+            kf[t][s] = *reinterpret_cast<const u32x4_t *>(kp + 32 * s);
+    }
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j) {
+        const int key = min(cw + j * RPI + lane / LPR, ctx - 1);
+        vr[j] = *reinterpret_cast<const u32x4_t *>(Vg + (int64_t)key * DH + 8 * (lane % LPR));
+    }
+    // every load above is issued before the first result is waited for
+    __builtin_amdgcn_sched_barrier(0);
+    float qx[ES][8];
+    {
+        const float scale = 1.0f / sqrtf((float)DH);
+#pragma unroll
+        for (int s = 0; s < ES; ++s)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                qx[s][u] = qok ? qraw[s][0][u] * scale : 0.0f;
+                qx[s][4 + u] = qok ? qraw[s][1][u] * scale : 0.0f;
+            }
+    }
+
+    // scores of the wave's 32 keys for query column col
+    f32x4_t sacc[2];
+    {
+        u32x4_t qf[ES][X_TERMS];
+#pragma unroll
+        for (int s = 0; s < ES; ++s)
+            split3x8(qx[s], qf[s]);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            sacc[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int s = 0; s < ES; ++s)
+#pragma unroll
+                for (int i = 0; i < X_TERMS; ++i)
+                    sacc[t] = mfma_bf16(kf[t][s], qf[s][i], sacc[t]);
+        }
+    }
+    // softmax over those keys; slot u = 4 t + v of this lane is key 16 t + 4 v + grp
+    const int lim = pos + r;  // last key row r sees
+    float sv[8], mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int key = cw + 16 * (u >> 2) + 4 * (u & 3) + grp;
+        sv[u] = (qok && key < ctx && key <= lim) ? sacc[u >> 2][u & 3] : -INFINITY;
+        mx = fmaxf(mx, sv[u]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float p[8], ls = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        p[u] = mx == -INFINITY ? 0.0f : expf(sv[u] - mx);
+        ls += p[u];
+    }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    u32x4_t pf[X_TERMS];
+    split3x8(p, pf);
+
+    // V rows into the wave's LDS tile, then O^T = V^T P^T tile by tile
+    uint16_t *vs = reinterpret_cast<uint16_t *>(tile[wave]);
+#pragma unroll
+    for (int j = 0; j < NVJ; ++j)
+        *reinterpret_cast<u32x4_t *>(vs + (j * RPI + lane / LPR) * VP + 8 * (lane % LPR)) = vr[j];
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    f32x4_t oacc[ET];
+#pragma unroll
+    for (int et = 0; et < ET; ++et) {
+        uint16_t h[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            h[u] = vs[(16 * (u >> 2) + 4 * (u & 3) + grp) * VP + 16 * et + col];
+        const u32x4_t vf = pack_bf16x8(h);
+        oacc[et] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < X_TERMS; ++i)
+            oacc[et] = mfma_bf16(vf, pf[i], oacc[et]);
+    }
+    // this wave's (max, sum, O^T) into its tile, which the V rows no longer need
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    float *ro = reinterpret_cast<float *>(tile[wave]);
+#pragma unroll
+    for (int et = 0; et < ET; ++et)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            ro[(16 * et + 4 * grp + v) * OP + col] = oacc[et][v];
+    if (grp == 0)
+        red_ml[wave][col] = make_float2(mx, ls);
+    __syncthreads();
+    // merge the waves in wave order; one (query, element) per thread
+    for (int t = threadIdx.x; t < 16 * DH; t += MW * 64) {
+        const int qc = t / DH, e = t - qc * DH;
+        const int qj = qt * 16 + qc;
+        if (qj >= Q)
+            break;  // t only grows
+        float m = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < MW; ++w)
+            m = fmaxf(m, red_ml[w][qc].x);
+        float L = 0.0f, O = 0.0f;
+        if (m != -INFINITY) {
+#pragma unroll
+            for (int w = 0; w < MW; ++w) {
+                const float2 ml = red_ml[w][qc];
+                if (ml.x != -INFINITY) {
+                    const float wt = expf(ml.x - m);
+                    L = fmaf(wt, ml.y, L);
+                    O = fmaf(wt, reinterpret_cast<const float *>(tile[w])[e * OP + qc], O);
+                }
+            }
+        }
+        const int rj = qj / G, hj = g * G + (qj - rj * G);
+        const int64_t slot = ((int64_t)split * H + hj) * MAX_ROWS + rj;
+        a.part_o[slot * DH + e] = O;
+        if (e == 0)
+            a.part_ml[slot] = make_float2(m, L);
     }
 }
 
@@ -445,21 +707,52 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
     }
 }
 
-template <typename TK>
-static hipError_t launch_attn_split(const AttnArgs &a, hipStream_t s) {
+// QB query vectors per pass: 1 or 2 when the host's bound on query vectors
+// per kv head is that small (draft, autoregressive, one-draft verification
+// of multi-head attention), which keeps the registers of the unused passes
+// free; 4 otherwise.
+template <typename TK, int QB>
+static hipError_t launch_attn_split_qb(const AttnArgs &a, hipStream_t s) {
     dim3 grid(a.splits, a.n_kv_heads), block(AW * 64);
     switch (a.head_dim) {
     case 16:
-        hipLaunchKernelGGL((k_attn_split<TK, 1>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_attn_split<TK, 1, QB>), grid, block, 0, s, a);
         break;
     case 32:
-        hipLaunchKernelGGL((k_attn_split<TK, 2>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_attn_split<TK, 2, QB>), grid, block, 0, s, a);
         break;
     case 64:
-        hipLaunchKernelGGL((k_attn_split<TK, 4>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_attn_split<TK, 4, QB>), grid, block, 0, s, a);
         break;
     case 128:
-        hipLaunchKernelGGL((k_attn_split<TK, 8>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_attn_split<TK, 8, QB>), grid, block, 0, s, a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+template <typename TK>
+static hipError_t launch_attn_split(const AttnArgs &a, int max_q, hipStream_t s) {
+    if (max_q <= 1)
+        return launch_attn_split_qb<TK, 1>(a, s);
+    if (max_q <= 2)
+        return launch_attn_split_qb<TK, 2>(a, s);
+    return launch_attn_split_qb<TK, 4>(a, s);
+}
+
+static hipError_t launch_attn_mfma(const AttnArgs &a, int max_q, hipStream_t s) {
+    dim3 grid(a.splits, a.n_kv_heads, (max_q + 15) / 16), block(MW * 64);
+    switch (a.head_dim) {
+    case 32:
+        hipLaunchKernelGGL(k_attn_mfma<32>, grid, block, 0, s, a);
+        break;
+    case 64:
+        hipLaunchKernelGGL(k_attn_mfma<64>, grid, block, 0, s, a);
+        break;
+    case 128:
+        hipLaunchKernelGGL(k_attn_mfma<128>, grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;
@@ -489,6 +782,9 @@ static hipError_t launch_attn_head(const AttnArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Query vectors per kv head from which bfloat16 caches take the MFMA kernel.
+constexpr int ATTN_MFMA_MIN_Q = 1;
+
 hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s) {
     if (a.splits > MAX_SPLITS)
         return hipErrorInvalidValue;
@@ -497,7 +793,12 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
     // vectors per head fit; otherwise split the keys over work-groups
     if (G * max_rows <= QH && a.splits * ATTN_CHUNK <= 256)
         return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
-    const hipError_t e = bf16 ? launch_attn_split<uint16_t>(a, s) : launch_attn_split<float>(a, s);
+    const int max_q = G * max_rows;
+    hipError_t e;
+    if (bf16 && a.head_dim >= 32 && max_q >= ATTN_MFMA_MIN_Q)
+        e = launch_attn_mfma(a, max_q, s);
+    else
+        e = bf16 ? launch_attn_split<uint16_t>(a, max_q, s) : launch_attn_split<float>(a, max_q, s);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(k_attn_combine, dim3(a.n_heads, MAX_ROWS), dim3(128), 0, s, a);

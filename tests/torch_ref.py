@@ -19,8 +19,10 @@ import torch
 import torch.nn.functional as F
 
 
-def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0):
-    """Logits [T, vocab] (float64) of a causal forward over tokens."""
+def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0, hide_key=None):
+    """Logits [T, vocab] (float64) of a causal forward over tokens.  hide_key
+    (a row index) removes that key from every other row's attention, a planted
+    mistake for measuring how far logits move when attention loses a key."""
     tok = torch.as_tensor(np.asarray(tokens, dtype=np.int64))
     T = tok.numel()
     n_full = T if (skip is None or n_full is None) else n_full
@@ -60,8 +62,15 @@ def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0):
                 v = v.to(torch.bfloat16).to(torch.float64)
             k = k.repeat_interleave(grp, dim=1)
             v = v.repeat_interleave(grp, dim=1)
-            o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
-                                               is_causal=True)
+            if hide_key is None:
+                o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
+                                                   is_causal=True)
+            else:
+                allow = torch.ones(T, T, dtype=torch.bool).tril()
+                allow[:, hide_key] = False
+                allow[hide_key, hide_key] = True
+                o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
+                                                   attn_mask=allow)
             o = o.transpose(0, 1).reshape(T, H * dh)
             h = h + a[:, None] * F.linear(o, W[f"layers.{l}.w_o"])
         m = applies(2 * l + 1)
