@@ -57,6 +57,18 @@ class Adaptive(ctypes.Structure):
 PAPER_ADAPTIVE = dict(gamma0=0.6, alpha=0.9, epsilon=0.01, beta1=0.5, beta2=0.9)
 
 
+class Sampling(ctypes.Structure):
+    """Sampling parameters of the sampling variant: temperature, top-p, seed."""
+
+    _fields_ = [("temperature", ctypes.c_double), ("top_p", ctypes.c_double), ("seed", ctypes.c_uint64)]
+
+
+# Purposes of the uniforms (the second counter word): the draw of a draft,
+# the acceptance test of a draft, and the draw after the accepted drafts
+# (residual or bonus; every draw of autoregressive sampling).
+U_DRAFT, U_ACCEPT, U_FINAL = 0, 1, 2
+
+
 class SDStats(ctypes.Structure):
     _fields_ = [
         ("n_stages", ctypes.c_int64), ("n_drafted", ctypes.c_int64), ("n_accepted", ctypes.c_int64),
@@ -86,8 +98,18 @@ def _load(path: str = LIB_PATH):
         lib.orc_generate_sd.argtypes = [vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, vp, p(SDStats), vp, vp]
         lib.orc_generate_sd_adaptive.argtypes = [vp, vp, i32, i32, vp, i32, p(Adaptive), vp, vp, p(SDStats), vp,
                                                  vp, vp]
+        u64 = ctypes.c_uint64
+        lib.orc_philox4x64.argtypes = [vp, vp, vp]
+        lib.orc_philox4x64.restype = None
+        lib.orc_uniform.argtypes = [u64, ctypes.c_int64, i32, ctypes.c_int64]
+        lib.orc_uniform.restype = ctypes.c_double
+        lib.orc_warp.argtypes = [vp, i32, ctypes.c_double, ctypes.c_double, vp, vp]
+        lib.orc_warp.restype = i32
+        lib.orc_generate_ar_sample.argtypes = [vp, vp, i32, i32, p(Sampling), vp, vp]
+        lib.orc_generate_sd_sample.argtypes = [vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(Sampling), vp, vp,
+                                               p(SDStats), vp, vp, vp]
         for fn in ("orc_cache_truncate", "orc_cache_load", "orc_forward", "orc_generate_ar", "orc_generate_sd",
-                   "orc_generate_sd_adaptive"):
+                   "orc_generate_sd_adaptive", "orc_generate_ar_sample", "orc_generate_sd_sample"):
             getattr(lib, fn).restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
@@ -95,6 +117,30 @@ def _load(path: str = LIB_PATH):
 
 def num_threads() -> int:
     return int(_load().orc_num_threads())
+
+
+def philox4x64(ctr, key, lib_path: str = LIB_PATH) -> np.ndarray:
+    """The four 64-bit words of Philox4x64-10 block ctr (4 words) under key (2 words)."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.empty(4, np.uint64)
+    _load(lib_path).orc_philox4x64(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out
+
+
+def uniform(seed: int, index: int, purpose: int, stage: int, lib_path: str = LIB_PATH) -> float:
+    return float(_load(lib_path).orc_uniform(seed, index, purpose, stage))
+
+
+def warp(logits, temperature: float, top_p: float, lib_path: str = LIB_PATH):
+    """(pi, kept count, cut margin) of the warped distribution of one logits row."""
+    lg = np.ascontiguousarray(logits, dtype=np.float64)
+    pi = np.empty_like(lg)
+    cm = ctypes.c_double()
+    kept = _load(lib_path).orc_warp(lg.ctypes.data, lg.size, temperature, top_p, pi.ctypes.data, ctypes.byref(cm))
+    if kept < 0:
+        raise OracleError(f"orc_warp failed with status {kept}")
+    return pi, int(kept), cm.value
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -115,6 +161,7 @@ class Model:
 
     def __init__(self, cfg, weights: Dict[str, np.ndarray], lib_path: str = LIB_PATH):
         self._lib = lib = _load(lib_path)
+        self._lib_path = lib_path
         self.cfg = cfg
         self._w = weights  # keep arrays alive
         c = _Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab,
@@ -203,6 +250,46 @@ class Model:
         return {
             "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
             "draft_pmax": pm[: st.n_draft_steps].copy(), "gammas": glog[: st.n_stages].copy(),
+            "n_stages": st.n_stages, "n_drafted": st.n_drafted, "n_accepted": st.n_accepted,
+            "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
+        }
+
+
+    def generate_ar_sample(self, prompt, max_new: int, temperature: float, top_p: float, seed: int):
+        sp = Sampling(temperature, top_p, seed)
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.empty(max_new, np.int32)
+        margin = np.empty(max_new, np.float64)
+        _check(self._lib.orc_generate_ar_sample(self._h, pr.ctypes.data, pr.size, max_new, ctypes.byref(sp),
+                                              out.ctypes.data, margin.ctypes.data), "orc_generate_ar_sample")
+        return out, margin
+
+    def generate_sd_sample(self, prompt, max_new: int, skip, k_max: int, temperature: float, top_p: float,
+                           seed: int, gamma: Optional[float] = None, adaptive: Optional[dict] = None):
+        """Self-speculative sampling with a static gamma, or with the adaptive
+        threshold when adaptive is a dict of its parameters (defaults:
+        PAPER_ADAPTIVE)."""
+        sp = Sampling(temperature, top_p, seed)
+        ad = None if adaptive is None else Adaptive(**{**PAPER_ADAPTIVE, **adaptive})
+        if ad is None and gamma is None:
+            raise ValueError("gamma or adaptive is required")
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        out = np.empty(max_new, np.int32)
+        margin = np.empty(max_new, np.float64)
+        log = np.zeros((max(max_new, 1), 2), np.int32)
+        qm = np.zeros(max(max_new * max(k_max, 1), 1), np.float32)
+        glog = np.zeros(max(max_new, 1), np.float32)
+        st = SDStats()
+        _check(self._lib.orc_generate_sd_sample(self._h, pr.ctypes.data, pr.size, max_new, _ptr(sk), k_max,
+                                              ctypes.c_float(0.0 if gamma is None else gamma),
+                                              None if ad is None else ctypes.byref(ad), ctypes.byref(sp),
+                                              out.ctypes.data, margin.ctypes.data, ctypes.byref(st),
+                                              log.ctypes.data, qm.ctypes.data, glog.ctypes.data),
+               "orc_generate_sd_sample")
+        return {
+            "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
+            "draft_qmax": qm[: st.n_draft_steps].copy(), "gammas": glog[: st.n_stages].copy(),
             "n_stages": st.n_stages, "n_drafted": st.n_drafted, "n_accepted": st.n_accepted,
             "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
         }

@@ -479,6 +479,44 @@ int orc_generate_ar(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_
     return rc;
 }
 
+/* Reading: at most K drafts per stage, and never more than the tokens still
+ * to emit minus the one the verification adds. */
+static int32_t stage_budget(int32_t k_max, int32_t max_new, int32_t emitted)
+{
+    int32_t kcap = k_max;
+    if (kcap > max_new - emitted - 1)
+        kcap = max_new - emitted - 1;
+    return kcap;
+}
+
+/* Adaptive threshold, after the verification stage (Eqs. 2-4): the stage's
+ * acceptance rate AR_e = n_e / k_e is smoothed into AR (AR = AR_e at the
+ * first stage), the threshold moves by epsilon up when AR is at most the
+ * target alpha and down otherwise, and the move is smoothed by beta2.
+ * Reading: a stage without drafts (k_e = 0, only at the end of generation or
+ * with K = 0) says nothing about acceptance and leaves AR and gamma as they
+ * are.  Returns the threshold of the next stage. */
+typedef struct {
+    double ar, gamma_d; /* gamma_d: the threshold in float64; the exit test uses it rounded to float32 */
+    int64_t n_updates;
+} adapt_state;
+
+static float adapt_threshold(const orc_adaptive *ad, int32_t k, int32_t na, adapt_state *s, float gamma)
+{
+    if (!ad || k <= 0)
+        return gamma;
+    double ar = s->ar, gamma_d = s->gamma_d;
+    const int64_t n_updates = s->n_updates;
+    const double ar_e = (double)na / (double)k;
+    ar = n_updates == 0 ? ar_e : ad->beta1 * ar + (1.0 - ad->beta1) * ar_e;
+    const double gamma_t = ar <= ad->alpha ? gamma_d + ad->epsilon : gamma_d - ad->epsilon;
+    gamma_d = ad->beta2 * gamma_d + (1.0 - ad->beta2) * gamma_t;
+    s->ar = ar;
+    s->gamma_d = gamma_d;
+    s->n_updates = n_updates + 1;
+    return (float)gamma_d;
+}
+
 /* Self-speculative decoding; ad == NULL keeps the threshold fixed at gamma,
  * otherwise it starts at ad->gamma0 and follows Eqs. 2-4. */
 static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new, const uint8_t *skip,
@@ -487,13 +525,9 @@ static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t m
 {
     if (!m || max_new < 0 || (max_new > 0 && !out) || k_max < 0 || gamma != gamma || check_prompt(m, prompt, t))
         return -1;
-    /* threshold state of the adaptive rule: gamma_d is the threshold in
-     * float64, the exit test uses it rounded to float32 */
-    double gamma_d = ad ? ad->gamma0 : (double)gamma;
-    double ar = 0.0;
-    int64_t n_updates = 0;
+    adapt_state as = {0.0, ad ? ad->gamma0 : (double)gamma, 0};
     if (ad)
-        gamma = (float)gamma_d;
+        gamma = (float)as.gamma_d;
     if (skip)
         for (int i = 0; i < 2 * m->c.n_layers; ++i)
             if (skip[i] > 1)
@@ -524,11 +558,7 @@ static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t m
 
     while (rc == 0 && emitted < max_new) {
         const int32_t lc = c->len; /* committed length: the cache holds all but `last` */
-        /* Reading: at most K drafts per stage, and never more than the
-         * tokens still to emit minus the one the verification adds. */
-        int32_t kcap = k_max;
-        if (kcap > max_new - emitted - 1)
-            kcap = max_new - emitted - 1;
+        const int32_t kcap = stage_budget(k_max, max_new, emitted);
 
         /* Drafting stage: greedy tokens of the model with the skip set
          * bypassed; exit right after a token whose top-1 probability is
@@ -591,22 +621,7 @@ static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t m
         st.n_stages++;
         st.n_drafted += k;
         st.n_accepted += na;
-
-        /* Adaptive threshold, after the verification stage (Eqs. 2-4): the
-         * stage's acceptance rate AR_e = n_e / k_e is smoothed into AR
-         * (AR = AR_e at the first stage), the threshold moves by epsilon up
-         * when AR is at most the target alpha and down otherwise, and the
-         * move is smoothed by beta2.  Reading: a stage without drafts
-         * (k_e = 0, only at the end of generation or with K = 0) says
-         * nothing about acceptance and leaves AR and gamma as they are. */
-        if (ad && k > 0) {
-            const double ar_e = (double)na / (double)k;
-            ar = n_updates == 0 ? ar_e : ad->beta1 * ar + (1.0 - ad->beta1) * ar_e;
-            n_updates++;
-            const double gamma_t = ar <= ad->alpha ? gamma_d + ad->epsilon : gamma_d - ad->epsilon;
-            gamma_d = ad->beta2 * gamma_d + (1.0 - ad->beta2) * gamma_t;
-            gamma = (float)gamma_d;
-        }
+        gamma = adapt_threshold(ad, k, na, &as, gamma);
     }
     st.n_emitted = emitted;
     if (stats)
@@ -637,4 +652,350 @@ int orc_generate_sd_adaptive(orc_model *m, const int32_t *prompt, int32_t t, int
         return -1;
     return generate_sd(m, prompt, t, max_new, skip, k_max, 0.0f, ad, out, margin, stats, stage_log, draft_pmax,
                        gamma_log);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sampling variant (appendix: self-speculative decoding with random
+ * sampling and the adaptive draft exit). */
+
+/* Philox4x64-10, from its definition (Salmon, Moraes, Dror, Shaw,
+ * "Parallel random numbers: as easy as 1, 2, 3", SC'11): ten rounds of
+ * (x0, x1, x2, x3) -> (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1,
+ * lo(M0 x0)), with the key advanced by the Weyl constants between rounds. */
+void orc_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4])
+{
+    const uint64_t M0 = 0xD2E7470EE14C6C93ULL, M1 = 0xCA5A826395121157ULL;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ULL, W1 = 0xBB67AE8584CAA73BULL;
+    uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint64_t k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        const unsigned __int128 p0 = (unsigned __int128)M0 * x0;
+        const unsigned __int128 p1 = (unsigned __int128)M1 * x2;
+        const uint64_t y0 = (uint64_t)(p1 >> 64) ^ x1 ^ k0;
+        const uint64_t y1 = (uint64_t)p1;
+        const uint64_t y2 = (uint64_t)(p0 >> 64) ^ x3 ^ k1;
+        const uint64_t y3 = (uint64_t)p0;
+        x0 = y0;
+        x1 = y1;
+        x2 = y2;
+        x3 = y3;
+    }
+    out[0] = x0;
+    out[1] = x1;
+    out[2] = x2;
+    out[3] = x3;
+}
+
+double orc_uniform(uint64_t seed, int64_t index, int32_t purpose, int64_t stage)
+{
+    const uint64_t ctr[4] = {(uint64_t)index, (uint64_t)(uint32_t)purpose, (uint64_t)stage, 0};
+    const uint64_t key[2] = {seed, 0};
+    uint64_t o[4];
+    orc_philox4x64(ctr, key, o);
+    return (double)(o[0] >> 40) * 0x1p-24;
+}
+
+typedef struct {
+    int32_t id;
+    double w;
+} wtok;
+
+static int wtok_order(const void *a, const void *b)
+{
+    const wtok *x = (const wtok *)a, *y = (const wtok *)b;
+    if (x->w != y->w)
+        return x->w > y->w ? -1 : 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+int32_t orc_warp(const double *logits, int32_t V, double temperature, double top_p, double *pi, double *cut_margin)
+{
+    if (!logits || !pi || V < 1 || !(temperature > 0.0) || !(top_p > 0.0))
+        return -1;
+    double mx = -INFINITY;
+    for (int32_t v = 0; v < V; ++v)
+        if ((double)(float)logits[v] > mx)
+            mx = (double)(float)logits[v];
+    /* unnormalised weights exp((l - max) / T); the top token has weight 1 */
+    double z = 0.0;
+    for (int32_t v = 0; v < V; ++v) {
+        pi[v] = exp(((double)(float)logits[v] - mx) / temperature);
+        z += pi[v];
+    }
+    int32_t kept = V;
+    double cm = INFINITY;
+    if (top_p < 1.0) {
+        wtok *ord = (wtok *)malloc(sizeof(wtok) * (size_t)V);
+        if (!ord)
+            return -3;
+        for (int32_t v = 0; v < V; ++v) {
+            ord[v].id = v;
+            ord[v].w = pi[v];
+        }
+        qsort(ord, (size_t)V, sizeof(wtok), wtok_order);
+        /* the nucleus: the shortest prefix of that order whose mass reaches top_p */
+        const double target = top_p * z;
+        double s = 0.0;
+        kept = 0;
+        while (kept < V) {
+            const double before = s;
+            s += ord[kept].w;
+            ++kept;
+            if (s >= target) {
+                cm = fmin(target - before, s - target) / z;
+                break;
+            }
+        }
+        for (int32_t i = kept; i < V; ++i)
+            pi[ord[i].id] = 0.0;
+        free(ord);
+    }
+    double zs = 0.0;
+    for (int32_t v = 0; v < V; ++v)
+        zs += pi[v];
+    for (int32_t v = 0; v < V; ++v)
+        pi[v] /= zs;
+    if (cut_margin)
+        *cut_margin = cm;
+    return kept;
+}
+
+/* Inverse-CDF draw in id order: the smallest x with u * W < w_0 + .. + w_x
+ * (W the total weight); margin: the distance of u * W from the ends of x's
+ * interval, relative to W. */
+static int32_t draw(const double *w, int32_t V, double u, double *margin)
+{
+    double tot = 0.0;
+    for (int32_t v = 0; v < V; ++v)
+        tot += w[v];
+    const double target = u * tot;
+    double c = 0.0;
+    int32_t last = 0;
+    for (int32_t v = 0; v < V; ++v) {
+        if (!(w[v] > 0.0))
+            continue;
+        const double before = c;
+        c += w[v];
+        last = v;
+        if (target < c) {
+            *margin = fmin(target - before, c - target) / tot;
+            return v;
+        }
+    }
+    *margin = 0.0; /* u * W reached the rounded total: the last token with weight */
+    return last;
+}
+
+static int check_sampling(const orc_sampling *sp)
+{
+    return (sp && sp->temperature > 0.0 && sp->top_p > 0.0 && sp->top_p <= 1.0 && isfinite(sp->temperature)) ? 0
+                                                                                                               : -1;
+}
+
+int orc_generate_ar_sample(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                           const orc_sampling *sp, int32_t *out, double *margin)
+{
+    if (!m || max_new < 0 || (max_new > 0 && !out) || check_prompt(m, prompt, t) || check_sampling(sp))
+        return -1;
+    const int32_t V = m->c.vocab;
+    orc_cache *c = orc_cache_create(m, t + max_new + 1);
+    double *lg = (double *)malloc(sizeof(double) * (size_t)V);
+    double *pi = (double *)malloc(sizeof(double) * (size_t)V);
+    if (!c || !lg || !pi) {
+        orc_cache_destroy(c);
+        free(lg);
+        free(pi);
+        return -3;
+    }
+    int rc = prefill(m, c, prompt, t);
+    int32_t last = prompt[t - 1];
+    /* token i ~ the warped full-model distribution given everything before it */
+    for (int32_t i = 0; rc == 0 && i < max_new; ++i) {
+        rc = orc_forward(m, c, &last, 1, NULL, lg, NULL, NULL, NULL);
+        if (rc)
+            break;
+        double cm, dm;
+        orc_warp(lg, V, sp->temperature, sp->top_p, pi, &cm);
+        out[i] = draw(pi, V, orc_uniform(sp->seed, i, ORC_U_FINAL, i), &dm);
+        if (margin)
+            margin[i] = fmin(cm, dm);
+        last = out[i];
+    }
+    orc_cache_destroy(c);
+    free(lg);
+    free(pi);
+    return rc;
+}
+
+int orc_generate_sd_sample(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                           const uint8_t *skip, int32_t k_max, float gamma, const orc_adaptive *ad,
+                           const orc_sampling *sp, int32_t *out, double *margin, orc_sd_stats *stats,
+                           int32_t *stage_log, float *draft_qmax, float *gamma_log)
+{
+    if (!m || max_new < 0 || (max_new > 0 && !out) || k_max < 0 || gamma != gamma || check_prompt(m, prompt, t) ||
+        check_sampling(sp))
+        return -1;
+    if (ad && (ad->gamma0 != ad->gamma0 || ad->alpha != ad->alpha || ad->epsilon != ad->epsilon ||
+               ad->beta1 != ad->beta1 || ad->beta2 != ad->beta2))
+        return -1;
+    if (skip)
+        for (int i = 0; i < 2 * m->c.n_layers; ++i)
+            if (skip[i] > 1)
+                return -1;
+    const int32_t V = m->c.vocab;
+    const size_t K1 = (size_t)k_max + 1;
+    adapt_state as = {0.0, ad ? ad->gamma0 : (double)gamma, 0};
+    if (ad)
+        gamma = (float)as.gamma_d;
+    orc_sd_stats st;
+    memset(&st, 0, sizeof st);
+    st.min_gamma_gap = INFINITY;
+    orc_cache *c = orc_cache_create(m, t + max_new + k_max + 1);
+    int32_t *draft = (int32_t *)malloc(sizeof(int32_t) * K1);
+    int32_t *rows = (int32_t *)malloc(sizeof(int32_t) * K1);
+    double *dmarg = (double *)malloc(sizeof(double) * K1);      /* draw margin of each draft */
+    double *qcut = (double *)malloc(sizeof(double) * K1);       /* top-p cut margins, draft rows */
+    double *pcut = (double *)malloc(sizeof(double) * K1);       /* and verification rows */
+    double *q = (double *)malloc(sizeof(double) * K1 * (size_t)V);  /* warped draft distributions */
+    double *p = (double *)malloc(sizeof(double) * K1 * (size_t)V);  /* warped full-model distributions */
+    double *lg = (double *)malloc(sizeof(double) * K1 * (size_t)V);
+    if (!c || !draft || !rows || !dmarg || !qcut || !pcut || !q || !p || !lg) {
+        orc_cache_destroy(c);
+        free(draft);
+        free(rows);
+        free(dmarg);
+        free(qcut);
+        free(pcut);
+        free(q);
+        free(p);
+        free(lg);
+        return -3;
+    }
+    int rc = prefill(m, c, prompt, t);
+    int32_t last = prompt[t - 1];
+    int32_t emitted = 0;
+
+    while (rc == 0 && emitted < max_new) {
+        const int64_t stage = st.n_stages;
+        const int32_t lc = c->len;
+        const int32_t kcap = stage_budget(k_max, max_new, emitted);
+
+        /* Drafting: each draft is drawn from the warped draft distribution;
+         * the stage stops after a draft whose warped maximum is below gamma
+         * (that draft is still verified). */
+        int32_t k = 0;
+        for (int32_t j = 0; j < kcap; ++j) {
+            int32_t in = j > 0 ? draft[j - 1] : last;
+            rc = orc_forward(m, c, &in, 1, skip, lg, NULL, NULL, NULL);
+            if (rc)
+                break;
+            double *qj = q + (size_t)j * V;
+            orc_warp(lg, V, sp->temperature, sp->top_p, qj, &qcut[j]);
+            double qmax = 0.0;
+            for (int32_t v = 0; v < V; ++v)
+                if (qj[v] > qmax)
+                    qmax = qj[v];
+            draft[j] = draw(qj, V, orc_uniform(sp->seed, emitted + j, ORC_U_DRAFT, stage), &dmarg[j]);
+            const float qf = (float)qmax;
+            if (draft_qmax)
+                draft_qmax[st.n_draft_steps] = qf;
+            st.n_draft_steps++;
+            const double gap = fabs((double)qf - (double)gamma);
+            if (gap < st.min_gamma_gap)
+                st.min_gamma_gap = gap;
+            k = j + 1;
+            if (qf < gamma)
+                break;
+        }
+        if (rc)
+            break;
+
+        /* Verification: one full-model forward over [last, d_1 .. d_k]. */
+        rc = orc_cache_truncate(c, lc);
+        if (rc)
+            break;
+        rows[0] = last;
+        for (int32_t j = 0; j < k; ++j)
+            rows[j + 1] = draft[j];
+        rc = orc_forward(m, c, rows, k + 1, NULL, lg, NULL, NULL, NULL);
+        if (rc)
+            break;
+        for (int32_t i = 0; i <= k; ++i)
+            orc_warp(lg + (size_t)i * V, V, sp->temperature, sp->top_p, p + (size_t)i * V, &pcut[i]);
+
+        /* Draft i is accepted when r < min(1, p_i(d) / q_i(d)); the first
+         * rejection ends the stage. */
+        int32_t na = 0;
+        double reject_margin = INFINITY;
+        for (; na < k; ++na) {
+            const int32_t d = draft[na];
+            const double r = orc_uniform(sp->seed, emitted + na, ORC_U_ACCEPT, stage);
+            const double ratio = p[(size_t)na * V + d] / q[(size_t)na * V + d];
+            const double lim = ratio < 1.0 ? ratio : 1.0;
+            const double am = fabs(r - lim);
+            if (!(r < lim)) {
+                reject_margin = am;
+                break;
+            }
+            const double mg = fmin(fmin(dmarg[na], am), fmin(qcut[na], pcut[na]));
+            if (margin)
+                margin[emitted + na] = mg;
+            out[emitted + na] = d;
+        }
+        /* The token after the accepted drafts: at a rejection, a draw from
+         * max(0, p - q) normalised (from p if that is empty); after a fully
+         * accepted stage, a draw from p. */
+        const double uf = orc_uniform(sp->seed, emitted + na, ORC_U_FINAL, stage);
+        double fm, mg;
+        int32_t y;
+        const double *pn = p + (size_t)na * V;
+        if (na < k) {
+            const double *qn = q + (size_t)na * V;
+            double *res = lg; /* logits no longer needed */
+            double tot = 0.0;
+            for (int32_t v = 0; v < V; ++v) {
+                res[v] = pn[v] > qn[v] ? pn[v] - qn[v] : 0.0;
+                tot += res[v];
+            }
+            y = tot > 0.0 ? draw(res, V, uf, &fm) : draw(pn, V, uf, &fm);
+            mg = fmin(fmin(fm, reject_margin), fmin(qcut[na], pcut[na]));
+        } else {
+            y = draw(pn, V, uf, &fm);
+            mg = fmin(fm, pcut[na]);
+        }
+        if (margin)
+            margin[emitted + na] = mg;
+        out[emitted + na] = y;
+        emitted += na + 1;
+        last = y;
+        rc = orc_cache_truncate(c, lc + 1 + na);
+
+        if (stage_log) {
+            stage_log[2 * st.n_stages] = k;
+            stage_log[2 * st.n_stages + 1] = na;
+        }
+        if (gamma_log)
+            gamma_log[st.n_stages] = gamma;
+        st.n_stages++;
+        st.n_drafted += k;
+        st.n_accepted += na;
+        gamma = adapt_threshold(ad, k, na, &as, gamma); /* the same rule as the greedy form */
+    }
+    st.n_emitted = emitted;
+    if (stats)
+        *stats = st;
+    orc_cache_destroy(c);
+    free(draft);
+    free(rows);
+    free(dmarg);
+    free(qcut);
+    free(pcut);
+    free(q);
+    free(p);
+    free(lg);
+    return rc;
 }

@@ -119,6 +119,54 @@ int orc_generate_sd_adaptive(orc_model *m, const int32_t *prompt, int32_t t, int
                              double *margin, orc_sd_stats *stats, int32_t *stage_log, float *draft_pmax,
                              float *gamma_log);
 
+/* ------------------------------------------------------------------------
+ * Sampling variant (appendix, the sampling form of self-speculative
+ * decoding): tokens are drawn from the temperature- and top-p-warped
+ * distributions of the draft (q) and full (p) models; a draft d is accepted
+ * when r < min(1, p(d) / q(d)) for a uniform r, the first rejected position
+ * is redrawn from max(0, p - q) normalised, and a fully accepted stage ends
+ * with a draw from p.  Every uniform comes from Philox4x64-10 keyed by the
+ * seed, with the counter (output index, purpose, stage, 0).
+ */
+typedef struct {
+    double temperature; /* > 0 */
+    double top_p;       /* in (0, 1] */
+    uint64_t seed;
+} orc_sampling;
+
+enum { ORC_U_DRAFT = 0, ORC_U_ACCEPT = 1, ORC_U_FINAL = 2 };
+
+/* Philox4x64-10 (Salmon et al., SC'11): out = the 4 words of block ctr under key. */
+void orc_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+/* The uniform of (index, purpose, stage): (word 0 >> 40) * 2^-24, in [0, 1). */
+double orc_uniform(uint64_t seed, int64_t index, int32_t purpose, int64_t stage);
+
+/* The warped distribution of one row of logits (decided on their float32
+ * roundings): softmax(l / T), restricted to the shortest prefix of tokens in
+ * (probability descending, id ascending) order whose mass reaches top_p,
+ * renormalised.  pi float64 [V]; returns the kept count.  cut_margin
+ * (optional): distance, in probability, of top_p from the masses just
+ * without and with the last kept token (infinity when top_p >= 1). */
+int32_t orc_warp(const double *logits, int32_t V, double temperature, double top_p, double *pi,
+                 double *cut_margin);
+
+/* Self-speculative sampling.  ad == NULL: static threshold gamma; otherwise
+ * the adaptive rule.  margin float64 [max_new] (optional): for each emitted
+ * token the smallest margin of the decisions that produced it (the draw's
+ * distance to its CDF boundaries, the acceptance test's |r - min(1, p/q)|,
+ * the top-p cut margins of the rows involved).  draft_qmax float32
+ * [max_new * K_max] (optional): the warped draft maximum of each draft
+ * step.  Other outputs as for orc_generate_sd_adaptive. */
+int orc_generate_sd_sample(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                           const uint8_t *skip, int32_t k_max, float gamma, const orc_adaptive *ad,
+                           const orc_sampling *sp, int32_t *out, double *margin, orc_sd_stats *stats,
+                           int32_t *stage_log, float *draft_qmax, float *gamma_log);
+
+/* Autoregressive sampling: token i is drawn from the warped full-model
+ * distribution with the uniform of (i, ORC_U_FINAL, i). */
+int orc_generate_ar_sample(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
+                           const orc_sampling *sp, int32_t *out, double *margin);
+
 #ifdef __cplusplus
 }
 #endif

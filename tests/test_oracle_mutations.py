@@ -32,8 +32,8 @@ MUTATIONS = {
     "accept_index": ("while (na < k && draft[na] == y[na])", "while (na < k && draft[na] == y[na + 1])"),
     "rollback_len": ("rc = orc_cache_truncate(c, lc + na + 1);", "rc = orc_cache_truncate(c, lc + na);"),
     "exit_after_token": ("if (p < gamma)\n                break;", "if (p >= gamma)\n                break;"),
-    "kcap": ("if (kcap > max_new - emitted - 1)\n            kcap = max_new - emitted - 1;",
-             "if (kcap > max_new - emitted - 2)\n            kcap = max_new - emitted - 2 > 0 ? max_new - emitted - 2 : 0;"),
+    "kcap": ("if (kcap > max_new - emitted - 1)\n        kcap = max_new - emitted - 1;",
+             "if (kcap > max_new - emitted - 2)\n        kcap = max_new - emitted - 2 > 0 ? max_new - emitted - 2 : 0;"),
     "draft_input": ("int32_t in = j == 0 ? last : draft[j - 1];", "int32_t in = last;"),
     "kv_not_rounded": ("if (m->c.wdtype != 1 || x == 0.0 || !isfinite(x))", "if (1)"),
     "kv_round_7bits": ("return ldexp(rint(ldexp(f, 8)), e - 8);", "return ldexp(rint(ldexp(f, 7)), e - 7);"),
@@ -46,6 +46,35 @@ MUTATIONS = {
     "adapt_rate_with_bonus": ("const double ar_e = (double)na / (double)k;",
                               "const double ar_e = (double)na / (double)(k + 1);"),
 }
+
+
+# Mistakes in the sampling variant, caught by the pins of test_oracle_sampling.py.
+SAMPLING_MUTATIONS = {
+    "philox_weyl": ("W1 = 0xBB67AE8584CAA73BULL", "W1 = 0xBB67AE8584CAA73DULL"),
+    "philox_output_order": ("const uint64_t y1 = (uint64_t)p1;", "const uint64_t y1 = (uint64_t)p0;"),
+    "warp_tie_order": ("return (x->id > y->id) - (x->id < y->id);", "return (x->id < y->id) - (x->id > y->id);"),
+    "warp_temperature": ("pi[v] = exp(((double)(float)logits[v] - mx) / temperature);",
+                         "pi[v] = exp(((double)(float)logits[v] - mx) * temperature);"),
+    "warp_norm_all": ("        pi[v] /= zs;", "        pi[v] /= z;"),
+    "accept_ratio_inverted": ("const double ratio = p[(size_t)na * V + d] / q[(size_t)na * V + d];",
+                              "const double ratio = q[(size_t)na * V + d] / p[(size_t)na * V + d];"),
+    "residual_swapped": ("res[v] = pn[v] > qn[v] ? pn[v] - qn[v] : 0.0;", "res[v] = qn[v] > pn[v] ? qn[v] - pn[v] : 0.0;"),
+    "residual_from_p": ("y = tot > 0.0 ? draw(res, V, uf, &fm) : draw(pn, V, uf, &fm);", "y = draw(pn, V, uf, &fm);"),
+    "final_uses_accept_uniform": ("orc_uniform(sp->seed, emitted + na, ORC_U_FINAL, stage)",
+                                  "orc_uniform(sp->seed, emitted + na, ORC_U_ACCEPT, stage)"),
+}
+
+
+def _sampling_pins_hold(lib_path) -> bool:
+    from tests import test_oracle_sampling as P
+
+    try:
+        for check in P.ALL_CHECKS:
+            check(lib_path=lib_path)
+        P.check_sd_matches_ar_distribution(lib_path=lib_path, n=8000, T=0.2, top_p=0.85, gamma=0.6, head_gain=1.6)
+        return True
+    except (oracle.OracleError, AssertionError, IndexError, ValueError):
+        return False
 
 
 def _pins_hold(lib_path) -> bool:
@@ -103,6 +132,7 @@ def _pins_hold(lib_path) -> bool:
 
 def test_unmodified_oracle_passes(tmp_path):
     assert _pins_hold(oracle.LIB_PATH)
+    assert _sampling_pins_hold(oracle.LIB_PATH)
 
 
 @pytest.mark.parametrize("name", sorted(MUTATIONS))
@@ -114,3 +144,14 @@ def test_planted_mistake_is_caught(name, tmp_path):
     mutated.write_text(src.replace(old, new))
     lib = oracle.build(src=str(mutated), out=str(tmp_path / f"liboracle_{name}.so"))
     assert not _pins_hold(lib), f"planted mistake {name} passed every pin"
+
+
+@pytest.mark.parametrize("name", sorted(SAMPLING_MUTATIONS))
+def test_planted_sampling_mistake_is_caught(name, tmp_path):
+    old, new = SAMPLING_MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    mutated = tmp_path / "sd_oracle.c"
+    mutated.write_text(src.replace(old, new))
+    lib = oracle.build(src=str(mutated), out=str(tmp_path / f"liboracle_{name}.so"))
+    assert not _sampling_pins_hold(lib), f"planted mistake {name} passed every sampling pin"
