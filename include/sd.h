@@ -178,6 +178,43 @@ sd_status sd_self_spec_generate_adaptive(sd_model *model, const int32_t *prompt,
 sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                      int32_t *out_tokens, sd_stats *stats);
 
+/* Sampling variant (the appendix's self-speculative decoding with random
+ * sampling).  A row's distribution is warped: softmax(logits / temperature)
+ * restricted to its top-p nucleus, the shortest run of tokens in
+ * (probability descending, id ascending) order whose mass reaches top_p,
+ * renormalised.  Every uniform is the top 24 bits of the first word of
+ * Philox4x64-10 (Salmon et al., SC'11) with key (seed, 0) and counter
+ * (output index, purpose, stage, 0); purposes: 0 draft draw, 1 acceptance
+ * test, 2 the draw after the accepted drafts (and every autoregressive
+ * draw, with stage = output index).  Identical inputs and seed give
+ * identical tokens. */
+typedef struct {
+    float temperature; /* > 0, finite */
+    float top_p;       /* in (0, 1] */
+    uint64_t seed;
+} sd_sampling;
+
+/* Self-speculative sampling: drafts are drawn from the warped draft
+ * distribution q, and a stage stops right after a draft whose warped
+ * maximum is below the threshold (gamma, or the adaptive rule when adaptive
+ * is not NULL, as in sd_self_spec_generate_adaptive).  Draft d at a
+ * position is accepted when r < min(1, p(d) / q(d)), p the warped full-model
+ * distribution there and r uniform; the first rejected position is redrawn
+ * from max(0, p - q) normalised (from p if that is empty); a fully accepted
+ * stage ends with a draw from p.  The emitted tokens are distributed as
+ * autoregressive sampling from the full model.  Masses are exact 40-bit
+ * fixed-point sums.  Other arguments and errors as for
+ * sd_self_spec_generate; sampling is a HOST sd_sampling. */
+sd_status sd_self_spec_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                              const uint8_t *skip_mask, int32_t K_max, float gamma, const sd_adaptive *adaptive,
+                              const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats);
+
+/* Autoregressive sampling: token i is drawn from the warped full-model
+ * distribution with the uniform of (i, purpose 2, stage i), so
+ * sd_self_spec_sample with K_max = 0 returns the same tokens. */
+sd_status sd_autoregressive_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                   const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats);
+
 /* Measurement hook.  Selects one linear-layer class whose launches the
  * library brackets with HIP events on its stream: layer 0 = QKV, 1 = attention
  * output, 2 = gate/up, 3 = down, 4 = lm-head; rows = 1, 2 or 16 selects the

@@ -24,6 +24,7 @@ EXPORTS = (
     "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
     "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
+    "sd_self_spec_sample", "sd_autoregressive_sample",
     "sd_model_time_kernel", "sd_model_kernel_time",
     "sd_last_error", "sd_version",
 )
@@ -66,6 +67,10 @@ class sd_adaptive(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("gamma0", "alpha", "epsilon", "beta1", "beta2")]
 
 
+class sd_sampling(ctypes.Structure):
+    _fields_ = [("temperature", ctypes.c_float), ("top_p", ctypes.c_float), ("seed", ctypes.c_uint64)]
+
+
 # The paper's adaptive-exit settings (gamma0, epsilon, beta1, beta2; alpha
 # for LLaMA-2-13B on CNN/DM).
 PAPER_ADAPTIVE = dict(gamma0=0.6, alpha=0.9, epsilon=0.01, beta1=0.5, beta2=0.9)
@@ -97,6 +102,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_self_spec_generate_adaptive": ([vp, vp, i32, i32, vp, i32, p(sd_adaptive), vp, p(sd_stats)],
                                            ctypes.c_int),
         "sd_autoregressive_generate": ([vp, vp, i32, i32, vp, p(sd_stats)], ctypes.c_int),
+        "sd_self_spec_sample": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_sampling), vp, p(sd_stats)],
+                                ctypes.c_int),
+        "sd_autoregressive_sample": ([vp, vp, i32, i32, p(sd_sampling), vp, p(sd_stats)], ctypes.c_int),
         "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
         "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
                                   p(ctypes.c_int64), p(ctypes.c_int64)], ctypes.c_int),
@@ -255,6 +263,40 @@ class Model:
         out = np.zeros(max(max_new, 1), np.int32)
         st = sd_stats()
         check(load().sd_autoregressive_generate(self._h, _ptr(pr), pr.size, max_new, _ptr(out), ctypes.byref(st)))
+        return out[:max_new], _stats(st, None)
+
+    def generate_sd_sample(self, prompt, max_new: int, skip, k_max: int, temperature: float, top_p: float,
+                           seed: int, gamma: Optional[float] = None, adaptive: Optional[dict] = None,
+                           log_cap: Optional[int] = None):
+        """sd_self_spec_sample: a fixed threshold gamma, or the adaptive rule
+        when adaptive is a dict of its parameters (defaults: PAPER_ADAPTIVE)."""
+        if gamma is None and adaptive is None:
+            raise ValueError("gamma or adaptive is required")
+        ad = None if adaptive is None else sd_adaptive(**{**PAPER_ADAPTIVE, **adaptive})
+        sp = sd_sampling(temperature, top_p, seed)
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        out = np.zeros(max(max_new, 1), np.int32)
+        cap = max(max_new, 1) if log_cap is None else log_cap
+        log = np.zeros((cap, 2), np.int32)
+        glog = np.zeros(cap, np.float32)
+        st = sd_stats()
+        st.stage_log = log.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        st.gamma_log = glog.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+        st.stage_log_cap = cap
+        check(load().sd_self_spec_sample(self._h, _ptr(pr), pr.size, max_new, _ptr(sk), k_max,
+                                         ctypes.c_float(0.0 if gamma is None else gamma),
+                                         None if ad is None else ctypes.byref(ad), ctypes.byref(sp), _ptr(out),
+                                         ctypes.byref(st)))
+        return out[:max_new], _stats(st, log, glog)
+
+    def generate_ar_sample(self, prompt, max_new: int, temperature: float, top_p: float, seed: int):
+        sp = sd_sampling(temperature, top_p, seed)
+        pr = np.ascontiguousarray(prompt, dtype=np.int32)
+        out = np.zeros(max(max_new, 1), np.int32)
+        st = sd_stats()
+        check(load().sd_autoregressive_sample(self._h, _ptr(pr), pr.size, max_new, ctypes.byref(sp), _ptr(out),
+                                              ctypes.byref(st)))
         return out[:max_new], _stats(st, None)
 
 

@@ -497,10 +497,10 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
 constexpr int QH = 4;
 constexpr int HW = 8;
 
-template <typename TK, int ED>
-__global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
-    __shared__ float wst[HW][QH][2];
-    __shared__ float wo[HW][QH][MAX_HEAD_DIM];
+template <typename TK, int ED, int NWV = HW>
+__global__ __launch_bounds__(NWV * 64) void k_attn_head(AttnArgs a) {
+    __shared__ float wst[NWV][QH][2];
+    __shared__ float wo[NWV][QH][MAX_HEAD_DIM];
     const int g = blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int pos = a.ctl->pos, M = a.ctl->m;
@@ -547,8 +547,8 @@ __global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
         }
     };
     load_blk(wave, kc, vc);
-    for (int b = wave; b < nblk; b += HW) {
-        load_blk(b + HW, kn, vn);
+    for (int b = wave; b < nblk; b += NWV) {
+        load_blk(b + NWV, kn, vn);
 #pragma unroll
         for (int qi = 0; qi < QH; ++qi) {
             if (qi >= nq)
@@ -627,13 +627,13 @@ __global__ __launch_bounds__(HW * 64) void k_attn_head(AttnArgs a) {
         }
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < nq * dh; t += HW * 64) {
+    for (int t = threadIdx.x; t < nq * dh; t += NWV * 64) {
         const int qi = t / dh, e = t - qi * dh;
         float mx = -INFINITY;
-        for (int w = 0; w < HW; ++w)
+        for (int w = 0; w < NWV; ++w)
             mx = fmaxf(mx, wst[w][qi][0]);
         float L = 0.0f, O = 0.0f;
-        for (int w = 0; w < HW; ++w) {
+        for (int w = 0; w < NWV; ++w) {
             const float m = wst[w][qi][0];
             if (m == -INFINITY)
                 continue;

@@ -17,6 +17,7 @@
 // as its input also accumulates sum(h^2) and scales its outputs at the end;
 // no separate normalisation pass.
 #include "sd_internal.h"
+#include "decode_step.h"
 
 namespace sdk {
 
@@ -137,102 +138,26 @@ __device__ __forceinline__ HeadPart head_comb(HeadPart a, HeadPart b) {
     return r;
 }
 
-__device__ void post_mailbox(DevState *st, Mailbox *mb) {
-    st->seq += 1;
-    __hip_atomic_store(&mb->word, mb_pack(st->seq, st->phase, st->gen_done, st->emitted), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_SYSTEM);
-}
-
 // The decoding decision after one step, taken by one thread once the
 // argmax y[r] and top-1 probability p[r] of every row are known.
 //   AR:     Algorithm 1, append y and feed it back.
 //   DRAFT:  Algorithm 2 drafting with the exit of Sec. 3.4: keep d_j, stop
-//           after it when p_j < gamma or the stage budget is reached; the
-//           next step is then the verification of [last, d_1..d_k].
+//           after it when p_j < gamma or the stage budget is reached.
 //   VERIFY: Algorithm 2 verification: the longest prefix of drafts equal
 //           to the model's own tokens is accepted, followed by the model's
-//           token at the first mismatch (or the bonus token); the committed
-//           length advances past them, which rolls back the KV positions of
-//           rejected drafts; then the adaptive threshold update, if on.
+//           token at the first mismatch (or the bonus token).
+// The state updates themselves are shared with the sampling variant.
 __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, const float *p) {
     DevState *st = h.st;
     if (h.mode == HEAD_AR) {
-        const int tok = y[0];
-        h.out_tokens[st->emitted] = tok;
-        st->emitted += 1;
-        st->lc += 1;
-        st->last = tok;
-        ctl->pos += 1;
-        ctl->tokens[0] = tok;
+        ar_commit(h, ctl, y[0]);
     } else if (h.mode == HEAD_DRAFT) {
-        const int j = st->k;
-        st->drafts[j] = y[0];
-        st->dpmax[j] = p[0];
-        st->k = j + 1;
-        st->n_draft_steps += 1;
-        const bool exit_now = (p[0] < st->gamma) || (j + 1 >= st->kcap);
-        if (!exit_now) {
-            ctl->pos = st->lc + j + 1;
-            ctl->m = 1;
-            ctl->tokens[0] = y[0];
-        } else {
-            st->phase = PHASE_VERIFY;
-            ctl->pos = st->lc;
-            ctl->m = j + 2;
-            ctl->tokens[0] = st->last;
-            for (int i = 0; i <= j; ++i)
-                ctl->tokens[i + 1] = st->drafts[i];
-        }
-        post_mailbox(st, h.mb);
+        draft_commit(h, ctl, y[0], p[0]);
     } else if (h.mode == HEAD_VERIFY) {
-        const int k = st->k;
         int n = 0;
-        while (n < k && st->drafts[n] == y[n])
+        while (n < st->k && st->drafts[n] == y[n])
             ++n;
-        int e = st->emitted;
-        for (int i = 0; i < n; ++i)
-            h.out_tokens[e + i] = st->drafts[i];
-        h.out_tokens[e + n] = y[n];
-        e += n + 1;
-        st->emitted = e;
-        if (h.stage_log && st->n_stages < h.stage_log_cap) {
-            h.stage_log[2 * st->n_stages] = k;
-            h.stage_log[2 * st->n_stages + 1] = n;
-            h.gamma_log[st->n_stages] = st->gamma;
-        }
-        st->n_stages += 1;
-        st->n_drafted += k;
-        st->n_accepted += n;
-        // Adaptive threshold (Sec. 3.4, Eqs. 2-4): smooth the stage's
-        // acceptance rate into AR (the first stage sets it), step the
-        // threshold up when AR is at most the target and down otherwise,
-        // and smooth the step.  Float64, each operation rounded on its own
-        // in the order of the equations (contraction into FMAs is off, so
-        // the host-side definition gives the same bits); a stage without
-        // drafts carries no acceptance rate and leaves both unchanged.
-        if (st->adaptive && k > 0) {
-#pragma clang fp contract(off)
-            const double ar_e = (double)n / (double)k;
-            st->ar = st->n_updates == 0 ? ar_e : st->beta1 * st->ar + (1.0 - st->beta1) * ar_e;
-            st->n_updates += 1;
-            const double gt = st->ar <= st->alpha ? st->gamma_d + st->epsilon : st->gamma_d - st->epsilon;
-            st->gamma_d = st->beta2 * st->gamma_d + (1.0 - st->beta2) * gt;
-            st->gamma = __double2float_rn(st->gamma_d);
-        }
-        st->lc += n + 1;
-        st->last = y[n];
-        if (e >= st->max_new) {
-            st->gen_done = 1;
-        } else {
-            const int kcap = min(st->k_max, st->max_new - e - 1);
-            st->k = 0;
-            st->kcap = kcap;
-            st->phase = kcap > 0 ? PHASE_DRAFT : PHASE_VERIFY;
-        }
-        ctl->pos = st->lc;
-        ctl->m = 1;
-        ctl->tokens[0] = st->last;
-        post_mailbox(st, h.mb);
+        stage_commit(h, ctl, n, y[n]);
     }
 }
 
@@ -384,7 +309,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                 const float v = fin[i * MR + m] * inv[m];
                 fin[i * MR + m] = v;
                 if (h.logits)
-                    h.logits[(int64_t)m * h.ld_logits + n] = v;
+                    h.logits[(int64_t)(h.logits_by_draft ? h.st->k : m) * h.ld_logits + n] = v;
             }
         }
         __syncthreads();

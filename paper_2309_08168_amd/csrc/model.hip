@@ -91,6 +91,11 @@ struct sd_model {
     uint16_t *xa = nullptr, *xb = nullptr;
     int64_t xld = 0;
     float4 *head_part = nullptr;
+    // sampling variant: logits of the verification / autoregressive rows and
+    // of the stage's drafts, the rows' nucleus statistics, the parameters
+    float *slog_v = nullptr, *slog_d = nullptr;
+    RowStat *svstat = nullptr, *sdstat = nullptr;
+    SampleParams sp_cur{};
     float *attn_o = nullptr;
     float2 *attn_ml = nullptr;
     int attn_splits_cap = 0;
@@ -358,8 +363,20 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
         SD_HIP(hipEventRecord(m->tev[m->tev_used + 1], m->stream));
         m->tev_used += 2;
     }
-    if (p.epi == EPI_HEAD)
+    if (p.epi == EPI_HEAD && epi.head.sampled) {
+        SampleArgs sa{};
+        sa.sp = m->sp_cur;
+        sa.vocab = m->cfg.vocab;
+        sa.ctl = m->ctl;
+        sa.vlog = m->slog_v;
+        sa.dlog = m->slog_d;
+        sa.vstat = m->svstat;
+        sa.dstat = m->sdstat;
+        sa.head = epi.head;
+        SD_TRY(launch(launch_sample_step(sa, max_rows, m->stream), "sampling step"));
+    } else if (p.epi == EPI_HEAD) {
         SD_TRY(launch(launch_head_finalize(a, p.n_tiles, m->stream), "head finalize"));
+    }
     return SD_OK;
 }
 
@@ -383,6 +400,7 @@ struct HeadSpec {
     int mode = HEAD_NONE;
     float *logits = nullptr;
     bool run = false;
+    bool sampled = false;  // sampling variant (parameters in sd_model::sp_cur)
 };
 
 // One decoder forward over the rows described by the device control block.
@@ -500,6 +518,11 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.stage_log = m->d_log;
         eh.head.gamma_log = m->d_glog;
         eh.head.stage_log_cap = std::min(m->d_log_cap / 2, m->d_glog_cap);
+        if (hs.sampled) {
+            eh.head.sampled = 1;
+            eh.head.logits = hs.mode == HEAD_DRAFT ? m->slog_d : m->slog_v;
+            eh.head.logits_by_draft = hs.mode == HEAD_DRAFT;
+        }
         SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending, fresh));
         SD_TRY(run_linear(m, P[LK_HEAD], max_rows, m->lm_head, m->h, ldh, m->final_norm, eh, m->xa));
     }
@@ -738,8 +761,22 @@ sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     return SD_OK;
 }
 
+// Checks and installs the parameters of the sampling variant (sp == null:
+// greedy decoding).
+sd_status use_sampling(sd_model *m, const SampleParams *sp) {
+    if (!sp)
+        return SD_OK;
+    if (!(sp->temperature > 0.0f) || !std::isfinite(sp->temperature))
+        return fail(SD_ERR_INVALID_ARG, "temperature must be positive and finite");
+    if (!(sp->top_p > 0.0f) || !(sp->top_p <= 1.0f))
+        return fail(SD_ERR_INVALID_ARG, "top_p must be in (0, 1]");
+    m->sp_cur = *sp;
+    return SD_OK;
+}
+
 sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new, const uint8_t *skip,
-                    int32_t k_max, const ExitRule &rule, int32_t *out_tokens, sd_stats *stats) {
+                    int32_t k_max, const ExitRule &rule, const SampleParams *sp, int32_t *out_tokens,
+                    sd_stats *stats) {
     SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
     if (k_max < 0 || k_max > MAX_ROWS - 1)
         return fail(SD_ERR_INVALID_ARG, "K_max must be in [0, 15]");
@@ -749,6 +786,7 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
                           std::isnan(rule.beta1) || std::isnan(rule.beta2)))
         return fail(SD_ERR_INVALID_ARG, "adaptive parameters must not be NaN");
     SD_TRY(check_mask(m, skip));
+    SD_TRY(use_sampling(m, sp));
     SD_TRY(start_generate(m, prompt, prompt_len, max_new, k_max, rule));
     sd_kv_cache *kc = m->gen_cache;
 
@@ -766,6 +804,7 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
         SD_HIP(hipEventRecord(e0, m->stream));
         HeadSpec hs;
         hs.run = true;
+        hs.sampled = sp != nullptr;
         if (phase == PHASE_DRAFT) {
             hs.mode = HEAD_DRAFT;
             SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, 1, hs));
@@ -806,13 +845,15 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
 }
 
 sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
-                         int32_t *out_tokens, sd_stats *stats) {
+                         const SampleParams *sp, int32_t *out_tokens, sd_stats *stats) {
     SD_TRY(check_generate(m, prompt, prompt_len, max_new, out_tokens));
+    SD_TRY(use_sampling(m, sp));
     SD_TRY(start_generate(m, prompt, prompt_len, max_new, 0, ExitRule{}));
     sd_kv_cache *kc = m->gen_cache;
     HeadSpec hs;
     hs.run = true;
     hs.mode = HEAD_AR;
+    hs.sampled = sp != nullptr;
     for (int32_t i = 0; i < max_new; ++i)
         SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, 1, hs));
     SD_HIP(hipEventRecord(m->ev[2], m->stream));
@@ -876,6 +917,10 @@ void destroy_model(sd_model *m) {
     dev_free(m->xa);
     dev_free(m->xb);
     dev_free(m->head_part);
+    dev_free(m->slog_v);
+    dev_free(m->slog_d);
+    dev_free(m->svstat);
+    dev_free(m->sdstat);
     dev_free(m->attn_o);
     dev_free(m->attn_ml);
     dev_free(m->rope);
@@ -954,6 +999,10 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->xa, (size_t)X_TERMS * MAX_ROWS * m->xld));
     chain(dev_alloc(&m->xb, (size_t)X_TERMS * MAX_ROWS * m->xld));
     chain(dev_alloc(&m->head_part, (size_t)max_head_tiles * MAX_ROWS));
+    chain(dev_alloc(&m->slog_v, (size_t)MAX_ROWS * c.vocab));
+    chain(dev_alloc(&m->slog_d, (size_t)MAX_ROWS * c.vocab));
+    chain(dev_alloc(&m->svstat, (size_t)MAX_ROWS));
+    chain(dev_alloc(&m->sdstat, (size_t)MAX_ROWS));
     chain(dev_alloc(&m->ctl, 1));
     chain(dev_alloc(&m->st, 1));
     if (st != SD_OK) {
@@ -1092,7 +1141,8 @@ sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t 
                                 const uint8_t *skip_mask, int32_t K_max, float gamma, int32_t *out_tokens,
                                 sd_stats *stats) {
     SD_GUARD(ExitRule rule{}; rule.gamma = gamma;
-             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, out_tokens, stats);)
+             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, nullptr, out_tokens,
+                              stats);)
 }
 
 sd_status sd_self_spec_generate_adaptive(sd_model *model, const int32_t *prompt, int32_t prompt_len,
@@ -1102,12 +1152,50 @@ sd_status sd_self_spec_generate_adaptive(sd_model *model, const int32_t *prompt,
              rule.adaptive = 1; rule.gamma = (float)params->gamma0; rule.gamma0 = params->gamma0;
              rule.alpha = params->alpha; rule.epsilon = params->epsilon; rule.beta1 = params->beta1;
              rule.beta2 = params->beta2;
-             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, out_tokens, stats);)
+             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, nullptr, out_tokens,
+                              stats);)
 }
 
 sd_status sd_autoregressive_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                      int32_t *out_tokens, sd_stats *stats) {
-    SD_GUARD(return autoregressive(model, prompt, prompt_len, max_new, out_tokens, stats);)
+    SD_GUARD(return autoregressive(model, prompt, prompt_len, max_new, nullptr, out_tokens, stats);)
+}
+
+namespace {
+SampleParams sample_params(const sd_sampling &s) {
+    SampleParams p;
+    p.temperature = s.temperature;
+    p.top_p = s.top_p;
+    p.seed = s.seed;
+    return p;
+}
+ExitRule adaptive_rule(const sd_adaptive &a) {
+    ExitRule r{};
+    r.adaptive = 1;
+    r.gamma = (float)a.gamma0;
+    r.gamma0 = a.gamma0;
+    r.alpha = a.alpha;
+    r.epsilon = a.epsilon;
+    r.beta1 = a.beta1;
+    r.beta2 = a.beta2;
+    return r;
+}
+}  // namespace
+
+sd_status sd_self_spec_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                              const uint8_t *skip_mask, int32_t K_max, float gamma, const sd_adaptive *adaptive,
+                              const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats) {
+    SD_GUARD(if (!sampling) return fail(SD_ERR_INVALID_ARG, "sampling is null"); ExitRule rule{};
+             rule.gamma = gamma; if (adaptive) rule = adaptive_rule(*adaptive);
+             const SampleParams sp = sample_params(*sampling);
+             return self_spec(model, prompt, prompt_len, max_new, skip_mask, K_max, rule, &sp, out_tokens, stats);)
+}
+
+sd_status sd_autoregressive_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
+                                   const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats) {
+    SD_GUARD(if (!sampling) return fail(SD_ERR_INVALID_ARG, "sampling is null");
+             const SampleParams sp = sample_params(*sampling);
+             return autoregressive(model, prompt, prompt_len, max_new, &sp, out_tokens, stats);)
 }
 
 sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows) {

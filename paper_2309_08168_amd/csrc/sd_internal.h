@@ -50,6 +50,7 @@ struct DevState {
     int32_t drafts[MAX_ROWS];
     float dpmax[MAX_ROWS];
     int64_t n_stages, n_drafted, n_accepted, n_draft_steps;
+    uint64_t dqw[MAX_ROWS];  // sampling: fixed-point weight of each draft under its draft distribution
 };
 
 // Pinned host memory the GPU writes after every self-speculative step: one
@@ -142,6 +143,48 @@ struct HeadArgs {
     int32_t *stage_log;  // [stage_log_cap][2]
     float *gamma_log;    // [stage_log_cap]: threshold each stage drafted with
     int32_t stage_log_cap;
+    int32_t logits_by_draft;  // sampling drafts: the (one-row) logits go to row st->k of logits
+    int32_t sampled;          // sampling variant: the sampling kernels take the decision
+};
+
+// ---------------------------------------------------------------------------
+// Sampling variant.  The warped distribution of a row of logits l is
+// w_x = exp((l_x - max l) / T) restricted to its top-p nucleus: the shortest
+// prefix of the tokens in (w descending, id ascending) order whose mass
+// reaches top_p.  Masses are fixed point, W_x = trunc(w_x 2^40) in uint64,
+// so every sum, cut and cumulative mass is exact and independent of the
+// summation order.  The nucleus is {w_x > w*} plus the first n_tie tokens
+// (by id) with w_x == w*.
+constexpr float WFIX = 1099511627776.0f;  // 2^40
+
+struct SampleParams {
+    float temperature;
+    float top_p;
+    uint64_t seed;
+};
+
+struct RowStat {
+    float mx;         // max logit of the row
+    uint32_t bstar;   // bit pattern of w*
+    uint32_t n_tie;   // tokens with w == w* in the nucleus, lowest ids first
+    uint32_t pad;
+    uint64_t zs;      // nucleus mass
+    uint64_t wd;      // verification row r: weight of draft r + 1 if in the nucleus, else 0
+};
+
+// Purposes of the uniforms: the second counter word of Philox4x64-10, whose
+// counter is (output index, purpose, stage, 0) and key (seed, 0).
+enum UniformPurpose : int32_t { U_DRAFT = 0, U_ACCEPT = 1, U_FINAL = 2 };
+
+struct SampleArgs {
+    SampleParams sp;
+    int32_t vocab;
+    const DevCtl *ctl;
+    const float *vlog;  // [MAX_ROWS][vocab]: logits of the verification or autoregressive rows
+    const float *dlog;  // [MAX_ROWS][vocab]: logits of the drafts of the stage, by draft index
+    RowStat *vstat;     // [MAX_ROWS]
+    RowStat *dstat;     // [MAX_ROWS]
+    HeadArgs head;
 };
 
 struct EpiArgs {
@@ -204,6 +247,10 @@ hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, 
                             hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
+// Sampling variant, after a head linear that wrote the logits: the nucleus
+// statistics of every row (one work-group per row, up to max_rows), then the
+// decision of the step in one work-group (draw, acceptance, state update).
+hipError_t launch_sample_step(const SampleArgs &a, int max_rows, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s);
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);
