@@ -21,6 +21,10 @@ Other modes:
                         static and adaptive draft exit; --supp-mask picks
                         another skip set (e.g. random36, the paper's 13B
                         skip count)
+  --sampling            labelled runs of the sampling variant (temperature and
+                        top-p as in the paper's appendix) against autoregressive
+                        sampling, static and adaptive exit, random and planted
+                        weights
   --calibrate-copy      a plain device copy of known size, for scaling the
                         FETCH_SIZE / WRITE_SIZE profiler counters
   --summarize-stats / --summarize-pmc   write profiles/ summaries from
@@ -389,6 +393,57 @@ def run_supplementary(args):
 
 
 # ---------------------------------------------------------------------------
+# sampling variant (labelled supplementary runs)
+
+
+def run_sampling(args):
+    import torch  # noqa: F401
+
+    from paper_2309_08168_amd import binding
+
+    wl = S.WORKLOADS[args.workload]
+    cfg = S.MODELS[wl.model]
+    max_new = args.max_new or wl.max_new
+    host = S.make_weights(cfg, args.seed)
+    prompt = S.prompt(cfg, wl.prompt_len, args.seed)
+    skip = S.skip_mask(cfg, wl.mask, args.seed)
+    # (temperature, top_p): the paper's summarisation and code settings
+    settings = [(0.2, 0.85), (0.6, 0.95)]
+    out = []
+    for label, rho, gain in (("random weights", None, None), ("planted, rho 0 / head gain 16", 0.0, 16.0)):
+        w = host if rho is None else S.plant_redundancy(cfg, host, skip, rho, gain)
+        model = binding.Model(cfg, binding.DeviceWeights(cfg, w))
+        _, greedy = model.generate_ar(prompt, max_new)
+        for T, top_p in settings:
+            seed = 1234
+            model.generate_sd_sample(prompt, max_new, skip, wl.k_max, T, top_p, seed, gamma=wl.gamma)
+            _, sd = model.generate_sd_sample(prompt, max_new, skip, wl.k_max, T, top_p, seed, gamma=wl.gamma)
+            _, ad = model.generate_sd_sample(prompt, max_new, skip, wl.k_max, T, top_p, seed, adaptive={})
+            _, ar = model.generate_ar_sample(prompt, max_new, T, top_p, seed)
+            n_st, n_dr = max(sd["n_stages"], 1), max(sd["n_draft_steps"], 1)
+            r = {"weights": label, "temperature": T, "top_p": top_p,
+                 "sd_tokens_per_s": round(max_new / (sd["decode_ms"] / 1e3), 2),
+                 "adaptive_sd_tokens_per_s": round(max_new / (ad["decode_ms"] / 1e3), 2),
+                 "ar_tokens_per_s": round(max_new / (ar["decode_ms"] / 1e3), 2),
+                 "speedup": round(ar["decode_ms"] / sd["decode_ms"], 4),
+                 "adaptive_speedup": round(ar["decode_ms"] / ad["decode_ms"], 4),
+                 "acceptance": round(sd["n_accepted"] / max(sd["n_drafted"], 1), 4),
+                 "adaptive_acceptance": round(ad["n_accepted"] / max(ad["n_drafted"], 1), 4),
+                 "tokens_per_stage": round(max_new / n_st, 3),
+                 "draft_step_ms": round(sd["draft_ms"] / n_dr, 4),
+                 "verify_step_ms": round(sd["verify_ms"] / n_st, 4),
+                 "ar_sample_step_ms": round(ar["decode_ms"] / max_new, 4),
+                 "ar_greedy_step_ms": round(greedy["decode_ms"] / max_new, 4)}
+            out.append(r)
+            log(json.dumps(r))
+        model.close()
+        del w
+    print(json.dumps({"mode": "sampling (labelled supplementary)", "workload": wl.name, "mask": wl.mask,
+                      "k_max": wl.k_max, "gamma": wl.gamma, "adaptive": binding.PAPER_ADAPTIVE,
+                      "results": out}))
+
+
+# ---------------------------------------------------------------------------
 # profiler helpers
 
 
@@ -475,6 +530,8 @@ def main():
                     help="skip mask for --supplementary (default: the workload's; e.g. random36)")
     ap.add_argument("--planted", default="0.05:8:0.6,0.05:8:0.0,0.02:16:0.6",
                     help="rho:head_gain:gamma triples for --supplementary")
+    ap.add_argument("--sampling", action="store_true",
+                    help="labelled runs of the sampling variant (temperature, top-p) against AR sampling")
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--with-copy", action="store_true", help="also run the calibration copy after the bench")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
@@ -503,6 +560,8 @@ def main():
         run_verify_micro(args)
     elif args.supplementary:
         run_supplementary(args)
+    elif args.sampling:
+        run_sampling(args)
     else:
         run_bench(args)
     if args.with_copy:

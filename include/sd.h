@@ -202,9 +202,10 @@ typedef struct {
  * distribution there and r uniform; the first rejected position is redrawn
  * from max(0, p - q) normalised (from p if that is empty); a fully accepted
  * stage ends with a draw from p.  The emitted tokens are distributed as
- * autoregressive sampling from the full model.  Masses are exact 40-bit
- * fixed-point sums.  Other arguments and errors as for
- * sd_self_spec_generate; sampling is a HOST sd_sampling. */
+ * autoregressive sampling from the full model.  Masses are exact sums of
+ * 31-bit fixed-point weights.  Other arguments and errors as for
+ * sd_self_spec_generate; sampling is a HOST sd_sampling; the vocabulary
+ * must have at most 524288 ids (INVALID_ARG otherwise). */
 sd_status sd_self_spec_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                               const uint8_t *skip_mask, int32_t K_max, float gamma, const sd_adaptive *adaptive,
                               const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats);

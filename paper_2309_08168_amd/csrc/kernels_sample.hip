@@ -24,6 +24,11 @@ namespace sdk {
 
 constexpr int SW = 1024;         // threads of the sampling work-groups
 constexpr int SWAVES = SW / 64;
+// RowStat::n_tie when every token at w* is in the nucleus (no rank needed)
+constexpr uint32_t ALL_TIES = 0xffffffffu;
+// draws walk the vocabulary in chunks of DRAW_CHUNK ids, 8 adjacent ids per thread
+constexpr int DRAW_CHUNK = 8 * SW;
+constexpr int MAX_DRAW_CHUNKS = MAX_SAMPLE_VOCAB / DRAW_CHUNK;
 
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
 // easy as 1, 2, 3", SC'11), from its definition: ten rounds of
@@ -53,7 +58,8 @@ __device__ inline uint32_t uniform24(uint64_t seed, int64_t index, int32_t purpo
 }
 
 __device__ inline float warp_w(float l, float mx, float T) { return expf((l - mx) / T); }
-__device__ inline uint64_t wfix(float w) { return (uint64_t)(w * WFIX); }  // exact scaling, truncation
+// fixed-point weight: exact scaling by 2^31, truncation; at most 2^31
+__device__ inline uint32_t wfix(float w) { return (uint32_t)(w * WFIX); }
 
 __device__ inline uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
@@ -62,7 +68,9 @@ __device__ inline uint64_t wave_sum_u64(uint64_t v) {
     return v;
 }
 
-// Block sum; red is LDS scratch of SWAVES words.  Integer: any order is exact.
+// Block sum over NT threads; red is LDS scratch of NT / 64 words.  Integer:
+// any order is exact.
+template <int NT = SW>
 __device__ uint64_t block_sum_u64(uint64_t v, uint64_t *red) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     v = wave_sum_u64(v);
@@ -71,12 +79,13 @@ __device__ uint64_t block_sum_u64(uint64_t v, uint64_t *red) {
     __syncthreads();
     uint64_t t = 0;
 #pragma unroll
-    for (int w = 0; w < SWAVES; ++w)
+    for (int w = 0; w < NT / 64; ++w)
         t += red[w];
     __syncthreads();
     return t;
 }
 
+template <int NT = SW>
 __device__ float block_max_f(float v, float *red) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -87,13 +96,14 @@ __device__ float block_max_f(float v, float *red) {
     __syncthreads();
     float t = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < SWAVES; ++w)
+    for (int w = 0; w < NT / 64; ++w)
         t = fmaxf(t, red[w]);
     __syncthreads();
     return t;
 }
 
-// Exclusive prefix sum over the threads in thread order; *total receives the sum.
+// Exclusive prefix sum over the NT threads in thread order; *total receives the sum.
+template <int NT = SW>
 __device__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t *red, uint64_t *total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint64_t x = v;
@@ -108,7 +118,7 @@ __device__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t *red, uint64_t *tot
     __syncthreads();
     uint64_t base = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < SWAVES; ++w) {
+    for (int w = 0; w < NT / 64; ++w) {
         const uint64_t r = red[w];
         base += w < wave ? r : 0;
         tot += r;
@@ -120,12 +130,44 @@ __device__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t *red, uint64_t *tot
 
 // ---------------------------------------------------------------------------
 // Nucleus statistics of one row per work-group.
+//
+// Element i of thread t is token t + i SW.  With EPT > 0 every thread keeps
+// the weight bit patterns of its EPT tokens in registers (vocab <= EPT SW),
+// computed once, and rebuilds the fixed-point weight from them; with
+// EPT == 0 each pass recomputes both from the logits (any vocab).
 
-__global__ __launch_bounds__(SW) void k_warp_rows(SampleArgs a, int mode) {
-    __shared__ uint64_t red[SWAVES];
-    __shared__ float redf[SWAVES];
-    __shared__ uint64_t bins[SWAVES][16];
+
+template <int NT>
+__device__ uint32_t block_min_u32(uint32_t v, uint64_t *red) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        v = min(v, (uint32_t)__shfl_xor((int)v, o, 64));
+    if (lane == 0)
+        red[wave] = v;
+    __syncthreads();
+    uint32_t t = 0xffffffffu;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w)
+        t = min(t, (uint32_t)red[w]);
+    __syncthreads();
+    return t;
+}
+
+// NT threads per row: 512 keeps up to 256 registers per lane, room for the
+// cached patterns (EPT of them) and the 16 accumulators.
+// Once at most CAND tokens lie in the search interval, their patterns move
+// to LDS and the remaining passes read only those.
+constexpr int CAND = 2048;
+
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) void k_warp_rows(SampleArgs a, int mode) {
+    constexpr int NWV = NT / 64;
+    __shared__ uint64_t red[NWV];
+    __shared__ float redf[NWV];
+    __shared__ uint64_t bins[NWV][16];
     __shared__ uint64_t bsum[16];
+    __shared__ uint32_t cand[EPT > 0 ? CAND : 1];
     const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int M = a.ctl->m, V = a.vocab;
     if (r >= M)
@@ -137,40 +179,84 @@ __global__ __launch_bounds__(SW) void k_warp_rows(SampleArgs a, int mode) {
     const float T = a.sp.temperature;
 
     float mx = -INFINITY;
-    for (int x = tid; x < V; x += SW)
-        mx = fmaxf(mx, lg[x]);
-    mx = block_max_f(mx, redf);
+    float lv[EPT > 0 ? EPT : 1];
+    if constexpr (EPT > 0) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const int x = tid + i * NT;
+            lv[i] = x < V ? lg[x] : -INFINITY;
+            mx = fmaxf(mx, lv[i]);
+        }
+    } else {
+        for (int x = tid; x < V; x += NT)
+            mx = fmaxf(mx, lg[x]);
+    }
+    mx = block_max_f<NT>(mx, redf);
+    uint32_t cb[EPT > 0 ? EPT : 1];  // weight bit patterns (padding: weight 0)
     uint64_t z = 0;
-    for (int x = tid; x < V; x += SW)
-        z += wfix(warp_w(lg[x], mx, T));
-    z = block_sum_u64(z, red);
+    uint32_t bmin = 0xffffffffu;
+    if constexpr (EPT > 0) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const float w = tid + i * NT < V ? warp_w(lv[i], mx, T) : 0.0f;
+            cb[i] = __float_as_uint(w);
+            z += wfix(w);
+            bmin = tid + i * NT < V ? min(bmin, cb[i]) : bmin;
+        }
+    } else {
+        for (int x = tid; x < V; x += NT) {
+            const float w = warp_w(lg[x], mx, T);
+            z += wfix(w);
+            bmin = min(bmin, __float_as_uint(w));
+        }
+    }
+    z = block_sum_u64<NT>(z, red);
 
-    uint32_t bstar = 0, n_tie = 0xffffffffu;
+    uint32_t bstar = 0, n_tie = ALL_TIES;  // top_p = 1: every token (pattern >= 0)
     uint64_t zs = z;
     if (a.sp.top_p < 1.0f) {
         // target mass: mass >= top_p * Z  <=>  mass >= ceil(top_p * Z) for integer masses
         uint64_t target = (uint64_t)ceil((double)a.sp.top_p * (double)z);
         target = target < 1 ? 1 : target;
         // Largest bit pattern b* with M(b*) >= target, M(b) = mass of w with bits >= b.
-        // Invariant: M(lo) >= target > M(hi); m_hi = M(hi).
-        uint32_t lo = 0, hi = 0x3f800001u;  // every weight is in (0, 1]
+        // Invariant: M(lo) >= target > M(hi); m_hi = M(hi).  Every weight's
+        // pattern is in [min pattern, pattern of 1.0].
+        uint32_t lo = block_min_u32<NT>(bmin, red), hi = 0x3f800001u;
         uint64_t m_hi = 0;
+        bool compacted = false;  // the interval's patterns are cand[0, ncand)
+        int ncand = 0;
         while (hi - lo > 1) {
-            const uint32_t step = (hi - lo + 15) / 16;
+            // lo, hi and step are the same in every thread: keep them scalar
+            lo = __builtin_amdgcn_readfirstlane(lo);
+            hi = __builtin_amdgcn_readfirstlane(hi);
+            const uint32_t step = __builtin_amdgcn_readfirstlane((hi - lo + 15) / 16);
+            // acc_i = mass of the tokens with lo + i step <= bits < hi, so
+            // M(lo + i step) = m_hi + acc_i (thresholds at or past hi stay 0)
             uint64_t acc[16];
 #pragma unroll
             for (int i = 0; i < 16; ++i)
                 acc[i] = 0;
-            for (int x = tid; x < V; x += SW) {
-                const float w = warp_w(lg[x], mx, T);
-                const uint32_t b = __float_as_uint(w);
+            auto add = [&](uint32_t b) {
                 if (b >= lo && b < hi) {
-                    const uint32_t idx = (b - lo) / step;
-                    const uint64_t W = wfix(w);
+                    const uint32_t d = b - lo, W = wfix(__uint_as_float(b));
 #pragma unroll
                     for (int i = 0; i < 16; ++i)
-                        acc[i] += idx == (uint32_t)i ? W : 0;
+                        acc[i] += d >= (uint32_t)i * step ? W : 0u;
                 }
+            };
+            if constexpr (EPT > 0) {
+                if (compacted) {
+                    for (int k = tid; k < ncand; k += NT)
+                        add(cand[k]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < EPT; ++i)
+                        if (tid + i * NT < V)
+                            add(cb[i]);
+                }
+            } else {
+                for (int x = tid; x < V; x += NT)
+                    add(__float_as_uint(warp_w(lg[x], mx, T)));
             }
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -181,43 +267,62 @@ __global__ __launch_bounds__(SW) void k_warp_rows(SampleArgs a, int mode) {
             __syncthreads();
             if (tid < 16) {
                 uint64_t t = 0;
-                for (int w = 0; w < SWAVES; ++w)
+                for (int w = 0; w < NWV; ++w)
                     t += bins[w][tid];
                 bsum[tid] = t;
             }
             __syncthreads();
-            // largest sub-interval start t_i = lo + i step (below hi) with M(t_i) >= target
-            uint64_t above = m_hi;  // M(t_{i+1}) while scanning down
+            // largest threshold t_i below hi with M(t_i) >= target (t_0 = lo qualifies)
             int best = 0;
-            uint64_t m_next = m_hi;
-            for (int i = 15; i >= 0; --i) {
-                if (lo + (uint64_t)i * step >= hi)
-                    continue;
-                const uint64_t mi = above + bsum[i];
-                if (mi >= target) {
+            for (int i = 15; i > 0; --i) {
+                if (lo + (uint64_t)i * step < hi && m_hi + bsum[i] >= target) {
                     best = i;
-                    m_next = above;
                     break;
                 }
-                above = mi;
             }
+            const uint64_t m_next = best < 15 && lo + (uint64_t)(best + 1) * step < hi ? m_hi + bsum[best + 1] : m_hi;
             const uint64_t nh = (uint64_t)lo + (uint64_t)(best + 1) * step;
             hi = nh < hi ? (uint32_t)nh : hi;
             lo = lo + (uint32_t)best * step;
             m_hi = m_next;
             __syncthreads();  // bsum is rewritten by the next pass
+            if constexpr (EPT > 0) {
+                if (!compacted && hi - lo > 1) {
+                    uint64_t n = 0;
+#pragma unroll
+                    for (int i = 0; i < EPT; ++i)
+                        n += (tid + i * NT < V && cb[i] >= lo && cb[i] < hi) ? 1 : 0;
+                    uint64_t tot;
+                    uint64_t pos = block_excl_scan_u64<NT>(n, red, &tot);
+                    if (tot <= CAND) {  // uniform
+#pragma unroll
+                        for (int i = 0; i < EPT; ++i)
+                            if (tid + i * NT < V && cb[i] >= lo && cb[i] < hi)
+                                cand[pos++] = cb[i];
+                        compacted = true;
+                        ncand = (int)tot;
+                        __syncthreads();
+                    }
+                }
+            }
         }
         bstar = lo;
         // the tokens at w*: all of them, or the lowest ids until the target
         uint64_t c_tie = 0;
-        for (int x = tid; x < V; x += SW)
-            c_tie += __float_as_uint(warp_w(lg[x], mx, T)) == bstar ? 1 : 0;
-        c_tie = block_sum_u64(c_tie, red);
+        if constexpr (EPT > 0) {
+#pragma unroll
+            for (int i = 0; i < EPT; ++i)
+                c_tie += (tid + i * NT < V && cb[i] == bstar) ? 1 : 0;
+        } else {
+            for (int x = tid; x < V; x += NT)
+                c_tie += __float_as_uint(warp_w(lg[x], mx, T)) == bstar ? 1 : 0;
+        }
+        c_tie = block_sum_u64<NT>(c_tie, red);
         const uint64_t wstar = wfix(__uint_as_float(bstar));
         uint64_t need = target - m_hi;  // > 0 by the invariant
         uint64_t nt = wstar == 0 ? c_tie : (need + wstar - 1) / wstar;
         nt = nt < c_tie ? nt : c_tie;
-        n_tie = (uint32_t)nt;
+        n_tie = nt == c_tie ? ALL_TIES : (uint32_t)nt;
         zs = m_hi + nt * wstar;
     }
 
@@ -227,12 +332,12 @@ __global__ __launch_bounds__(SW) void k_warp_rows(SampleArgs a, int mode) {
         const int d = a.ctl->tokens[r + 1];
         const float w = warp_w(lg[d], mx, T);
         const uint32_t b = __float_as_uint(w);
-        bool kept = b > bstar || n_tie == 0xffffffffu;
+        bool kept = b > bstar || (b == bstar && n_tie == ALL_TIES);
         if (!kept && b == bstar) {
             uint64_t rank = 0;  // ties with lower ids
-            for (int x = tid; x < d; x += SW)
+            for (int x = tid; x < d; x += NT)
                 rank += __float_as_uint(warp_w(lg[x], mx, T)) == bstar ? 1 : 0;
-            rank = block_sum_u64(rank, red);
+            rank = block_sum_u64<NT>(rank, red);
             kept = rank < n_tie;
         }
         wd = kept ? wfix(w) : 0;
@@ -252,89 +357,141 @@ __global__ __launch_bounds__(SW) void k_warp_rows(SampleArgs a, int mode) {
 // ---------------------------------------------------------------------------
 // Draws.
 
-// The nucleus weight of token x of a row given its rank among the row's
-// tokens at w* (only consulted for those).
+// A row's nucleus: token x is in it when its weight pattern exceeds b*, or
+// equals b* and, unless every such token is, its rank among them by id is
+// below n_tie.
 struct RowView {
     const float *lg;
     float mx, T;
     uint32_t bstar, n_tie;
-    __device__ uint64_t weight(int x, uint64_t &tie_rank, float *wout) const {
+    __device__ bool partial() const { return n_tie != ALL_TIES; }
+    // weight of x (0 outside the nucleus); tie_rank counts the ties seen
+    __device__ uint32_t weight(int x, uint32_t &tie_rank, float *wout) const {
         const float w = warp_w(lg[x], mx, T);
         *wout = w;
         const uint32_t b = __float_as_uint(w);
-        if (n_tie == 0xffffffffu || b > bstar)
+        if (b > bstar)
             return wfix(w);
         if (b == bstar)
-            return tie_rank++ < n_tie ? wfix(w) : 0;
-        return 0;
+            return (!partial() || tie_rank++ < n_tie) ? wfix(w) : 0u;
+        return 0u;
     }
-    __device__ bool is_tie(int x) const {
-        return n_tie != 0xffffffffu && __float_as_uint(warp_w(lg[x], mx, T)) == bstar;
-    }
+    __device__ bool is_tie(int x) const { return __float_as_uint(warp_w(lg[x], mx, T)) == bstar; }
 };
 
 __device__ RowView row_view(const float *lg, const RowStat &s, float T) {
     return RowView{lg, s.mx, T, s.bstar, s.n_tie};
 }
 
-// Inverse-CDF draw with uniform u24 / 2^24 over the weights of p (residual
-// == false) or over fixed(max(0, p_x - q_x)) with p and q normalised by
-// their nucleus masses (residual == true).  Returns the token, or -1 when
+struct DrawScratch {
+    uint64_t red[SWAVES];
+    uint64_t chunk_tot[MAX_DRAW_CHUNKS];
+    uint32_t tie_p[MAX_DRAW_CHUNKS], tie_q[MAX_DRAW_CHUNKS];  // ties before each chunk
+    int sel;
+    uint32_t selw;
+};
+
+// Inverse-CDF draw with uniform u24 / 2^24 over the nucleus weights of p
+// (residual == false) or over fixed(max(0, p_x - q_x)), p and q normalised by
+// their nucleus masses (residual == true), in id order.  Chunk j holds ids
+// [j DRAW_CHUNK, (j + 1) DRAW_CHUNK); thread t its ids j DRAW_CHUNK + 8 t ..
+// + 7.  The chunk totals locate the draw; one exclusive scan inside that
+// chunk locates the thread, which walks its 8 ids.  Ranks among ties are
+// followed only when a row cuts its ties.  Returns the token, or -1 when
 // every weight is zero; *wsel receives the chosen token's weight.
 __device__ int block_draw(const RowView &p, uint64_t zs_p, const RowView &q, uint64_t zs_q, bool residual,
-                          uint32_t u24, int V, uint64_t *wsel, uint64_t *red, int *sel, uint64_t *selw) {
+                          uint32_t u24, int V, uint32_t *wsel, DrawScratch &sc) {
     const int tid = threadIdx.x;
-    const int seg = (V + SW - 1) / SW;
-    const int x0 = min(V, tid * seg), x1 = min(V, x0 + seg);
-    // ranks of this segment's first tie tokens in each row
-    uint64_t tp = 0, tq = 0, tot;
-    for (int x = x0; x < x1; ++x) {
-        tp += p.is_tie(x) ? 1 : 0;
-        if (residual)
-            tq += q.is_tie(x) ? 1 : 0;
-    }
-    uint64_t rp0 = block_excl_scan_u64(tp, red, &tot);
-    uint64_t rq0 = residual ? block_excl_scan_u64(tq, red, &tot) : 0;
+    const int nchunks = (V + DRAW_CHUNK - 1) / DRAW_CHUNK;
+    const bool ranks = p.partial() || (residual && q.partial());
     const float izp = WFIX / (float)zs_p, izq = residual ? WFIX / (float)zs_q : 0.0f;
-    auto wt = [&](int x, uint64_t &rp, uint64_t &rq) -> uint64_t {
+    auto wt = [&](int x, uint32_t &rp, uint32_t &rq) -> uint32_t {
         float wp, wq;
-        const uint64_t Wp = p.weight(x, rp, &wp);
+        const uint32_t Wp = p.weight(x, rp, &wp);
         if (!residual)
             return Wp;
-        const uint64_t Wq = q.weight(x, rq, &wq);
+        const uint32_t Wq = q.weight(x, rq, &wq);
         const float px = Wp ? wp * izp : 0.0f, qx = Wq ? wq * izq : 0.0f;
         return wfix(fmaxf(px - qx, 0.0f));
     };
-    uint64_t s = 0;
-    {
-        uint64_t rp = rp0, rq = rq0;
+    // pass 1: chunk totals (and, with ranks, the ties before each chunk and thread)
+    uint32_t tp_run = 0, tq_run = 0;
+    uint64_t total = 0, tot;
+    for (int j = 0; j < nchunks; ++j) {
+        const int x0 = j * DRAW_CHUNK + 8 * tid, x1 = min(V, x0 + 8);
+        uint32_t rp = 0, rq = 0;
+        if (ranks) {
+            uint32_t cp = 0, cq = 0;
+            for (int x = x0; x < x1; ++x) {
+                cp += p.partial() && p.is_tie(x) ? 1 : 0;
+                cq += residual && q.partial() && q.is_tie(x) ? 1 : 0;
+            }
+            const uint64_t pp = block_excl_scan_u64(cp, sc.red, &tot);
+            if (tid == 0)
+                sc.tie_p[j] = tp_run;
+            rp = tp_run + (uint32_t)pp;
+            tp_run += (uint32_t)tot;
+            const uint64_t pq = block_excl_scan_u64(cq, sc.red, &tot);
+            if (tid == 0)
+                sc.tie_q[j] = tq_run;
+            rq = tq_run + (uint32_t)pq;
+            tq_run += (uint32_t)tot;
+        }
+        uint64_t s = 0;
         for (int x = x0; x < x1; ++x)
             s += wt(x, rp, rq);
+        s = block_sum_u64(s, sc.red);
+        if (tid == 0)
+            sc.chunk_tot[j] = s;
+        total += s;
     }
-    const uint64_t pre = block_excl_scan_u64(s, red, &tot);
     if (tid == 0)
-        *sel = -1;
+        sc.sel = -1;
     __syncthreads();
-    if (tot > 0) {
+    if (total > 0) {
         // floor(u24 * total / 2^24): the draw is the first x whose cumulative mass exceeds it
-        const uint64_t hi = __umul64hi((uint64_t)u24, tot), lo = (uint64_t)u24 * tot;
+        const uint64_t hi = __umul64hi((uint64_t)u24, total), lo = (uint64_t)u24 * total;
         const uint64_t thr = (hi << 40) | (lo >> 24);
-        if (pre <= thr && thr < pre + s) {
-            uint64_t c = pre, rp = rp0, rq = rq0;
+        int js = 0;
+        uint64_t before = 0;
+        while (js + 1 < nchunks && before + sc.chunk_tot[js] <= thr)
+            before += sc.chunk_tot[js++];
+        // pass 2, chunk js only: this thread's 8 ids
+        const int x0 = js * DRAW_CHUNK + 8 * tid, x1 = min(V, x0 + 8);
+        uint32_t rp0 = 0, rq0 = 0;
+        if (ranks) {
+            uint32_t cp = 0, cq = 0;
             for (int x = x0; x < x1; ++x) {
-                const uint64_t w = wt(x, rp, rq);
+                cp += p.partial() && p.is_tie(x) ? 1 : 0;
+                cq += residual && q.partial() && q.is_tie(x) ? 1 : 0;
+            }
+            rp0 = sc.tie_p[js] + (uint32_t)block_excl_scan_u64(cp, sc.red, &tot);
+            rq0 = sc.tie_q[js] + (uint32_t)block_excl_scan_u64(cq, sc.red, &tot);
+        }
+        uint64_t s = 0;
+        {
+            uint32_t rp = rp0, rq = rq0;
+            for (int x = x0; x < x1; ++x)
+                s += wt(x, rp, rq);
+        }
+        const uint64_t pre = before + block_excl_scan_u64(s, sc.red, &tot);
+        if (pre <= thr && thr < pre + s) {
+            uint64_t c = pre;
+            uint32_t rp = rp0, rq = rq0;
+            for (int x = x0; x < x1; ++x) {
+                const uint32_t w = wt(x, rp, rq);
                 c += w;
                 if (c > thr) {
-                    *sel = x;
-                    *selw = w;
+                    sc.sel = x;
+                    sc.selw = w;
                     break;
                 }
             }
         }
     }
     __syncthreads();
-    const int x = *sel;
-    *wsel = *selw;
+    const int x = sc.sel;
+    *wsel = sc.selw;
     __syncthreads();
     return x;
 }
@@ -343,48 +500,50 @@ __device__ int block_draw(const RowView &p, uint64_t zs_p, const RowView &q, uin
 // The decision of one step.
 
 __global__ __launch_bounds__(SW) void k_sample_decide(SampleArgs a, int mode) {
-    __shared__ uint64_t red[SWAVES];
-    __shared__ int sel;
-    __shared__ uint64_t selw;
+    __shared__ DrawScratch sc;
     __shared__ int n_acc;
+    __shared__ bool acc_ok[MAX_ROWS];
     const int tid = threadIdx.x, V = a.vocab;
     DevState *st = a.head.st;
     DevCtl *ctl = const_cast<DevCtl *>(a.ctl);
     const float T = a.sp.temperature;
     const uint64_t seed = a.sp.seed;
     const int e = st->emitted;
-    uint64_t w;
+    uint32_t w;
     if (mode == HEAD_AR) {
         // token e of autoregressive sampling: counter (e, final draw, stage e)
         const RowStat s0 = a.vstat[0];
         const RowView p = row_view(a.vlog, s0, T);
-        const int tok = block_draw(p, s0.zs, p, 0, false, uniform24(seed, e, U_FINAL, e), V, &w, red, &sel, &selw);
+        const int tok = block_draw(p, s0.zs, p, 0, false, uniform24(seed, e, U_FINAL, e), V, &w, sc);
         if (tid == 0)
             ar_commit(a.head, ctl, tok);
     } else if (mode == HEAD_DRAFT) {
         const int j = st->k;
         const RowStat sj = a.dstat[j];
         const RowView q = row_view(a.dlog + (int64_t)j * V, sj, T);
-        const int d = block_draw(q, sj.zs, q, 0, false, uniform24(seed, e + j, U_DRAFT, st->n_stages), V, &w, red,
-                                 &sel, &selw);
+        const int d = block_draw(q, sj.zs, q, 0, false, uniform24(seed, e + j, U_DRAFT, st->n_stages), V, &w, sc);
         if (tid == 0) {
             st->dqw[j] = w;
-            // the top token has weight exactly 2^40, so max q = 2^40 / mass
+            // the top token has weight exactly WFIX, so max q = WFIX / mass
             draft_commit(a.head, ctl, d, (float)((double)WFIX / (double)sj.zs));
         }
     } else {
         const int k = st->k;
         const int64_t stage = st->n_stages;
+        // draft i is accepted when r_i < min(1, p_i(d) / q_i(d)); thread i
+        // evaluates test i, thread 0 finds the first failure
+        if (tid < k) {
+            const double r = (double)uniform24(seed, e + tid, U_ACCEPT, stage) * 0x1p-24;
+            const double pd = (double)a.vstat[tid].wd / (double)a.vstat[tid].zs;
+            const double qd = (double)st->dqw[tid] / (double)a.dstat[tid].zs;
+            const double ratio = pd / qd;
+            acc_ok[tid] = r < (ratio < 1.0 ? ratio : 1.0);
+        }
+        __syncthreads();
         if (tid == 0) {
             int n = 0;
-            for (; n < k; ++n) {
-                const double r = (double)uniform24(seed, e + n, U_ACCEPT, stage) * 0x1p-24;
-                const double pd = (double)a.vstat[n].wd / (double)a.vstat[n].zs;
-                const double qd = (double)st->dqw[n] / (double)a.dstat[n].zs;
-                const double ratio = pd / qd;
-                if (!(r < (ratio < 1.0 ? ratio : 1.0)))
-                    break;
-            }
+            while (n < k && acc_ok[n])
+                ++n;
             n_acc = n;
         }
         __syncthreads();
@@ -396,11 +555,11 @@ __global__ __launch_bounds__(SW) void k_sample_decide(SampleArgs a, int mode) {
         if (n < k) {
             const RowStat sq = a.dstat[n];
             const RowView q = row_view(a.dlog + (int64_t)n * V, sq, T);
-            tok = block_draw(p, sp.zs, q, sq.zs, true, u, V, &w, red, &sel, &selw);
+            tok = block_draw(p, sp.zs, q, sq.zs, true, u, V, &w, sc);
             if (tok < 0)  // an empty residual (rounding): draw from p
-                tok = block_draw(p, sp.zs, p, 0, false, u, V, &w, red, &sel, &selw);
+                tok = block_draw(p, sp.zs, p, 0, false, u, V, &w, sc);
         } else {
-            tok = block_draw(p, sp.zs, p, 0, false, u, V, &w, red, &sel, &selw);
+            tok = block_draw(p, sp.zs, p, 0, false, u, V, &w, sc);
         }
         if (tid == 0)
             stage_commit(a.head, ctl, n, tok);
@@ -411,9 +570,13 @@ hipError_t launch_sample_step(const SampleArgs &a, int max_rows, hipStream_t s) 
     const int mode = a.head.mode;
     if (mode != HEAD_AR && mode != HEAD_DRAFT && mode != HEAD_VERIFY)
         return hipErrorInvalidValue;
-    if (max_rows < 1 || max_rows > MAX_ROWS || a.vocab < 1)
+    if (max_rows < 1 || max_rows > MAX_ROWS || a.vocab < 1 || a.vocab > MAX_DRAW_CHUNKS * DRAW_CHUNK)
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_warp_rows, dim3(mode == HEAD_VERIFY ? max_rows : 1), dim3(SW), 0, s, a, mode);
+    const dim3 grid(mode == HEAD_VERIFY ? max_rows : 1);
+    if (a.vocab <= 64 * 512)
+        hipLaunchKernelGGL((k_warp_rows<512, 64>), grid, dim3(512), 0, s, a, mode);
+    else
+        hipLaunchKernelGGL((k_warp_rows<SW, 0>), grid, dim3(SW), 0, s, a, mode);
     hipLaunchKernelGGL(k_sample_decide, dim3(1), dim3(SW), 0, s, a, mode);
     return hipGetLastError();
 }

@@ -770,6 +770,8 @@ sd_status use_sampling(sd_model *m, const SampleParams *sp) {
         return fail(SD_ERR_INVALID_ARG, "temperature must be positive and finite");
     if (!(sp->top_p > 0.0f) || !(sp->top_p <= 1.0f))
         return fail(SD_ERR_INVALID_ARG, "top_p must be in (0, 1]");
+    if (m->cfg.vocab > MAX_SAMPLE_VOCAB)
+        return fail(SD_ERR_INVALID_ARG, "sampling takes vocabularies of at most 524288 ids");
     m->sp_cur = *sp;
     return SD_OK;
 }

@@ -151,11 +151,11 @@ struct HeadArgs {
 // Sampling variant.  The warped distribution of a row of logits l is
 // w_x = exp((l_x - max l) / T) restricted to its top-p nucleus: the shortest
 // prefix of the tokens in (w descending, id ascending) order whose mass
-// reaches top_p.  Masses are fixed point, W_x = trunc(w_x 2^40) in uint64,
-// so every sum, cut and cumulative mass is exact and independent of the
-// summation order.  The nucleus is {w_x > w*} plus the first n_tie tokens
-// (by id) with w_x == w*.
-constexpr float WFIX = 1099511627776.0f;  // 2^40
+// reaches top_p.  Masses are fixed point, W_x = trunc(w_x 2^31) (at most
+// 2^31, as w_x <= 1), summed in uint64, so every sum, cut and cumulative
+// mass is exact and independent of the summation order.  The nucleus is
+// {w_x > w*} plus the first n_tie tokens (by id) with w_x == w*.
+constexpr float WFIX = 2147483648.0f;  // 2^31
 
 struct SampleParams {
     float temperature;
@@ -251,6 +251,7 @@ hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s)
 // statistics of every row (one work-group per row, up to max_rows), then the
 // decision of the step in one work-group (draw, acceptance, state update).
 hipError_t launch_sample_step(const SampleArgs &a, int max_rows, hipStream_t s);
+constexpr int32_t MAX_SAMPLE_VOCAB = 524288;  // largest vocabulary the sampling kernels take
 hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s);
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);

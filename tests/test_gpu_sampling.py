@@ -155,3 +155,28 @@ def test_sampling_rejects_bad_parameters():
             dm.generate_sd_sample(pr, 4, None, 2, T, p, 0, gamma=0.5)
         with pytest.raises(binding.SDError):
             dm.generate_ar_sample(pr, 4, T, p, 0)
+
+
+def test_cut_through_tied_tokens():
+    """Identical lm-head rows give every token the same logit: the warped
+    distribution is uniform, the nucleus is the ceil(top_p V) lowest ids (a
+    cut through one group of ties), the draft equals the full model (every
+    draft accepted), and the draws are uniform over the nucleus."""
+    cfg = U.MICRO_GQA
+    w = S.make_weights(cfg, 3)
+    w["lm_head"] = np.repeat(w["lm_head"][:1], cfg.vocab, axis=0).copy()
+    dm = U.device_model(cfg, w)
+    om = oracle.Model(cfg, w)
+    pr = S.prompt(cfg, 5, seed=2)
+    top_p = _f32(0.3)
+    keep = int(np.ceil(top_p * cfg.vocab))
+    ref = om.generate_sd_sample(pr, 30, S.skip_mask(cfg, "random2", seed=11), 4, 0.7, top_p, 5, gamma=0.0)
+    counts = np.zeros(cfg.vocab)
+    for seed in range(60):
+        tok, st = dm.generate_sd_sample(pr, 30, S.skip_mask(cfg, "random2", seed=11), 4, 0.7, top_p, seed, gamma=0.0)
+        assert st["n_accepted"] == st["n_drafted"]
+        if seed == 5:
+            assert np.array_equal(tok, ref["tokens"])
+        np.add.at(counts, tok, 1)
+    assert counts[keep:].sum() == 0 and np.all(counts[:keep] > 0)
+    assert P._chi2_pvalue(counts[:keep], np.full(keep, 1.0 / keep)) > 1e-3
