@@ -372,19 +372,60 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
             acc[r][i] = 0.0f;
     }
 
+    // Up to 4 rows, every row's product is computed, whatever the row count
+    // (the X buffers hold MAX_ROWS rows; rows past M are never stored), and
+    // the weight, gain and X loads of an iteration are all issued before the
+    // first is used: a branch around the X loads, or unpacking as loads
+    // arrive, would make the compiler wait for each group of loads in turn.
+    constexpr bool BATCH = MR > 1 && MR <= 4 && sizeof(TW) == 2;
     for (int c = tid; c < nch; c += 256) {
         float w[R][8];
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            ldw8(W + roff[i] + (int64_t)c * 8, w[i]);
         float g[8];
-        if constexpr (NORM)
-            ldg8(G + c * 8, g);
+        float xb[BATCH ? MR : 1][8];
+        if constexpr (BATCH) {
+            u32x4_t wr[R], gr;
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                wr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(W + roff[i] + (int64_t)c * 8));
+            if constexpr (NORM)
+                gr = *reinterpret_cast<const u32x4_t *>(G + c * 8);
+            f32x4_t xr[MR][2];
+#pragma unroll
+            for (int r = 0; r < MR; ++r) {
+                xr[r][0] = reinterpret_cast<const f32x4_t *>(a.X + (int64_t)r * a.ldx + c * 8)[0];
+                xr[r][1] = reinterpret_cast<const f32x4_t *>(a.X + (int64_t)r * a.ldx + c * 8)[1];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                unpack8(wr[i], w[i]);
+            if constexpr (NORM)
+                unpack8(gr, g);
+#pragma unroll
+            for (int r = 0; r < MR; ++r)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    xb[r][k] = xr[r][0][k];
+                    xb[r][4 + k] = xr[r][1][k];
+                }
+        } else {
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                ldw8(W + roff[i] + (int64_t)c * 8, w[i]);
+            if constexpr (NORM)
+                ldg8(G + c * 8, g);
+        }
 #pragma unroll
         for (int r = 0; r < MR; ++r) {
-            if (r < M) {
+            if (BATCH || r < M) {
                 float x[8];
-                ldg8(a.X + (int64_t)r * a.ldx + c * 8, x);
+                if constexpr (BATCH) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        x[k] = xb[r][k];
+                } else {
+                    ldg8(a.X + (int64_t)r * a.ldx + c * 8, x);
+                }
                 if constexpr (NORM) {
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {

@@ -180,11 +180,13 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
         p.epi = EPI_HEAD;
         break;
     }
-    // Two rows (one-draft verification): the normed layers run on MFMA with
+    // Two rows (one-draft verification): QKV and the lm-head run on MFMA with
     // the norm folded in, fed by the VALU output projections, which prepare
-    // g * h for them (no norm kernel); the output projections stay VALU.
-    const bool fused2 = rows == 2 && (kind == LK_QKV || kind == LK_GATE_UP || kind == LK_HEAD) &&
-                        mfma_ok(m, LK_QKV) && mfma_ok(m, LK_GATE_UP) && mfma_ok(m, LK_HEAD);
+    // g * h for them (no norm kernel); the output projections and gate/up
+    // stay VALU (gate/up with 8 weight rows per work-group, 50.8 against
+    // 53.4 us on MFMA at the 13B shape).
+    const bool fused2 = rows == 2 && (kind == LK_QKV || kind == LK_HEAD) && mfma_ok(m, LK_QKV) &&
+                        mfma_ok(m, LK_GATE_UP) && mfma_ok(m, LK_HEAD);
     if ((rows > 2 || fused2) && mfma_ok(m, kind)) {
         p.path = PATH_MFMA;
         p.fused_norm = fused2;
@@ -213,7 +215,7 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
     p.path = rows == 1 ? PATH_GEMV : (rows <= 2 ? PATH_VALU2 : PATH_VALU16);
     // weight rows per work-group: 8 for the wide layers of the one-row GEMV,
     // 4 otherwise (the QKV tile also holds whole rotary pairs)
-    const int wide = rows == 1 ? 8 : 4;
+    const int wide = (rows == 1 || (rows == 2 && kind == LK_GATE_UP)) ? 8 : 4;
     if (kind == LK_QKV) {
         p.rows = qkv_gemv_rows(c.head_dim, rows <= 2 ? 8 : 4);
         p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
