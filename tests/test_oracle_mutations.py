@@ -155,3 +155,58 @@ def test_planted_sampling_mistake_is_caught(name, tmp_path):
     mutated.write_text(src.replace(old, new))
     lib = oracle.build(src=str(mutated), out=str(tmp_path / f"liboracle_{name}.so"))
     assert not _sampling_pins_hold(lib), f"planted mistake {name} passed every sampling pin"
+
+
+# Mistakes in the skip-set search, caught by the pins of test_oracle_search.py.
+SEARCH_SRC = os.path.join(os.path.dirname(oracle.__file__), "skip_search.py")
+SEARCH_MUTATIONS = {
+    "philox_key": ("philox4x64([a, purpose, c, 0], [seed, 1])", "philox4x64([a, purpose, c, 0], [seed, 0])"),
+    "ei_sign": ("imp = best - mu - xi", "imp = mu - best - xi"),
+    "ei_no_sigma": ("return imp * cdf + sigma * pdf", "return imp * cdf + pdf"),
+    "kernel_not_scaled_by_L": ("np.exp(-hamming / (length_scale * A.shape[1]))", "np.exp(-hamming / length_scale)"),
+    "posterior_var_sign": ("var = 1.0 - np.sum(", "var = 1.0 + np.sum("),
+    "no_noise": ("+ noise * np.eye(len(X))", ""),
+    "standardise_sample_sd": ("np.sqrt(np.mean((y - y.mean()) ** 2))",
+                              "np.sqrt(np.sum((y - y.mean()) ** 2) / max(len(y) - 1, 1))"),
+    "worst_incumbent": ("incumbent = X[int(np.argmin(y))]", "incumbent = X[int(np.argmax(y))]"),
+    "pick_least_ei": ("pick = int(np.argmax(ei))", "pick = int(np.argmin(ei))"),
+    "best_is_max": ("best = float(ys.min())", "best = float(ys.max())"),
+    "four_flips": ("flips = 1 + int(search_uniform(seed, t, P_NFLIP, c) * 3.0)",
+                   "flips = 1 + int(search_uniform(seed, t, P_NFLIP, c) * 4.0)"),
+    "density_range": ("p = 0.6 * search_uniform(seed, t, P_DENSITY, c)", "p = search_uniform(seed, t, P_DENSITY, c)"),
+    "no_dedupe": ("if not any(np.array_equal(z, x) for x in X)]", "]"),
+    "draft_mlp_cost_on_attention": ("att = int(np.sum(mask[0::2] == 0))", "att = int(np.sum(mask[1::2] == 0))"),
+}
+
+
+def _search_module(src: str):
+    """The search oracle executed from src, as a module of the oracle package."""
+    import types
+
+    mod = types.ModuleType("oracle._mutated_skip_search")
+    mod.__package__ = "oracle"
+    exec(compile(src, SEARCH_SRC, "exec"), mod.__dict__)
+    return mod
+
+
+def _search_pins_hold(mod) -> bool:
+    from tests import test_oracle_search as P
+
+    try:
+        for check in P.ALL_CHECKS:
+            check(mod)
+        return True
+    except (AssertionError, IndexError, ValueError, np.linalg.LinAlgError):
+        return False
+
+
+def test_unmodified_search_oracle_passes():
+    assert _search_pins_hold(_search_module(open(SEARCH_SRC).read()))
+
+
+@pytest.mark.parametrize("name", sorted(SEARCH_MUTATIONS))
+def test_planted_search_mistake_is_caught(name):
+    old, new = SEARCH_MUTATIONS[name]
+    src = open(SEARCH_SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    assert not _search_pins_hold(_search_module(src.replace(old, new))), f"planted mistake {name} passed every pin"
