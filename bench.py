@@ -444,6 +444,111 @@ def run_sampling(args):
 
 
 # ---------------------------------------------------------------------------
+# skip-set search (labelled supplementary runs)
+
+
+def strategy_mask(cfg, n_att: int, n_mlp: int, where: str, seed: int = 0) -> np.ndarray:
+    """A mask skipping n_att attention and n_mlp MLP sublayers at the first,
+    middle or last layers, or at random ones (the fixed strategies the
+    paper's appendix compares with the searched mask)."""
+    L = cfg.n_layers
+    z = np.zeros(2 * L, np.uint8)
+    g = np.random.default_rng(seed)
+    for kind, n in ((0, n_att), (1, n_mlp)):
+        if where == "first":
+            layers = np.arange(n)
+        elif where == "last":
+            layers = np.arange(L - n, L)
+        elif where == "mid":
+            layers = np.arange((L - n) // 2, (L - n) // 2 + n)
+        else:
+            layers = g.choice(L, size=n, replace=False)
+        z[2 * layers + kind] = 1
+    return z
+
+
+def run_search(args):
+    import torch  # noqa: F401
+
+    from paper_2309_08168_amd import binding
+
+    wl = S.WORKLOADS[args.workload]
+    cfg = S.MODELS[wl.model]
+    planted = S.skip_mask(cfg, args.search_mask, args.seed)
+    host = S.make_weights(cfg, args.seed)
+    w = S.plant_redundancy(cfg, host, planted, 0.0, 16.0)
+    model = binding.Model(cfg, binding.DeviceWeights(cfg, w))
+    dev = np.stack([S.prompt(cfg, args.search_prompt_len, seed=100 + i) for i in range(args.search_prompts)])
+    held = np.stack([S.prompt(cfg, args.search_prompt_len, seed=200 + i) for i in range(args.search_prompts)])
+    new_dev, new_held = args.search_new, 4 * args.search_new
+    model.generate_sd(dev[0], new_dev, planted, wl.k_max, wl.gamma)  # first-call set-up
+    prm = dict(n_init=args.search_init, iterations=args.search_iters, n_candidates=256, length_scale=0.5, noise=1e-3,
+               xi=0.01, seed=args.seed)
+    log(f"search: {cfg.name}, {2 * cfg.n_layers} sublayers, planted {int(planted.sum())}, "
+        f"{prm['n_init'] + prm['iterations']} evaluations of {len(dev)} x {new_dev} tokens")
+    t0 = time.perf_counter()
+    res = model.search_skip_set(dev, new_dev, wl.k_max, gamma=wl.gamma, objective="measured", **prm)
+    wall = time.perf_counter() - t0
+    best = res["best_mask"]
+    log(f"search done in {wall:.1f} s; best {res['best_value']:.4f} ms/token")
+
+    def decode_ms(prompts, n, mask):
+        tot, acc, drafted = 0.0, 0, 0
+        for pr in prompts:
+            if mask is None:
+                _, st = model.generate_ar(pr, n)
+            else:
+                _, st = model.generate_sd(pr, n, mask, wl.k_max, wl.gamma)
+                acc += st["n_accepted"]
+                drafted += st["n_drafted"]
+            tot += st["decode_ms"]
+        return tot / (len(prompts) * n), (acc / drafted if drafted else None)
+
+    n_att, n_mlp = int(best[0::2].sum()), int(best[1::2].sum())
+    masks = {"searched": best, "planted": planted, "none": np.zeros_like(best)}
+    for where in ("first", "mid", "last", "random"):
+        masks[where] = strategy_mask(cfg, n_att, n_mlp, where, args.seed)
+    ar_ms, _ = decode_ms(held, new_held, None)
+    table = {}
+    for name, z in masks.items():
+        decode_ms(held[:1], new_held, z)  # warm
+        ms, acc = decode_ms(held, new_held, z)
+        table[name] = {"ms_per_token": round(ms, 4), "speedup_vs_ar": round(ar_ms / ms, 4),
+                       "acceptance": None if acc is None else round(acc, 4),
+                       "attention_skipped": int(z[0::2].sum()), "mlp_skipped": int(z[1::2].sum())}
+        log(f"{name}: {json.dumps(table[name])}")
+    # host cost of the search itself, objective aside: the same steps over a
+    # free objective, and the oracle's search on a few of them
+    t0 = time.perf_counter()
+    binding.search_skip_set_fn(lambda z: float(z.sum()), 2 * cfg.n_layers, **prm)
+    native_s = time.perf_counter() - t0
+    steps = prm["n_init"] + prm["iterations"]
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import skip_search as O
+
+        k = 12
+        t0 = time.perf_counter()
+        O.search(lambda z: float(z.sum()), 2 * cfg.n_layers, **{**binding.SEARCH_DEFAULTS, **prm, "iterations": k})
+        osec = time.perf_counter() - t0
+        cpu = {"value": round(osec / (prm["n_init"] + k) * 1e3, 3), "unit": "ms per evaluation (search host cost)",
+               "cores": 1, "kind": "oracle",
+               "sample": f"oracle search of {prm['n_init']} + {k} evaluations of a free objective over "
+                         f"{2 * cfg.n_layers} sublayers, {prm['n_candidates']} candidates per step; {osec:.1f} s"}
+    print(json.dumps({
+        "mode": "skip-set search (labelled supplementary)", "workload": wl.name, "weights": "planted rho 0 gain 16",
+        "planted_mask": args.search_mask, "planted_sublayers": int(planted.sum()), "k_max": wl.k_max, "gamma": wl.gamma, "params": prm,
+        "dev_prompts": [len(dev), args.search_prompt_len, new_dev], "held_out": [len(held), new_held],
+        "evaluations": len(res["values"]), "search_wall_s": round(wall, 2),
+        "search_best_ms_per_token": round(res["best_value"], 4),
+        "initial_best_ms_per_token": round(float(res["values"][:prm["n_init"]].min()), 4),
+        "overlap_with_planted": int(np.sum(best & planted)),
+        "search_host_ms_per_evaluation": round(native_s / steps * 1e3, 3), "cpu_baseline": cpu,
+        "ar_ms_per_token": round(ar_ms, 4), "masks": table}))
+    model.close()
+
+
+# ---------------------------------------------------------------------------
 # profiler helpers
 
 
@@ -532,6 +637,13 @@ def main():
                     help="rho:head_gain:gamma triples for --supplementary")
     ap.add_argument("--sampling", action="store_true",
                     help="labelled runs of the sampling variant (temperature, top-p) against AR sampling")
+    ap.add_argument("--search", action="store_true", help="skip-set search on the planted model (supplementary)")
+    ap.add_argument("--search-prompts", type=int, default=2)
+    ap.add_argument("--search-prompt-len", type=int, default=32)
+    ap.add_argument("--search-mask", default="random36", help="the planted redundant sublayers")
+    ap.add_argument("--search-new", type=int, default=32)
+    ap.add_argument("--search-init", type=int, default=16)
+    ap.add_argument("--search-iters", type=int, default=144)
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--with-copy", action="store_true", help="also run the calibration copy after the bench")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
@@ -562,6 +674,8 @@ def main():
         run_supplementary(args)
     elif args.sampling:
         run_sampling(args)
+    elif args.search:
+        run_search(args)
     else:
         run_bench(args)
     if args.with_copy:

@@ -216,6 +216,78 @@ sd_status sd_self_spec_sample(sd_model *model, const int32_t *prompt, int32_t pr
 sd_status sd_autoregressive_sample(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,
                                    const sd_sampling *sampling, int32_t *out_tokens, sd_stats *stats);
 
+/* Skip-set search (Sec. 3.3, Eq. 1): z* = argmin f(z) over sublayer masks
+ * z in {0, 1}^L, by Bayesian optimisation for a fixed number of steps.
+ * Host code; every evaluation of f is one call of the objective.
+ *   - n_init initial masks, mask i with each bit set with probability
+ *     0.6 i / n_init (mask 0 is empty);
+ *   - surrogate: a zero-mean Gaussian process over the standardised
+ *     observations (mean 0, population deviation 1; a deviation below 1e-12
+ *     counts as 1), kernel exp(-hamming(a, b) / (length_scale L)), noise
+ *     variance `noise` on the observations;
+ *   - acquisition: expected improvement below the smallest standardised
+ *     observation by xi, of the posterior of the noise-free value;
+ *   - each step scores n_candidates masks, the first half 1 to 3 random
+ *     flips of the incumbent (the best mask so far, first on ties), the
+ *     rest random masks with one density drawn from [0, 0.6); masks
+ *     evaluated before are dropped, the first maximiser of EI is evaluated,
+ *     and a step with no new candidate evaluates nothing;
+ *   - random numbers: top 24 bits of the first word of Philox4x64-10 with
+ *     key (seed, 1), counter (index, purpose, sub-index, 0).
+ * Limits: 1 <= L <= 1024, n_init + iterations <= 4096, n_candidates <= 65536. */
+typedef enum { SD_SEARCH_MEASURED = 0, SD_SEARCH_MODELED = 1 } sd_search_objective;
+
+typedef struct {
+    int32_t n_init;       /* >= 1 */
+    int32_t iterations;   /* BO steps after the initial masks, >= 0 */
+    int32_t n_candidates; /* >= 1 */
+    double length_scale;  /* > 0 */
+    double noise;         /* > 0: observation noise variance of the standardised values */
+    double xi;            /* finite */
+    uint64_t seed;
+    int32_t objective;    /* sd_search_skip_set only: an sd_search_objective */
+    /* SD_SEARCH_MODELED costs (finite): a draft step costs cost[0] + cost[1] per
+     * attention + cost[2] per MLP sublayer it runs; a verification cost[3]
+     * + cost[4] per row (drafts + 1) */
+    double cost[5];
+} sd_search_params;
+
+/* Outputs.  best_mask is required; the arrays may be NULL, else they hold
+ * n_init + iterations entries of which the first n_evaluated are written. */
+typedef struct {
+    uint8_t *best_mask; /* HOST uint8 [L]: the evaluated mask of least f (the first on ties) */
+    double best_value;
+    int32_t n_evaluated;
+    uint8_t *masks;     /* HOST uint8 [n_init + iterations][L]: evaluated masks in order */
+    double *values;     /* HOST [n_init + iterations]: f of each */
+    double *margins;    /* HOST [n_init + iterations]: EI of the chosen candidate minus the largest EI
+                         * below it (infinity for the initial masks and for a single EI value) */
+} sd_search_result;
+
+/* The objective of sd_search_skip_set_fn: writes f(mask) to *value and
+ * returns SD_OK, or another status, which stops the search with it. */
+typedef sd_status (*sd_search_objective_fn)(const uint8_t *mask, int32_t n_dims, void *user, double *value);
+
+/* Search over masks of n_dims bits with a caller's objective (finite values).
+ * params->objective and cost are ignored.  Errors: INVALID_ARG (also for a
+ * non-finite objective value or a surrogate that is not positive definite),
+ * OOM, or the objective's status. */
+sd_status sd_search_skip_set_fn(int32_t n_dims, const sd_search_params *params, sd_search_objective_fn objective,
+                                void *user, sd_search_result *result);
+
+/* Search of the model's skip mask (L = 2 n_layers, layout of sd_forward),
+ * f(z) the time per emitted token of self-speculative decoding of max_new
+ * tokens after each of n_prompts HOST prompts of prompt_len ids (row-major
+ * [n_prompts][prompt_len]), with K_max and gamma (adaptive, when not NULL,
+ * as in sd_self_spec_generate_adaptive).  SD_SEARCH_MEASURED: summed
+ * decode_ms / (n_prompts max_new); SD_SEARCH_MODELED: the costs above summed
+ * over the stages of every decode / (n_prompts max_new), a function of the
+ * decoded tokens only.  Errors: as sd_self_spec_generate and
+ * sd_search_skip_set_fn. */
+sd_status sd_search_skip_set(sd_model *model, const int32_t *prompts, int32_t n_prompts, int32_t prompt_len,
+                             int32_t max_new, int32_t K_max, float gamma, const sd_adaptive *adaptive,
+                             const sd_search_params *params, sd_search_result *result);
+
 /* Measurement hook.  Selects one linear-layer class whose launches the
  * library brackets with HIP events on its stream: layer 0 = QKV, 1 = attention
  * output, 2 = gate/up, 3 = down, 4 = lm-head; rows = 1, 2 or 16 selects the

@@ -73,6 +73,7 @@ class SDStats(ctypes.Structure):
     _fields_ = [
         ("n_stages", ctypes.c_int64), ("n_drafted", ctypes.c_int64), ("n_accepted", ctypes.c_int64),
         ("n_emitted", ctypes.c_int64), ("n_draft_steps", ctypes.c_int64), ("min_gamma_gap", ctypes.c_double),
+        ("min_draft_margin", ctypes.c_double),
     ]
 
 
@@ -229,6 +230,7 @@ class Model:
             "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
             "draft_pmax": pm[: st.n_draft_steps].copy(), "n_stages": st.n_stages, "n_drafted": st.n_drafted,
             "n_accepted": st.n_accepted, "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
+            "min_draft_margin": st.min_draft_margin,
         }
 
     def generate_sd_adaptive(self, prompt, max_new: int, skip, k_max: int, **params):
@@ -251,9 +253,8 @@ class Model:
             "tokens": out, "margin": margin, "stages": log[: st.n_stages].copy(),
             "draft_pmax": pm[: st.n_draft_steps].copy(), "gammas": glog[: st.n_stages].copy(),
             "n_stages": st.n_stages, "n_drafted": st.n_drafted, "n_accepted": st.n_accepted,
-            "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap,
+            "n_emitted": st.n_emitted, "min_gamma_gap": st.min_gamma_gap, "min_draft_margin": st.min_draft_margin,
         }
-
 
     def generate_ar_sample(self, prompt, max_new: int, temperature: float, top_p: float, seed: int):
         sp = Sampling(temperature, top_p, seed)

@@ -535,6 +535,7 @@ static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t m
     orc_sd_stats st;
     memset(&st, 0, sizeof st);
     st.min_gamma_gap = INFINITY;
+    st.min_draft_margin = INFINITY;
     /* Reading: the draft shares the one KV cache.  Draft steps write K/V of
      * the non-skipped attention sublayers at the draft positions; the
      * verification forward overwrites those positions at every layer, and
@@ -567,9 +568,12 @@ static int generate_sd(orc_model *m, const int32_t *prompt, int32_t t, int32_t m
         for (int32_t j = 0; j < kcap; ++j) {
             int32_t in = j == 0 ? last : draft[j - 1];
             float p;
-            rc = orc_forward(m, c, &in, 1, skip, NULL, &draft[j], &p, NULL);
+            double dm;
+            rc = orc_forward(m, c, &in, 1, skip, NULL, &draft[j], &p, &dm);
             if (rc)
                 break;
+            if (dm < st.min_draft_margin)
+                st.min_draft_margin = dm;
             if (draft_pmax)
                 draft_pmax[st.n_draft_steps] = p;
             st.n_draft_steps++;
@@ -854,6 +858,7 @@ int orc_generate_sd_sample(orc_model *m, const int32_t *prompt, int32_t t, int32
     orc_sd_stats st;
     memset(&st, 0, sizeof st);
     st.min_gamma_gap = INFINITY;
+    st.min_draft_margin = INFINITY;
     orc_cache *c = orc_cache_create(m, t + max_new + k_max + 1);
     int32_t *draft = (int32_t *)malloc(sizeof(int32_t) * K1);
     int32_t *rows = (int32_t *)malloc(sizeof(int32_t) * K1);

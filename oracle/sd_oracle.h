@@ -60,6 +60,7 @@ typedef struct {
     int64_t n_emitted;     /* tokens emitted (= max_new) */
     int64_t n_draft_steps; /* draft forwards run (= n_drafted) */
     double min_gamma_gap;  /* min over draft steps of |p_max - gamma| */
+    double min_draft_margin; /* min over greedy draft steps of the top-2 logit margin (inf when sampling) */
 } orc_sd_stats;
 
 /* Errors: 0 ok, -1 invalid argument, -2 KV capacity exceeded, -3 out of memory. */

@@ -14,7 +14,7 @@ definite reading of every other detail, step by step:
 - z has one bit per sublayer, entry 2l the attention and 2l+1 the MLP of
   layer l (L = 2 n_layers, the count the paper gives for LLaMA-2-70B);
 - initial design: n_init masks, mask i with each bit set with probability
-  0.6 (i + 1) / (n_init + 1);
+  0.6 i / n_init, so mask 0 is empty (the full model as its own draft);
 - surrogate: the observations are standardised (mean 0, population
   standard deviation 1; a deviation below 1e-12 counts as 1); a zero-mean GP
   with kernel k(a, b) = exp(-hamming(a, b) / (length_scale L)) and
@@ -58,7 +58,7 @@ def search_uniform(seed: int, a: int, purpose: int, c: int) -> float:
 
 
 def initial_mask(seed: int, i: int, n_init: int, L: int) -> np.ndarray:
-    p = 0.6 * (i + 1) / (n_init + 1)
+    p = 0.6 * i / n_init
     return np.array([search_uniform(seed, i, P_INIT, j) < p for j in range(L)], np.uint8)
 
 
@@ -90,11 +90,19 @@ def kernel(A: np.ndarray, B: np.ndarray, length_scale: float) -> np.ndarray:
 
 def posterior(X: np.ndarray, ys: np.ndarray, Z: np.ndarray, length_scale: float, noise: float):
     """GP posterior mean and standard deviation of the noise-free values at
-    the rows of Z, given standardised observations ys at the rows of X."""
+    the rows of Z, given standardised observations ys at the rows of X.
+
+    One row of Z at a time: two masks at the same distances from every
+    observation then get the same values to the last bit, so such ties go
+    to the first of them (batched products may round rows differently)."""
     K = kernel(X, X, length_scale) + noise * np.eye(len(X))
-    Ks = kernel(Z, X, length_scale)
-    mu = Ks @ np.linalg.solve(K, ys)
-    var = 1.0 - np.sum(Ks * np.linalg.solve(K, Ks.T).T, axis=1)
+    alpha = np.linalg.solve(K, ys)
+    mu = np.empty(len(Z))
+    var = np.empty(len(Z))
+    for i, z in enumerate(np.atleast_2d(Z)):
+        k = kernel(z, X, length_scale)[0]
+        mu[i] = k @ alpha
+        var[i] = 1.0 - k @ np.linalg.solve(K, k)
     return mu, np.sqrt(np.maximum(var, 0.0))
 
 

@@ -24,7 +24,7 @@ EXPORTS = (
     "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
     "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
-    "sd_self_spec_sample", "sd_autoregressive_sample",
+    "sd_self_spec_sample", "sd_autoregressive_sample", "sd_search_skip_set_fn", "sd_search_skip_set",
     "sd_model_time_kernel", "sd_model_kernel_time",
     "sd_last_error", "sd_version",
 )
@@ -71,6 +71,32 @@ class sd_sampling(ctypes.Structure):
     _fields_ = [("temperature", ctypes.c_float), ("top_p", ctypes.c_float), ("seed", ctypes.c_uint64)]
 
 
+SD_SEARCH_MEASURED, SD_SEARCH_MODELED = 0, 1
+
+
+class sd_search_params(ctypes.Structure):
+    _fields_ = [
+        ("n_init", ctypes.c_int32), ("iterations", ctypes.c_int32), ("n_candidates", ctypes.c_int32),
+        ("length_scale", ctypes.c_double), ("noise", ctypes.c_double), ("xi", ctypes.c_double),
+        ("seed", ctypes.c_uint64), ("objective", ctypes.c_int32), ("cost", ctypes.c_double * 5),
+    ]
+
+
+class sd_search_result(ctypes.Structure):
+    _fields_ = [
+        ("best_mask", ctypes.POINTER(ctypes.c_uint8)), ("best_value", ctypes.c_double),
+        ("n_evaluated", ctypes.c_int32), ("masks", ctypes.POINTER(ctypes.c_uint8)),
+        ("values", ctypes.POINTER(ctypes.c_double)), ("margins", ctypes.POINTER(ctypes.c_double)),
+    ]
+
+
+SEARCH_OBJECTIVE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.POINTER(ctypes.c_double))
+
+# Defaults of the skip-set search.
+SEARCH_DEFAULTS = dict(n_init=8, iterations=32, n_candidates=64, length_scale=0.25, noise=1e-3, xi=0.01, seed=0)
+
+
 # The paper's adaptive-exit settings (gamma0, epsilon, beta1, beta2; alpha
 # for LLaMA-2-13B on CNN/DM).
 PAPER_ADAPTIVE = dict(gamma0=0.6, alpha=0.9, epsilon=0.01, beta1=0.5, beta2=0.9)
@@ -105,6 +131,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_self_spec_sample": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_sampling), vp, p(sd_stats)],
                                 ctypes.c_int),
         "sd_autoregressive_sample": ([vp, vp, i32, i32, p(sd_sampling), vp, p(sd_stats)], ctypes.c_int),
+        "sd_search_skip_set_fn": ([i32, p(sd_search_params), SEARCH_OBJECTIVE_FN, vp, p(sd_search_result)],
+                                  ctypes.c_int),
+        "sd_search_skip_set": ([vp, vp, i32, i32, i32, i32, ctypes.c_float, vp, p(sd_search_params),
+                                p(sd_search_result)], ctypes.c_int),
         "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
         "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
                                   p(ctypes.c_int64), p(ctypes.c_int64)], ctypes.c_int),
@@ -290,6 +320,21 @@ class Model:
                                          ctypes.byref(st)))
         return out[:max_new], _stats(st, log, glog)
 
+    def search_skip_set(self, prompts, max_new: int, k_max: int, gamma: Optional[float] = None,
+                        adaptive: Optional[dict] = None, objective: str = "measured", cost=None, **params) -> dict:
+        """sd_search_skip_set over the rows of prompts (int array [n, t]):
+        objective "measured" (GPU time per token) or "modeled" (cost, five
+        floats); params override SEARCH_DEFAULTS."""
+        if gamma is None and adaptive is None:
+            raise ValueError("gamma or adaptive is required")
+        ad = None if adaptive is None else sd_adaptive(**{**PAPER_ADAPTIVE, **adaptive})
+        pr = np.ascontiguousarray(np.atleast_2d(prompts), dtype=np.int32)
+        kind = {"measured": SD_SEARCH_MEASURED, "modeled": SD_SEARCH_MODELED}[objective]
+        L = 2 * self.cfg.n_layers
+        return _search_call(lambda sp, res: load().sd_search_skip_set(
+            self._h, _ptr(pr), pr.shape[0], pr.shape[1], max_new, k_max, ctypes.c_float(0.0 if gamma is None else gamma),
+            None if ad is None else ctypes.byref(ad), sp, res), L, kind, cost, params)
+
     def generate_ar_sample(self, prompt, max_new: int, temperature: float, top_p: float, seed: int):
         sp = sd_sampling(temperature, top_p, seed)
         pr = np.ascontiguousarray(prompt, dtype=np.int32)
@@ -298,6 +343,49 @@ class Model:
         check(load().sd_autoregressive_sample(self._h, _ptr(pr), pr.size, max_new, ctypes.byref(sp), _ptr(out),
                                               ctypes.byref(st)))
         return out[:max_new], _stats(st, None)
+
+
+def _search_call(call, n_dims: int, objective: int, cost, params: dict) -> dict:
+    """Runs call(params, result) with result arrays sized for params."""
+    prm = {**SEARCH_DEFAULTS, **params}
+    sp = sd_search_params(prm["n_init"], prm["iterations"], prm["n_candidates"], prm["length_scale"], prm["noise"],
+                          prm["xi"], prm["seed"], objective, (ctypes.c_double * 5)(*(cost or (0.0,) * 5)))
+    n = max(prm["n_init"] + prm["iterations"], 1)
+    best = np.zeros(max(n_dims, 1), np.uint8)
+    masks = np.zeros((n, max(n_dims, 1)), np.uint8)
+    values = np.zeros(n)
+    margins = np.zeros(n)
+    u8p, dp = ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_double)
+    res = sd_search_result(best.ctypes.data_as(u8p), 0.0, 0, masks.ctypes.data_as(u8p), values.ctypes.data_as(dp),
+                           margins.ctypes.data_as(dp))
+    check(call(ctypes.byref(sp), ctypes.byref(res)))
+    k = res.n_evaluated
+    return {"best_mask": best[:n_dims], "best_value": res.best_value, "masks": masks[:k, :n_dims],
+            "values": values[:k], "margins": margins[:k]}
+
+
+def search_skip_set_fn(objective, n_dims: int, **params) -> dict:
+    """sd_search_skip_set_fn with a Python objective (a function of a uint8
+    mask returning a float); params override SEARCH_DEFAULTS.  An exception
+    in the objective stops the search and is raised again here."""
+    err = []
+
+    def trampoline(mask, n, user, value):
+        try:
+            value[0] = float(objective(np.ctypeslib.as_array(mask, (n,)).copy()))
+            return SD_OK
+        except Exception as e:  # noqa: BLE001 - carried across the C boundary
+            err.append(e)
+            return SD_ERR_INVALID_ARG
+
+    fn = SEARCH_OBJECTIVE_FN(trampoline)
+    try:
+        return _search_call(lambda sp, res: load().sd_search_skip_set_fn(n_dims, sp, fn, None, res), n_dims, 0, None,
+                            params)
+    except SDError:
+        if err:
+            raise err[0]
+        raise
 
 
 def _stats(st: sd_stats, log, glog=None) -> dict:

@@ -15,6 +15,8 @@
 #include <string>
 #include <vector>
 
+#include "host_api.h"
+
 #if defined(__x86_64__)
 #include <immintrin.h>
 #endif
@@ -1232,3 +1234,11 @@ const char *sd_last_error(void) { return g_err.c_str(); }
 const char *sd_version(void) { return "sd-mi355x 0.1 (gfx950)"; }
 
 }  // extern "C"
+
+namespace sdk {
+
+sd_status report(sd_status st, const std::string &msg) { return fail(st, msg); }
+
+int32_t model_layers(const sd_model *m) { return m ? m->cfg.n_layers : 0; }
+
+}  // namespace sdk

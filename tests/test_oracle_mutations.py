@@ -164,7 +164,7 @@ SEARCH_MUTATIONS = {
     "ei_sign": ("imp = best - mu - xi", "imp = mu - best - xi"),
     "ei_no_sigma": ("return imp * cdf + sigma * pdf", "return imp * cdf + pdf"),
     "kernel_not_scaled_by_L": ("np.exp(-hamming / (length_scale * A.shape[1]))", "np.exp(-hamming / length_scale)"),
-    "posterior_var_sign": ("var = 1.0 - np.sum(", "var = 1.0 + np.sum("),
+    "posterior_var_sign": ("var[i] = 1.0 - k @", "var[i] = 1.0 + k @"),
     "no_noise": ("+ noise * np.eye(len(X))", ""),
     "standardise_sample_sd": ("np.sqrt(np.mean((y - y.mean()) ** 2))",
                               "np.sqrt(np.sum((y - y.mean()) ** 2) / max(len(y) - 1, 1))"),
@@ -174,6 +174,7 @@ SEARCH_MUTATIONS = {
     "four_flips": ("flips = 1 + int(search_uniform(seed, t, P_NFLIP, c) * 3.0)",
                    "flips = 1 + int(search_uniform(seed, t, P_NFLIP, c) * 4.0)"),
     "density_range": ("p = 0.6 * search_uniform(seed, t, P_DENSITY, c)", "p = search_uniform(seed, t, P_DENSITY, c)"),
+    "init_not_empty": ("p = 0.6 * i / n_init", "p = 0.6 * (i + 1) / (n_init + 1)"),
     "no_dedupe": ("if not any(np.array_equal(z, x) for x in X)]", "]"),
     "draft_mlp_cost_on_attention": ("att = int(np.sum(mask[0::2] == 0))", "att = int(np.sum(mask[1::2] == 0))"),
 }

@@ -109,9 +109,9 @@ def check_candidates(mod=O):
     assert local_flips.max() <= 3 and np.all(np.isin(np.bincount(local_flips, minlength=4), np.arange(1, 10**6)))
     # random masks: density uniform on [0, 0.6) on average 0.3
     assert abs(np.mean(dens) - 0.3) < 0.02 and max(dens) < 0.75
-    # initial design: increasing densities 0.6 (i + 1) / (n + 1)
+    # initial design: densities 0.6 i / n, the first mask empty
     init = np.array([mod.initial_mask(3, i, 8, 400).mean() for i in range(8)])
-    assert np.all(np.abs(init - 0.6 * np.arange(1, 9) / 9) < 0.06)
+    assert init[0] == 0.0 and np.all(np.abs(init - 0.6 * np.arange(8) / 8) < 0.06)
 
 
 PLANTED24 = np.zeros(24, np.uint8)
