@@ -103,6 +103,12 @@ struct sd_model {
     int attn_splits_cap = 0;
     float2 *rope = nullptr;
     int rope_cap = 0;
+    // large-M forward (bfloat16 models): residual stream, GEMM output,
+    // rotated queries, and the GEMM inputs as X_TERMS terms, PF_ROWS rows each
+    bool pf_ok = false;
+    float *pf_h = nullptr, *pf_c = nullptr, *pf_q = nullptr, *pf_part = nullptr;
+    uint16_t *pf_x = nullptr;
+    int64_t pf_term = 0;
     DevCtl *ctl = nullptr;
     DevState *st = nullptr;
     Mailbox *mb_host = nullptr;
@@ -632,9 +638,88 @@ sd_status ensure_gen_cache(sd_model *m, int32_t cap) {
     return create_cache(m, cap, nullptr, &m->gen_cache);
 }
 
-// Prefill: full-model forward of tokens [0, n) already on the device,
-// in chunks of up to MAX_ROWS rows, no head.
+// Large-M forward (bfloat16 models): the M <= PF_ROWS tokens dev_tokens at
+// positions [start, start + M), matrix-core GEMMs over all rows at once;
+// logits (device [M][vocab]) when not null.
+sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, const int32_t *dev_tokens,
+                                int32_t M, int32_t start, float *logits) {
+    const sd_config &c = m->cfg;
+    const int H = c.n_heads, KVH = c.n_kv_heads, dh = c.head_dim, d = c.d_model, F = c.ffn_dim;
+    const int hd = H * dh, nq = (H + 2 * KVH) * dh;
+    const int64_t head_stride = (int64_t)cap * dh;
+    const int64_t xt = m->pf_term;
+    hipStream_t s = m->stream;
+    auto gemm = [&](const void *W, int N, int K, float *C, int64_t ldc, int epi) {
+        PfGemmArgs g{};
+        g.W = static_cast<const uint16_t *>(W);
+        g.A = m->pf_x;
+        g.a_term = xt;
+        g.C = C;
+        g.ldc = ldc;
+        g.M = M;
+        g.N = N;
+        g.K = K;
+        g.lda = K;
+        g.part = epi == EPI_RESID ? m->pf_part : nullptr;  // [PF_MAX_SPLITS][M][d]: split reductions
+        return launch(launch_pf_gemm(g, epi, s), "prefill GEMM");
+    };
+    auto norm = [&](const void *gain) {
+        return launch(launch_pf_norm_split(m->pf_h, d, M, static_cast<const uint16_t *>(gain), c.rms_eps, m->pf_x,
+                                           xt, s),
+                      "prefill norm");
+    };
+    SD_TRY(launch(launch_pf_embed(static_cast<const uint16_t *>(m->tok_emb), d, dev_tokens, M, m->pf_h, s),
+                  "prefill embedding"));
+    for (int l = 0; l < c.n_layers; ++l) {
+        if (!(skip && skip[2 * l])) {
+            uint16_t *kbase = reinterpret_cast<uint16_t *>(kv) + (size_t)(2 * l) * KVH * head_stride;
+            uint16_t *vbase = reinterpret_cast<uint16_t *>(kv) + (size_t)(2 * l + 1) * KVH * head_stride;
+            SD_TRY(norm(m->attn_norm[l]));
+            SD_TRY(gemm(m->w_qkv[l], nq, d, m->pf_c, nq, EPI_STORE));
+            SD_TRY(launch(launch_pf_rope_kv(m->pf_c, M, start, m->rope, H, KVH, dh, m->pf_q, kbase, vbase,
+                                            head_stride, s),
+                          "prefill rotary"));
+            PfAttnArgs at{};
+            at.q = m->pf_q;
+            at.ldq = hd;
+            at.kcache = kbase;
+            at.vcache = vbase;
+            at.kv_head_stride = head_stride;
+            at.out = m->pf_x;
+            at.out_term = xt;
+            at.ldo = hd;
+            at.M = M;
+            at.start = start;
+            at.n_heads = H;
+            at.n_kv_heads = KVH;
+            at.head_dim = dh;
+            SD_TRY(launch(launch_pf_attention(at, s), "prefill attention"));
+            SD_TRY(gemm(m->w_o[l], d, hd, m->pf_h, d, EPI_RESID));
+        }
+        if (!(skip && skip[2 * l + 1])) {
+            SD_TRY(norm(m->mlp_norm[l]));
+            SD_TRY(gemm(m->w_gate_up[l], 2 * F, d, m->pf_c, 2 * F, EPI_STORE));
+            SD_TRY(launch(launch_pf_swiglu_split(m->pf_c, F, M, m->pf_x, xt, s), "prefill SwiGLU"));
+            SD_TRY(gemm(m->w_down[l], d, F, m->pf_h, d, EPI_RESID));
+        }
+    }
+    if (logits) {
+        SD_TRY(norm(m->final_norm));
+        SD_TRY(gemm(m->lm_head, c.vocab, d, logits, c.vocab, EPI_STORE));
+    }
+    return SD_OK;
+}
+
+// Prefill: full-model forward of tokens [0, n) already on the device, no
+// head: PF_ROWS-row chunks on the large-M path (bfloat16 models, more than
+// MAX_ROWS tokens), else MAX_ROWS-row chunks.
 sd_status enqueue_prefill(sd_model *m, sd_kv_cache *kc, const int32_t *dev_tokens, int32_t n, int32_t start) {
+    if (m->pf_ok && n > MAX_ROWS) {
+        for (int32_t c = 0; c < n; c += PF_ROWS)
+            SD_TRY(enqueue_forward_large(m, kc->buf, kc->cap, nullptr, dev_tokens + c, std::min(PF_ROWS, n - c),
+                                         start + c, nullptr));
+        return SD_OK;
+    }
     for (int32_t c = 0; c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
         SD_TRY(launch(launch_set_ctl(m->ctl, start + c, rows, dev_tokens + c, m->stream), "control block"));
@@ -892,7 +977,10 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
                                          " more do not fit");
     SD_TRY(ensure_buf(m, &m->d_tokens, &m->d_tokens_cap, n));
     SD_HIP(hipMemcpyAsync(m->d_tokens, tokens, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice, m->stream));
-    for (int32_t c = 0; c < n; c += MAX_ROWS) {
+    for (int32_t c = 0; m->pf_ok && n > MAX_ROWS && c < n; c += PF_ROWS)
+        SD_TRY(enqueue_forward_large(m, kc->buf, kc->cap, skip, m->d_tokens + c, std::min(PF_ROWS, n - c),
+                                     kc->len + c, logits ? logits + (size_t)c * m->cfg.vocab : nullptr));
+    for (int32_t c = 0; !(m->pf_ok && n > MAX_ROWS) && c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
         SD_TRY(launch(launch_set_ctl(m->ctl, kc->len + c, rows, m->d_tokens + c, m->stream), "control block"));
         HeadSpec hs;
@@ -930,6 +1018,11 @@ void destroy_model(sd_model *m) {
     dev_free(m->attn_o);
     dev_free(m->attn_ml);
     dev_free(m->rope);
+    dev_free(m->pf_h);
+    dev_free(m->pf_c);
+    dev_free(m->pf_q);
+    dev_free(m->pf_part);
+    dev_free(m->pf_x);
     dev_free(m->ctl);
     dev_free(m->st);
     dev_free(m->d_tokens);
@@ -1011,6 +1104,17 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->sdstat, (size_t)MAX_ROWS));
     chain(dev_alloc(&m->ctl, 1));
     chain(dev_alloc(&m->st, 1));
+    m->pf_ok = m->bf16 && (c.head_dim == 32 || c.head_dim == 64 || c.head_dim == 128);
+    if (m->pf_ok) {
+        const int64_t hd = (int64_t)c.n_heads * c.head_dim;
+        const int64_t nc = std::max<int64_t>((int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim, 2 * c.ffn_dim);
+        m->pf_term = (int64_t)PF_ROWS * std::max<int64_t>({c.d_model, hd, c.ffn_dim});
+        chain(dev_alloc(&m->pf_h, (size_t)PF_ROWS * c.d_model));
+        chain(dev_alloc(&m->pf_c, (size_t)PF_ROWS * nc));
+        chain(dev_alloc(&m->pf_q, (size_t)PF_ROWS * hd));
+        chain(dev_alloc(&m->pf_part, (size_t)PF_MAX_SPLITS * PF_ROWS * c.d_model));
+        chain(dev_alloc(&m->pf_x, (size_t)X_TERMS * m->pf_term));
+    }
     if (st != SD_OK) {
         destroy_model(m);
         return st;

@@ -234,6 +234,52 @@ struct AttnArgs {
     const DevCtl *ctl;
 };
 
+// ---------------------------------------------------------------------------
+// Large-M forward (prompt prefill, long forwards): up to PF_ROWS rows at
+// positions [start, start + M), bfloat16 weights and KV.  Activations that
+// feed a matrix-core GEMM are held as X_TERMS bf16 terms, row-major:
+// [X_TERMS][PF_ROWS][ld] with the term stride PF_ROWS * ld.
+constexpr int PF_ROWS = 1024;
+constexpr int PF_MAX_SPLITS = 4;  // k-splits of a narrow residual-update GEMM
+
+// C[m][n] = (EPI_STORE) or += (EPI_RESID) sum over the terms t of
+// A_t[m][0..K) . W[n][0..K).
+struct PfGemmArgs {
+    const uint16_t *W;  // [N][K] bf16
+    const uint16_t *A;  // [X_TERMS][.][lda] bf16 terms, M rows used
+    int64_t a_term;     // elements between terms
+    float *C;           // [M][ldc]
+    int64_t ldc;
+    int32_t M, N, K, lda;
+    float *part;        // EPI_RESID: [PF_MAX_SPLITS][M][ldc] scratch for a split reduction, or null
+    int32_t splits;     // set by the launcher
+};
+
+// Causal attention of M query rows (row m at position start + m) over the
+// cached keys [0, start + m], output written as X_TERMS bf16 terms.
+struct PfAttnArgs {
+    const float *q;  // [M][ldq] rotated queries
+    int64_t ldq;
+    const uint16_t *kcache, *vcache;  // this layer: [n_kv_heads][cap][head_dim]
+    int64_t kv_head_stride;
+    uint16_t *out;  // [X_TERMS][.][ldo]
+    int64_t out_term, ldo;
+    int32_t M, start, n_heads, n_kv_heads, head_dim;
+};
+
+hipError_t launch_pf_embed(const uint16_t *emb, int d, const int32_t *tokens, int M, float *h, hipStream_t s);
+// g * h / rms(h) of every row (g: gain [K] bf16), as X_TERMS terms into out.
+hipError_t launch_pf_norm_split(const float *h, int K, int M, const uint16_t *gain, float eps, uint16_t *out,
+                                int64_t out_term, hipStream_t s);
+hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s);
+// Rotary embedding of q and k from the QKV GEMM output [M][(H + 2 KVH) dh];
+// q into q [M][H dh], k and v into the cache at positions start + m.
+hipError_t launch_pf_rope_kv(const float *qkv, int M, int start, const float2 *rope, int H, int KVH, int dh,
+                             float *q, uint16_t *kcache, uint16_t *vcache, int64_t kv_head_stride, hipStream_t s);
+hipError_t launch_pf_attention(const PfAttnArgs &a, hipStream_t s);
+// silu(gate) * up of the gate/up GEMM output [M][2 F], as X_TERMS terms.
+hipError_t launch_pf_swiglu_split(const float *gu, int F, int M, uint16_t *out, int64_t out_term, hipStream_t s);
+
 // Kernel paths of the linear layers.
 enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4 };
 
