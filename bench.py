@@ -100,6 +100,31 @@ def traffic_for(kernel: str):
     return e["bytes_per_launch"]
 
 
+def prefill_flops(cfg, M: int) -> float:
+    """Useful flops of the full-model forward of M rows from position 0:
+    every linear layer (2 M N K) and causal attention (scores and weighted
+    values, 2 head_dim flops per query-key pair each)."""
+    hd = cfg.n_heads * cfg.head_dim
+    nq = (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim
+    lin = nq * cfg.d_model + cfg.d_model * hd + 2 * cfg.ffn_dim * cfg.d_model + cfg.d_model * cfg.ffn_dim
+    attn = 2 * 2 * cfg.head_dim * cfg.n_heads * M * (M + 1) / 2
+    return cfg.n_layers * (2.0 * M * lin + attn)
+
+
+def prefill_roofline(cfg, M: int, ms: float):
+    """The prefill against the bf16 matrix-core peak.  Activations enter the
+    matrix cores as three bf16 terms, so the cores issue three times the
+    useful flops."""
+    if ms <= 0 or M < 1:
+        return None
+    fl = prefill_flops(cfg, M)
+    useful = fl / (ms / 1e3) / 1e12
+    return {"bound": "mfma", "rows": M, "ms": round(ms, 2), "useful_tflops": round(useful, 1),
+            "issued_tflops": round(3 * useful, 1), "peak_tflops": MFMA_BF16_PEAK_TFLOPS,
+            "frac_useful": round(useful / MFMA_BF16_PEAK_TFLOPS, 4),
+            "frac_issued": round(3 * useful / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+
 def cpu_baseline(cfg, weights, prompt, wl, skip, sample_prompt=16, sample_new=4):
     import oracle
 
@@ -208,6 +233,7 @@ def run_bench(args):
         "verify_step_GBps": round(b_verify / (verify_ms / 1e3) / 1e9, 1),
         "verify_step_frac_hbm": round(b_verify / (verify_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
         "prefill_ms": round(sum(s["prefill_ms"] for s in sd_stats) / args.steps, 2),
+        "prefill": prefill_roofline(cfg, wl.prompt_len - 1, sum(s["prefill_ms"] for s in sd_stats) / args.steps),
     }
     if ar_stats:
         ar_ms = sum(s["decode_ms"] for s in ar_stats)

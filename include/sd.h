@@ -109,7 +109,9 @@ typedef struct {
 /* Creates a model over borrowed device weights.  hip_stream is a
  * hipStream_t (NULL = the default stream).  Validates the shape and
  * allocates the library's device workspace (activations of up to 16 rows,
- * rotary table, reduction scratch).  Errors: INVALID_ARG, OOM, DEVICE. */
+ * rotary table, reduction scratch; for bfloat16 models with head_dim 32, 64
+ * or 128 also the large-forward workspace of 1024 rows, about 270 MB at the
+ * 13B shape).  Errors: INVALID_ARG, OOM, DEVICE. */
 sd_status sd_model_create(const sd_config *config, const sd_weights *weights, void *hip_stream, sd_model **out);
 /* Waits for the model's stream, then frees the model and its workspace.
  * KV caches created on it stay valid objects but are detached: they can
@@ -142,9 +144,11 @@ sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len);
  * skip_mask keeps and sets len += n.  skip_mask is a HOST uint8
  * [2 n_layers] (entry 2l: attention of layer l, 2l+1: its MLP; 1 = bypass,
  * i.e. the identity on the residual stream) or NULL for the full model.
- * logits, when not NULL, is a DEVICE float32 [n, vocab].  Rows run in
- * chunks of at most 16.  Errors: INVALID_ARG, CAPACITY (nothing enqueued),
- * DEVICE. */
+ * logits, when not NULL, is a DEVICE float32 [n, vocab].  More than 16
+ * rows on a model with the large-forward workspace run in chunks of up to
+ * 1024 rows on matrix-core GEMMs (the prompt prefill of the generate calls
+ * takes the same path); otherwise rows run in chunks of at most 16.
+ * Errors: INVALID_ARG, CAPACITY (nothing enqueued), DEVICE. */
 sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
                      sd_kv_cache *cache, float *logits);
 
