@@ -515,9 +515,9 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
     if (a.M < 1 || a.N < 1 || a.K < 8 || a.K % 8 || a.lda % 8 || a.M > PF_ROWS)
         return hipErrorInvalidValue;
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
-    // wide layers: 4 x 2 waves, one stage in flight; narrow ones (fewer
-    // tiles than CUs): 2 x 4 waves, two stages in flight, and the reduction
-    // split when a partial buffer is given (residual updates only)
+    // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
+    // flight; narrow ones: split residual updates (below), else 2 x 4 waves
+    // with two stages in flight
     if (tiles >= 256) {
         PfGemmArgs b = a;
         b.splits = 1;
@@ -530,17 +530,21 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
             return hipErrorInvalidValue;
         return hipGetLastError();
     }
-    // one work-group per CU at a time: a split pays only while every split
-    // of every tile still runs in the same round
+    // Residual updates split the reduction over as many work-groups as fit
+    // in one round: the 4 x 2-wave kernel runs two work-groups per CU, so up
+    // to 512 (13B output and down projections: 160 tiles, 3 splits; at
+    // least 16 stages per split).  Other narrow layers run unsplit.
     int splits = 1;
-    if (epi == EPI_RESID && a.part)
-        while (splits < PF_MAX_SPLITS && tiles * 2 * splits <= 256 && a.K >= 2 * splits * GB_K * 16)
-            splits *= 2;
+    if (epi == EPI_RESID && a.part) {
+        splits = std::min(PF_MAX_SPLITS, 512 / tiles);
+        while (splits > 1 && a.K < splits * GB_K * 16)
+            --splits;
+    }
     PfGemmArgs b = a;
     b.splits = splits;
     const dim3 grid(8 * ((tiles * b.splits + 7) / 8)), block(G_THREADS);
     if (splits > 1) {
-        hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 2, 4, 2>), grid, block, 0, s, b);
+        hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
         const int64_t n = (int64_t)a.M * a.ldc;
         hipLaunchKernelGGL(k_pf_split_sum, dim3((unsigned)std::min<int64_t>((n + 255) / 256, 4096)), dim3(256), 0, s,
                            a.part, splits, n, a.C, n);
