@@ -801,37 +801,59 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
         e = bf16 ? launch_attn_split<uint16_t>(a, max_q, s) : launch_attn_split<float>(a, max_q, s);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_attn_combine, dim3(a.n_heads, MAX_ROWS), dim3(128), 0, s, a);
+    // one work-group per (head, row) the forward can have
+    hipLaunchKernelGGL(k_attn_combine, dim3(a.n_heads, max_rows), dim3(128), 0, s, a);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // small kernels
 
+// Work-group (row r, slice b) copies elements [2048 b, 2048 b + 2048) of the
+// embedding row of token r, 8 per thread with one load each, so every load
+// of the row is in flight at once (d is a multiple of 8).
 template <typename TW>
 __global__ __launch_bounds__(256) void k_embed(const TW *E, int d, const DevCtl *ctl, float *h, int64_t ldh) {
     const int r = blockIdx.x;
     if (r >= ctl->m)
         return;
-    const int64_t tok = ctl->tokens[r];
-    for (int i = threadIdx.x; i < d; i += 256) {
-        float v;
-        if constexpr (sizeof(TW) == 2)
-            v = __uint_as_float(((uint32_t)E[tok * d + i]) << 16);
-        else
-            v = E[tok * d + i];
-        h[(int64_t)r * ldh + i] = v;
+    const int i = (blockIdx.y * 256 + threadIdx.x) * 8;
+    if (i >= d)
+        return;
+    const TW *src = E + (int64_t)ctl->tokens[r] * d + i;
+    float v[8];
+    if constexpr (sizeof(TW) == 2) {
+        const u32x4_t w = *reinterpret_cast<const u32x4_t *>(src);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = __uint_as_float(w[j] << 16);
+            v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+        }
+    } else {
+        const f32x4_t a = reinterpret_cast<const f32x4_t *>(src)[0];
+        const f32x4_t b = reinterpret_cast<const f32x4_t *>(src)[1];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[j] = a[j];
+            v[4 + j] = b[j];
+        }
     }
+    f32x4_t *dst = reinterpret_cast<f32x4_t *>(h + (int64_t)r * ldh + i);
+    dst[0] = f32x4_t{v[0], v[1], v[2], v[3]};
+    dst[1] = f32x4_t{v[4], v[5], v[6], v[7]};
 }
 
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s) {
+    if ((d & 7) || (ldh & 7))
+        return hipErrorInvalidValue;
+    const dim3 grid(MAX_ROWS, (d + 2047) / 2048);
     if (bf16)
-        hipLaunchKernelGGL(k_embed<uint16_t>, dim3(MAX_ROWS), dim3(256), 0, s,
-                           reinterpret_cast<const uint16_t *>(emb), d, ctl, h, ldh);
+        hipLaunchKernelGGL(k_embed<uint16_t>, grid, dim3(256), 0, s, reinterpret_cast<const uint16_t *>(emb), d, ctl,
+                           h, ldh);
     else
-        hipLaunchKernelGGL(k_embed<float>, dim3(MAX_ROWS), dim3(256), 0, s, reinterpret_cast<const float *>(emb),
-                           d, ctl, h, ldh);
+        hipLaunchKernelGGL(k_embed<float>, grid, dim3(256), 0, s, reinterpret_cast<const float *>(emb), d, ctl, h,
+                           ldh);
     return hipGetLastError();
 }
 

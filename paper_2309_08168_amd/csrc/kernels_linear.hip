@@ -161,11 +161,12 @@ __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, co
     }
 }
 
-// Last work-group of the head: combine the per-tile partials of every row
-// in a fixed order (deterministic), then take the decoding decision.
-// Thread j takes tiles j, j + 256, ... of every row (independent loads,
-// issued together), then the 256 partial results of a row are combined by
-// a fixed tree across lanes and waves.
+// One work-group after the head: combine the per-tile partials of every
+// row in a fixed order (deterministic), then take the decoding decision.
+// Thread j takes tiles j, j + 1024, ... of every row (independent loads,
+// issued together: one round trip for up to 4096 tiles), then the 1024
+// partial results of a row are combined by a fixed tree across lanes and
+// waves.
 __device__ HeadPart head_shfl(HeadPart v, int o) {
     HeadPart r;
     r.mx = __shfl_xor(v.mx, o, 64);
@@ -174,8 +175,11 @@ __device__ HeadPart head_shfl(HeadPart v, int o) {
     return r;
 }
 
+constexpr int HF_THREADS = 1024;
+
 __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
-    __shared__ HeadPart wred[4][MAX_ROWS];
+    constexpr int NWF = HF_THREADS / 64;
+    __shared__ HeadPart wred[NWF][MAX_ROWS];
     __shared__ int ys[MAX_ROWS];
     __shared__ float ps[MAX_ROWS];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -183,16 +187,16 @@ __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
     for (int m = 0; m < M; ++m) {
         HeadPart acc = head_empty();
         int t = tid;
-        for (; t + 768 < n_tiles; t += 1024) {
+        for (; t + 3 * HF_THREADS < n_tiles; t += 4 * HF_THREADS) {
             float4 v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-                v[u] = h.partials[(int64_t)(t + 256 * u) * MAX_ROWS + m];
+                v[u] = h.partials[(int64_t)(t + HF_THREADS * u) * MAX_ROWS + m];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 acc = head_comb(acc, HeadPart{v[u].x, __float_as_int(v[u].y), v[u].z});
         }
-        for (; t < n_tiles; t += 256) {
+        for (; t < n_tiles; t += HF_THREADS) {
             const float4 v = h.partials[(int64_t)t * MAX_ROWS + m];
             acc = head_comb(acc, HeadPart{v.x, __float_as_int(v.y), v.z});
         }
@@ -205,7 +209,7 @@ __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
     __syncthreads();
     if (tid < M) {
         HeadPart r = wred[0][tid];
-        for (int w = 1; w < 4; ++w)
+        for (int w = 1; w < NWF; ++w)
             r = head_comb(r, wred[w][tid]);
         ys[tid] = r.idx;
         ps[tid] = 1.0f / r.sum;
@@ -238,19 +242,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                 const float v = fin[i * MR + m] * inv[m];
                 float *o = e.out + (int64_t)m * e.ld_out + n;
                 if constexpr (EPI == EPI_RESID) {
-                    const float hn = *o + v;
-                    *o = hn;
-                    // this work-group owns element n of every row of the
-                    // residual stream: it also prepares g * h for the next
-                    // norm's MFMA consumer (which divides by rms(h) itself)
-                    if (e.out_x) {
-                        float gk;
-                        if constexpr (sizeof(TK) == 2)
-                            gk = bf2f(reinterpret_cast<const uint16_t *>(e.next_gain)[n]);
-                        else
-                            gk = reinterpret_cast<const float *>(e.next_gain)[n];
-                        store_split3(e.out_x, m, n, M, gk * hn);
-                    }
+                    *o += v;
                 } else {
                     *o = v;
                 }
@@ -335,20 +327,33 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
 
 // One work-group after the head: combine the partials of all tiles and take
 // the decoding decision.
-__global__ __launch_bounds__(256) void k_head_finalize(LinearArgs a) {
+__global__ __launch_bounds__(HF_THREADS) void k_head_finalize(LinearArgs a) {
     head_finalize(a, a.n_tiles, a.ctl->m);
 }
 
 // ---------------------------------------------------------------------------
-// VALU main loop: one work-group per tile of R weight rows; the 256
-// threads stride over the reduction dimension in chunks of 8 elements
-// (one 16-byte load of bf16 weights per row), then reduce across the
-// work-group.  MR is the largest row count handled (1: the GEMV).
+// VALU main loop: one work-group per tile of R weight rows; the NT threads
+// stride over the reduction dimension in chunks of 8 elements (one 16-byte
+// load of bf16 weights per row), then reduce across the work-group.  MR is
+// the largest row count handled (1: the GEMV).
+//
+// NT = 256: four waves share a tile and meet in LDS.  NT = 64: one wave
+// owns its tile over the whole reduction (bf16 weights, up to 4 rows), so
+// the reduction is a wave sum with no cross-wave step, and the loads of U
+// chunks are issued before the first is used.  Measured at the 13B shapes,
+// the one-wave tiles are the faster choice for every layer at two rows
+// (down 27.8 -> 25.6 us, O 13.0 -> 11.8 us); at one row the four-wave
+// tiles are as fast or faster.  Keeping the next chunk's loads in flight
+// while the current one is used (software pipelining) was slower at every
+// shape: the extra registers cost more occupancy than the overlap gained.
 
-template <typename TW, int MR, int R, int EPI, bool NORM>
-__global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
+template <typename TW, int MR, int R, int EPI, bool NORM, int NT = 256, int U = 1>
+__global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
+    static_assert(NT == 256 || NT == 64, "four-wave or one-wave tiles");
+    static_assert(NT == 256 || (sizeof(TW) == 2 && MR <= 4), "one-wave tiles take bf16 weights and up to 4 rows");
+    constexpr int NWAVE = NT / 64;
     constexpr int NV = MR * R + (NORM ? MR : 0);
-    __shared__ float red[4][NV];
+    __shared__ float red[NWAVE][NV];
     __shared__ float fin[R * MR];
     __shared__ float inv_s[MR];
     const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -378,6 +383,72 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
     // first is used: a branch around the X loads, or unpacking as loads
     // arrive, would make the compiler wait for each group of loads in turn.
     constexpr bool BATCH = MR > 1 && MR <= 4 && sizeof(TW) == 2;
+    if constexpr (NT == 64) {
+        auto issue = [&](int c, u32x4_t(&wr)[R], u32x4_t &gr, f32x4_t(&xr)[MR][2]) {
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                wr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(W + roff[i] + (int64_t)c * 8));
+            if constexpr (NORM)
+                gr = *reinterpret_cast<const u32x4_t *>(G + c * 8);
+            else
+                gr = u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int r = 0; r < MR; ++r) {
+                xr[r][0] = reinterpret_cast<const f32x4_t *>(a.X + (int64_t)r * a.ldx + c * 8)[0];
+                xr[r][1] = reinterpret_cast<const f32x4_t *>(a.X + (int64_t)r * a.ldx + c * 8)[1];
+            }
+        };
+        auto use = [&](const u32x4_t(&wr)[R], const u32x4_t &gr, const f32x4_t(&xr)[MR][2]) {
+            float g[8], w[R][8];
+            if constexpr (NORM)
+                unpack8(gr, g);
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                unpack8(wr[i], w[i]);
+#pragma unroll
+            for (int r = 0; r < MR; ++r) {
+                float x[8];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    x[k] = xr[r][0][k];
+                    x[4 + k] = xr[r][1][k];
+                }
+                if constexpr (NORM) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        ss[r] = fmaf(x[k], x[k], ss[r]);
+                        x[k] *= g[k];
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < R; ++i)
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        acc[r][i] = fmaf(w[i][k], x[k], acc[r][i]);
+            }
+        };
+        int c = tid;
+        for (; c + 64 * (U - 1) < nch; c += 64 * U) {
+            u32x4_t wr[U][R], gr[U];
+            f32x4_t xr[U][MR][2];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                issue(c + 64 * u, wr[u], gr[u], xr[u]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                use(wr[u], gr[u], xr[u]);
+        }
+        if constexpr (U > 1) {
+            for (; c < nch; c += 64) {
+                u32x4_t wr[R], gr;
+                f32x4_t xr[MR][2];
+                issue(c, wr, gr, xr);
+                __builtin_amdgcn_sched_barrier(0);
+                use(wr, gr, xr);
+            }
+        }
+    } else
     for (int c = tid; c < nch; c += 256) {
         float w[R][8];
         float g[8];
@@ -459,19 +530,22 @@ __global__ __launch_bounds__(256) void k_linear_valu(LinearArgs a) {
         }
     }
     __syncthreads();
-    for (int j = tid; j < MR * R; j += 256) {
+    auto waves_sum = [&](int j) {
+        if constexpr (NWAVE == 1)
+            return red[0][j];
+        else
+            return (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+    };
+    for (int j = tid; j < MR * R; j += NT) {
         const int r = j / R, i = j - r * R;
         if (r < M)
-            fin[i * MR + r] = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+            fin[i * MR + r] = waves_sum(j);
     }
     if (tid < MR) {
         float v = 1.0f;
         if constexpr (NORM) {
-            if (tid < M) {
-                const int j = MR * R + tid;
-                const float s = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
-                v = 1.0f / sqrtf(s / (float)K + a.eps);
-            }
+            if (tid < M)
+                v = 1.0f / sqrtf(waves_sum(MR * R + tid) / (float)K + a.eps);
         }
         inv_s[tid] = v;
     }
@@ -558,24 +632,6 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     int q = ks0 + wave;
     if (q < ks1)
         load(q);
-    // RMSNorm folded into the outputs: the fragments hold g * h, and
-    // 1/rms(h) of every row comes from h itself (L2-resident, read while the
-    // first weights are in flight), summed in a fixed order
-    __shared__ float ssw[NW][MAX_ROWS];
-    if (a.gain) {
-        const int K4 = a.K >> 2;
-        for (int m = 0; m < M; ++m) {
-            const float4 *hr = reinterpret_cast<const float4 *>(a.X + (int64_t)m * a.ldx);
-            float ss = 0.0f;
-            for (int k = tid; k < K4; k += NW * 64) {
-                const float4 v = hr[k];
-                ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
-            }
-            ss = wave_sum(ss);
-            if (lane == 0)
-                ssw[wave][m] = ss;
-        }
-    }
     for (; q < ks1; q += NW) {
         // this k-step's weights into the staging tile; its activations stay
         // in registers while the next k-step's loads go out
@@ -641,17 +697,8 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         }
         fin[o] = v;
     }
-    if (tid < 16) {
-        float v = 1.0f;
-        if (a.gain && tid < M) {
-            float ss = 0.0f;
-#pragma unroll
-            for (int w = 0; w < NW; ++w)
-                ss += ssw[w][tid];
-            v = 1.0f / sqrtf(ss / (float)a.K + a.eps);
-        }
-        inv_s[tid] = v;
-    }
+    if (tid < 16)
+        inv_s[tid] = 1.0f;  // the activations arrive normalised
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -662,15 +709,14 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Activations for the MFMA path: u = g * h / rms(h), u = g * h (when the
-// consumer divides by rms(h) itself) or u = h without a gain, split into
-// X_TERMS bf16 terms in fragment layout, after folding pending split-K
-// partials into h.  One work-group per row.
+// Activations for the MFMA path: u = g * h / rms(h), or u = h without a
+// gain, split into X_TERMS bf16 terms in fragment layout, after folding
+// pending split-K partials into h.  One work-group per row.
 
 template <typename TW>
 __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
                                                     const DevCtl *ctl, uint16_t *xs, const float *part,
-                                                    int n_part, bool normalize) {
+                                                    int n_part) {
     __shared__ float red[16];
     const int r = blockIdx.x, M = ctl->m;
     if (r >= M)
@@ -702,7 +748,7 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
         ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
     }
     float inv = 1.0f;
-    if (g && normalize) {
+    if (g) {
         ss = wave_sum(ss);
         if ((tid & 63) == 0)
             red[tid >> 6] = ss;
@@ -745,43 +791,43 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
 }
 
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
-                            uint16_t *xs, const float *part, int n_part, bool normalize, hipStream_t s) {
+                            uint16_t *xs, const float *part, int n_part, hipStream_t s) {
     if ((K & 127) || (ldh & 3) || n_part > 8)
         return hipErrorInvalidValue;
     if (bf16)
         hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part, normalize);
+                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part);
     else
         hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part, normalize);
+                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // dispatch
 
-template <typename TW, int MR, int R>
+template <typename TW, int MR, int R, int NT = 256, int U = 1>
 static hipError_t launch_valu(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
-    dim3 grid(n_tiles), block(256);
+    dim3 grid(n_tiles), block(NT);
     const bool norm = a.gain != nullptr;
     switch (epi) {
     case EPI_STORE:
         if (norm)
-            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, true>), grid, block, 0, s, a);
+            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, true, NT, U>), grid, block, 0, s, a);
         else
-            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, false>), grid, block, 0, s, a);
+            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, false, NT, U>), grid, block, 0, s, a);
         break;
     case EPI_RESID:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_RESID, false>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_RESID, false, NT, U>), grid, block, 0, s, a);
         break;
     case EPI_SWIGLU:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_SWIGLU, true>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_SWIGLU, true, NT, U>), grid, block, 0, s, a);
         break;
     case EPI_QKV:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_QKV, true>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_QKV, true, NT, U>), grid, block, 0, s, a);
         break;
     case EPI_HEAD:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_HEAD, true>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_HEAD, true, NT, U>), grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;
@@ -800,6 +846,19 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
         if constexpr (MR <= 4)
             return launch_valu<TW, MR, 16>(a, epi, n_tiles, s);
         return hipErrorInvalidValue;
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+// Two rows on one-wave tiles (bf16 weights): loads of two chunks in flight
+// for 4 weight rows, one chunk for 8 (a sweep at the 13B shapes).
+static hipError_t launch_valu_wave2(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s) {
+    switch (R) {
+    case 4:
+        return launch_valu<uint16_t, 2, 4, 64, 2>(a, epi, n_tiles, s);
+    case 8:
+        return launch_valu<uint16_t, 2, 8, 64, 1>(a, epi, n_tiles, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -867,7 +926,7 @@ static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipS
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s) {
     LinearArgs b = a;
     b.n_tiles = n_tiles;
-    hipLaunchKernelGGL(k_head_finalize, dim3(1), dim3(256), 0, s, b);
+    hipLaunchKernelGGL(k_head_finalize, dim3(1), dim3(HF_THREADS), 0, s, b);
     return hipGetLastError();
 }
 
@@ -899,6 +958,8 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
     if (path == PATH_VALU2)
         return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s)
                     : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s);
+    if (path == PATH_WAVE2)
+        return bf16 ? launch_valu_wave2(a, epi, rows_per_tile, n_tiles, s) : hipErrorInvalidValue;
     return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s)
                 : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s);
 }

@@ -54,13 +54,12 @@ enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4
 struct Plan {
     int kind;     // LinearKind
     int regime;   // 1, 2 or 16: the row counts the plan serves
-    int path;     // PATH_GEMV, PATH_VALU2, PATH_VALU16 or PATH_MFMA
+    int path;     // LinearPath
     int rows;     // weight rows per work-group
     int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
     int waves;    // MFMA: waves per work-group splitting the reduction
     int splits;   // MFMA output projections: split-K partials folded by the next norm
     int N, K, epi;
-    bool fused_norm;  // MFMA with RMSNorm folded: fragments hold g * h, 1/rms from h
 };
 
 }  // namespace
@@ -188,16 +187,25 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
         p.epi = EPI_HEAD;
         break;
     }
-    // Two rows (one-draft verification): QKV and the lm-head run on MFMA with
-    // the norm folded in, fed by the VALU output projections, which prepare
-    // g * h for them (no norm kernel); the output projections and gate/up
-    // stay VALU (gate/up with 8 weight rows per work-group, 50.8 against
-    // 53.4 us on MFMA at the 13B shape).
-    const bool fused2 = rows == 2 && (kind == LK_QKV || kind == LK_HEAD) && mfma_ok(m, LK_QKV) &&
-                        mfma_ok(m, LK_GATE_UP) && mfma_ok(m, LK_HEAD);
-    if ((rows > 2 || fused2) && mfma_ok(m, kind)) {
+    // Two rows (one-draft verification) of a bf16 model: every layer on
+    // one-wave VALU tiles, 8 weight rows for the wide layers and 4 for the
+    // output projections.  Measured at the 13B shape against the earlier
+    // plan (MFMA for QKV and the lm-head, four-wave tiles otherwise): QKV
+    // 30.2 against 31.6 us, gate/up 49.0 against 50.0, O 11.8 against 13.0,
+    // down 25.6 against 27.8, lm-head 54.6 against 58.6.
+    if (rows == 2 && m->bf16) {
+        p.path = PATH_WAVE2;
+        p.rows = kind == LK_QKV ? qkv_gemv_rows(c.head_dim, 8) : ((kind == LK_O || kind == LK_DOWN) ? 4 : 8);
+        if (kind == LK_QKV)
+            p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
+        else if (kind == LK_GATE_UP)
+            p.n_tiles = cdiv(c.ffn_dim, p.rows / 2);
+        else
+            p.n_tiles = cdiv(p.N, p.rows);
+        return p;
+    }
+    if (rows > 2 && mfma_ok(m, kind)) {
         p.path = PATH_MFMA;
-        p.fused_norm = fused2;
         if (kind == LK_QKV)
             p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / 8);
         else if (kind == LK_GATE_UP)
@@ -338,11 +346,6 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
     if (p.path == PATH_MFMA) {
         a.Xs = xs;
         a.max_rows = max_rows;
-        if (p.fused_norm) {  // 1/rms(h) from h itself
-            a.X = X;
-            a.ldx = ldx;
-            a.gain = gain;
-        }
     } else {
         a.X = X;
         a.ldx = ldx;
@@ -391,16 +394,12 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
 }
 
 // The MFMA operand of a normed layer into xa (MFMA path only), after folding
-// the pending split-K partials of the last output projection: g * h / rms(h),
-// or g * h for a fused-norm consumer.  Skipped when the last output
-// projection already wrote g * h for this consumer (fresh).
-sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending, bool &fresh) {
-    const bool skip = fresh && p.fused_norm && pending == 0;
-    fresh = false;
-    if (p.path != PATH_MFMA || skip)
+// the pending split-K partials of the last output projection: g * h / rms(h).
+sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
+    if (p.path != PATH_MFMA)
         return SD_OK;
     SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa, m->part,
-                                   pending, !p.fused_norm, m->stream),
+                                   pending, m->stream),
                   "norm"));
     pending = 0;
     return SD_OK;
@@ -420,34 +419,10 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
                           const HeadSpec &hs) {
     const sd_config &c = m->cfg;
     const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
-    int pending = 0;     // split-K partials not yet folded into h
-    bool fresh = false;  // xa holds g * h for the next normed (fused-norm MFMA) layer
+    int pending = 0;  // split-K partials not yet folded into h
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
-    // An output projection that updates the residual stream on the VALU path
-    // also writes g * h for the next normed layer when that layer is a
-    // fused-norm MFMA consumer (g: that layer's norm gain).
-    auto fuse_out = [&](EpiArgs &eo, const Plan &po, int sub) {
-        const Plan *np = nullptr;
-        const void *g = nullptr;
-        for (int s2 = sub + 1; s2 < 2 * c.n_layers && !np; ++s2) {
-            if (skip && skip[s2])
-                continue;
-            np = (s2 & 1) ? &P[LK_GATE_UP] : &P[LK_QKV];
-            g = (s2 & 1) ? m->mlp_norm[s2 >> 1] : m->attn_norm[s2 >> 1];
-        }
-        if (!np && hs.run) {
-            np = &P[LK_HEAD];
-            g = m->final_norm;
-        }
-        if (po.path != PATH_MFMA && po.epi == EPI_RESID && np && np->fused_norm) {
-            eo.out_x = m->xa;
-            eo.next_gain = g;
-            return true;
-        }
-        return false;
-    };
     SD_TRY(launch(launch_embed(m->tok_emb, m->bf16, c.d_model, m->ctl, m->h, ldh, m->stream), "embedding"));
     for (int l = 0; l < c.n_layers; ++l) {
         if (!(skip && skip[2 * l])) {
@@ -464,7 +439,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             e.n_kv_heads = c.n_kv_heads;
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
-            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l], pending, fresh));
+            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l], pending));
             SD_TRY(run_linear(m, P[LK_QKV], max_rows, m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa));
             AttnArgs at{};
             at.q = m->q;
@@ -489,9 +464,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             EpiArgs eo{};
             eo.out = m->h;
             eo.ld_out = ldh;
-            const bool fo = fuse_out(eo, P[LK_O], 2 * l);
             SD_TRY(run_linear(m, P[LK_O], max_rows, m->w_o[l], m->o, ldq, nullptr, eo, m->xa));
-            fresh = fo;
             if (P[LK_O].epi == EPI_PARTIAL)
                 pending = P[LK_O].splits;
         }
@@ -504,14 +477,12 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
                 eg.out_x = m->xb;
                 eg.ld_out = m->xld;
             }
-            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l], pending, fresh));
+            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l], pending));
             SD_TRY(run_linear(m, P[LK_GATE_UP], max_rows, m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa));
             EpiArgs ed{};
             ed.out = m->h;
             ed.ld_out = ldh;
-            const bool fd = fuse_out(ed, P[LK_DOWN], 2 * l + 1);
             SD_TRY(run_linear(m, P[LK_DOWN], max_rows, m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb));
-            fresh = fd;
             if (P[LK_DOWN].epi == EPI_PARTIAL)
                 pending = P[LK_DOWN].splits;
         }
@@ -533,7 +504,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             eh.head.logits = hs.mode == HEAD_DRAFT ? m->slog_d : m->slog_v;
             eh.head.logits_by_draft = hs.mode == HEAD_DRAFT;
         }
-        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending, fresh));
+        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending));
         SD_TRY(run_linear(m, P[LK_HEAD], max_rows, m->lm_head, m->h, ldh, m->final_norm, eh, m->xa));
     }
     return SD_OK;
@@ -1165,9 +1136,14 @@ std::string kernel_symbol(const sd_model *m, const Plan &p) {
             nm += " (mixed packings)";
         return nm;
     }
-    const int mr = p.path == PATH_GEMV ? 1 : (p.path == PATH_VALU2 ? 2 : (p.path == PATH_VALU4 ? 4 : 16));
+    const int mr = p.path == PATH_GEMV
+                       ? 1
+                       : ((p.path == PATH_VALU2 || p.path == PATH_WAVE2) ? 2 : (p.path == PATH_VALU4 ? 4 : 16));
+    const bool wave = p.path == PATH_WAVE2;
+    const int nt = wave ? 64 : 256, u = wave && p.rows == 4 ? 2 : 1;
     return std::string("void sdk::k_linear_valu<") + tw + ", " + std::to_string(mr) + ", " + std::to_string(p.rows) +
-           ", " + std::to_string(p.epi) + ", " + (norm ? "true" : "false") + ">(sdk::LinearArgs)";
+           ", " + std::to_string(p.epi) + ", " + (norm ? "true" : "false") + ", " + std::to_string(nt) + ", " +
+           std::to_string(u) + ">(sdk::LinearArgs)";
 }
 
 const Plan *find_plan(const sd_model *m, int kind, int regime) {

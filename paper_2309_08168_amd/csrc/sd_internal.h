@@ -190,9 +190,7 @@ struct SampleArgs {
 struct EpiArgs {
     float *out;            // STORE/RESID: [m][ld_out]; SWIGLU: [m][ffn]
     int64_t ld_out;
-    uint16_t *out_x;       // SWIGLU: when set, the output split into bf16 terms in fragment layout (xfrag_off);
-                           // RESID: when set, also next_gain * (updated h) for the next norm's MFMA consumer
-    const void *next_gain; // RESID with out_x: gain of the next RMSNorm (weight dtype)
+    uint16_t *out_x;       // SWIGLU: when set, the output split into bf16 terms in fragment layout (xfrag_off)
     float *q;              // QKV: rotated queries [m][n_heads * head_dim]
     int64_t ld_q;
     void *kcache, *vcache; // QKV: this layer's K and V: [n_kv_heads][cap][head_dim]
@@ -209,8 +207,7 @@ struct LinearArgs {
     const uint16_t *Xs;    // MFMA path: activations split into bf16 terms in fragment layout (xfrag_off)
     int32_t max_rows;      // MFMA path: host bound on ctl->m, sets the MFMAs per k-step
     int64_t ldx;
-    const void *gain;      // RMSNorm gain [K] (weight dtype), or null: no norm.  MFMA path: the
-                           // fragments then hold gain * h and 1/rms(h) is taken from X = h
+    const void *gain;      // VALU paths: RMSNorm gain [K] (weight dtype), or null: no norm
     float eps;
     const DevCtl *ctl;
     EpiArgs epi;
@@ -281,16 +278,17 @@ hipError_t launch_pf_attention(const PfAttnArgs &a, hipStream_t s);
 hipError_t launch_pf_swiglu_split(const float *gu, int F, int M, uint16_t *out, int64_t out_term, hipStream_t s);
 
 // Kernel paths of the linear layers.
-enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4 };
+// PATH_WAVE2: up to two rows on one-wave tiles (bf16 weights).
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4, PATH_WAVE2 = 5 };
 
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s);
-// g * h / rms(h) (normalize), g * h (!normalize) or plain h (gain == null), split
-// into X_TERMS bf16 terms in fragment layout for the MFMA path (K a multiple of 128).  First adds n_part pending split-K partials ([n_part][MAX_ROWS][K]) into h.
+// g * h / rms(h), or plain h (gain == null), split into X_TERMS bf16 terms in
+// fragment layout for the MFMA path (K a multiple of 128).  First adds n_part
+// pending split-K partials ([n_part][MAX_ROWS][K]) into h.
 hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xs, const float *part, int n_part, bool normalize,
-                            hipStream_t s);
+                            const DevCtl *ctl, uint16_t *xs, const float *part, int n_part, hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
 // Sampling variant, after a head linear that wrote the logits: the nucleus
