@@ -653,8 +653,12 @@ __global__ __launch_bounds__(NWV * 64) void k_attn_head(AttnArgs a) {
 }
 
 // Ordered combine of the split partials of one (head, row): deterministic.
-// The running maxima and sums of all splits are loaded in parallel first.
+// Thread e owns output element e.  The running maxima and sums of the first
+// 128 splits and the partial outputs of the first CB splits are all loaded
+// before any of them is used, so a context of up to CB * ATTN_CHUNK keys
+// costs one round trip to memory.
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
+    constexpr int CB = 16;
     __shared__ float w_s[MAX_SPLITS];
     __shared__ float2 ml_s[MAX_SPLITS];
     __shared__ float red[2];
@@ -664,9 +668,23 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
         return;
     const int ns = (pos + M + ATTN_CHUNK - 1) / ATTN_CHUNK;
     const int dh = a.head_dim, H = a.n_heads, tid = threadIdx.x;
+    auto o_at = [&](int sp, int e) { return a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e]; };
+    auto ml_at = [&](int sp) { return a.part_ml[((int64_t)sp * H + head) * MAX_ROWS + r]; };
+    // every load below reads a split inside [0, ns) and an element inside
+    // [0, dh); the values past ns or dh are discarded
+    const int e = tid < dh ? tid : 0;
+    float ov[CB];
+#pragma unroll
+    for (int u = 0; u < CB; ++u)
+        ov[u] = o_at(min(u, ns - 1), e);
+    const float2 ml0 = ml_at(min(tid, ns - 1));
     float mx = -INFINITY;
-    for (int sp = tid; sp < ns; sp += 128) {
-        const float2 v = a.part_ml[((int64_t)sp * H + head) * MAX_ROWS + r];
+    if (tid < ns) {
+        ml_s[tid] = ml0;
+        mx = ml0.x;
+    }
+    for (int sp = tid + 128; sp < ns; sp += 128) {
+        const float2 v = ml_at(sp);
         ml_s[sp] = v;
         mx = fmaxf(mx, v.x);
     }
@@ -680,30 +698,34 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
         w_s[sp] = v.x == -INFINITY ? 0.0f : expf(v.x - mx);
     }
     __syncthreads();
+    if (tid >= dh)
+        return;
     float L = 0.0f;
     for (int sp = 0; sp < ns; ++sp)
         L = fmaf(w_s[sp], ml_s[sp].y, L);
-    for (int e = tid; e < dh; e += 128) {
-        float O = 0.0f;
-        int sp = 0;
-        for (; sp + 8 <= ns; sp += 8) {
-            float ov[8];
+    // the splits in order: the preloaded ones, then the rest 8 at a time
+    float O = 0.0f;
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                ov[u] = a.part_o[(((int64_t)(sp + u) * H + head) * MAX_ROWS + r) * dh + e];
+    for (int u = 0; u < CB; ++u)
+        if (u < ns)
+            O = fmaf(w_s[u], ov[u], O);
+    int sp = CB;
+    for (; sp + 8 <= ns; sp += 8) {
+        float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                O = fmaf(w_s[sp + u], ov[u], O);
-        }
-        for (; sp < ns; ++sp)
-            O = fmaf(w_s[sp], a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e], O);
-        const float y = O / L;
-        const int64_t oi = (int64_t)r * a.ld_out + (int64_t)head * dh + e;
-        if (a.out_x) {
-            store_split3(a.out_x, r, head * dh + e, M, y);
-        } else {
-            a.out[oi] = y;
-        }
+        for (int u = 0; u < 8; ++u)
+            v[u] = o_at(sp + u, tid);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            O = fmaf(w_s[sp + u], v[u], O);
+    }
+    for (; sp < ns; ++sp)
+        O = fmaf(w_s[sp], o_at(sp, tid), O);
+    const float y = O / L;
+    if (a.out_x) {
+        store_split3(a.out_x, r, head * dh + tid, M, y);
+    } else {
+        a.out[(int64_t)r * a.ld_out + (int64_t)head * dh + tid] = y;
     }
 }
 

@@ -163,10 +163,10 @@ __device__ void decode_decision(const HeadArgs &h, DevCtl *ctl, const int *y, co
 
 // One work-group after the head: combine the per-tile partials of every
 // row in a fixed order (deterministic), then take the decoding decision.
-// Thread j takes tiles j, j + 1024, ... of every row (independent loads,
-// issued together: one round trip for up to 4096 tiles), then the 1024
-// partial results of a row are combined by a fixed tree across lanes and
-// waves.
+// Thread j takes tiles j, j + 256, ... of every row; the loads of up to
+// HF_BATCH tiles per thread are issued together (one round trip for up to
+// 4096 tiles), then the 256 partial results of a row are combined by a
+// fixed tree across lanes and waves.
 __device__ HeadPart head_shfl(HeadPart v, int o) {
     HeadPart r;
     r.mx = __shfl_xor(v.mx, o, 64);
@@ -175,7 +175,8 @@ __device__ HeadPart head_shfl(HeadPart v, int o) {
     return r;
 }
 
-constexpr int HF_THREADS = 1024;
+constexpr int HF_THREADS = 256;
+constexpr int HF_BATCH = 16;
 
 __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
     constexpr int NWF = HF_THREADS / 64;
@@ -186,19 +187,16 @@ __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
     const HeadArgs &h = a.epi.head;
     for (int m = 0; m < M; ++m) {
         HeadPart acc = head_empty();
-        int t = tid;
-        for (; t + 3 * HF_THREADS < n_tiles; t += 4 * HF_THREADS) {
-            float4 v[4];
+        for (int t0 = 0; t0 < n_tiles; t0 += HF_THREADS * HF_BATCH) {
+            // tiles past n_tiles read the last one and are skipped
+            float4 v[HF_BATCH];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                v[u] = h.partials[(int64_t)(t + HF_THREADS * u) * MAX_ROWS + m];
+            for (int u = 0; u < HF_BATCH; ++u)
+                v[u] = h.partials[(int64_t)min(t0 + tid + HF_THREADS * u, n_tiles - 1) * MAX_ROWS + m];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                acc = head_comb(acc, HeadPart{v[u].x, __float_as_int(v[u].y), v[u].z});
-        }
-        for (; t < n_tiles; t += HF_THREADS) {
-            const float4 v = h.partials[(int64_t)t * MAX_ROWS + m];
-            acc = head_comb(acc, HeadPart{v.x, __float_as_int(v.y), v.z});
+            for (int u = 0; u < HF_BATCH; ++u)
+                if (t0 + tid + HF_THREADS * u < n_tiles)
+                    acc = head_comb(acc, HeadPart{v[u].x, __float_as_int(v[u].y), v[u].z});
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1)

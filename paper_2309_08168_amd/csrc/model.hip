@@ -51,6 +51,10 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4, LK_COUNT = 5 };
 
 // How one linear layer is launched for one row regime.
+// Forwards of the timed regime per forward whose launches the measurement
+// hook brackets with events.
+constexpr int64_t TIMED_SAMPLE = 16;
+
 struct Plan {
     int kind;     // LinearKind
     int regime;   // 1, 2 or 16: the row counts the plan serves
@@ -125,6 +129,8 @@ struct sd_model {
     hipEvent_t ev[6] = {};
     // measurement hook (sd_model_time_kernel)
     int timed_kind = -1, timed_regime = 0;
+    int64_t timed_forwards = 0;  // forwards of the timed regime since the hook was set
+    bool timed_now = false;      // this forward's launches of the timed class are bracketed
     int timed_rows_lo = 0, timed_rows_hi = 0;  // row bounds seen by the timed launches
     std::vector<hipEvent_t> tev;  // pairs
     size_t tev_used = 0;
@@ -358,7 +364,8 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
     a.splits = p.splits;
     a.part = m->part;
     a.n_tiles = p.n_tiles;
-    const bool timed = p.kind == m->timed_kind && p.regime == m->timed_regime && m->tev_used + 2 <= 2 * 65536;
+    const bool timed = m->timed_now && p.kind == m->timed_kind && p.regime == m->timed_regime &&
+                       m->tev_used + 2 <= 2 * 65536;
     if (timed) {
         if (m->tev_used + 2 > m->tev.size()) {
             for (int i = 0; i < 256; ++i) {
@@ -419,6 +426,12 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
                           const HeadSpec &hs) {
     const sd_config &c = m->cfg;
     const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
+    // The measurement hook brackets the timed class in one of every
+    // TIMED_SAMPLE forwards of its regime: an event pair costs about 5 us of
+    // stream time on each side of the launch, which would otherwise inflate
+    // the step it measures.
+    m->timed_now = P[0].regime == m->timed_regime && m->timed_kind >= 0 &&
+                   (m->timed_forwards++ % TIMED_SAMPLE) == 0;
     int pending = 0;  // split-K partials not yet folded into h
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
@@ -1289,6 +1302,7 @@ sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows) {
              if (layer != -1 && !find_plan(model, layer, rows))
                  return fail(SD_ERR_INVALID_ARG, "layer must be -1 or 0..4 and rows 1, 2 or 16");
              model->timed_kind = layer; model->timed_regime = rows; model->tev_used = 0;
+             model->timed_forwards = 0; model->timed_now = false;
              model->timed_rows_lo = 0; model->timed_rows_hi = 0;
              model->timed_launches = 0; model->timed_ms = 0.0; return SD_OK;)
 }

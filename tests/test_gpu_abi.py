@@ -82,3 +82,20 @@ def test_cache_outlives_model():
     assert c.length == 2
     c.close()  # after its model: must not touch the freed model
     m2.close()
+
+
+def test_kernel_timing_hook_samples_forwards(dm):
+    """The measurement hook brackets the chosen class in one of every 16
+    forwards of its regime: 32 autoregressive steps of the 4-layer model time
+    the gate/up launches of steps 0 and 16 only, and timing changes no token."""
+    cfg = dm.cfg
+    prompt = S.prompt(cfg, 8)
+    ref, _ = dm.generate_ar(prompt, 32)
+    dm.time_kernel("gate_up", 1)
+    out, _ = dm.generate_ar(prompt, 32)
+    kt = dm.kernel_time()
+    dm.time_kernel(None)
+    assert np.array_equal(out, ref)
+    assert kt["launches"] == 2 * cfg.n_layers
+    assert kt["total_ms"] > 0.0
+    assert kt["n"] == 2 * cfg.ffn_dim and kt["k"] == cfg.d_model
