@@ -16,6 +16,8 @@
 // RMSNorm is folded in: y = W (g * h) / rms(h), so the kernel that reads h
 // as its input also accumulates sum(h^2) and scales its outputs at the end;
 // no separate normalisation pass.
+#include <hip/hip_ext.h>
+
 #include "sd_internal.h"
 #include "decode_step.h"
 
@@ -804,28 +806,39 @@ hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, 
 // ---------------------------------------------------------------------------
 // dispatch
 
+// A launch, with the optional start/stop events attached to the dispatch
+// itself: they take the kernel's own start and end times and add no packets
+// to the stream.
+static void launch_k(void (*kern)(LinearArgs), dim3 grid, dim3 block, hipStream_t s, const LaunchTiming &t,
+                     const LinearArgs &a) {
+    if (t.start)
+        hipExtLaunchKernelGGL(kern, grid, block, 0, s, t.start, t.stop, 0, a);
+    else
+        hipLaunchKernelGGL(kern, grid, block, 0, s, a);
+}
+
 template <typename TW, int MR, int R, int NT = 256, int U = 1>
-static hipError_t launch_valu(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
+static hipError_t launch_valu(const LinearArgs &a, int epi, int n_tiles, hipStream_t s, const LaunchTiming &t) {
     dim3 grid(n_tiles), block(NT);
     const bool norm = a.gain != nullptr;
     switch (epi) {
     case EPI_STORE:
         if (norm)
-            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, true, NT, U>), grid, block, 0, s, a);
+            launch_k(k_linear_valu<TW, MR, R, EPI_STORE, true, NT, U>, grid, block, s, t, a);
         else
-            hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_STORE, false, NT, U>), grid, block, 0, s, a);
+            launch_k(k_linear_valu<TW, MR, R, EPI_STORE, false, NT, U>, grid, block, s, t, a);
         break;
     case EPI_RESID:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_RESID, false, NT, U>), grid, block, 0, s, a);
+        launch_k(k_linear_valu<TW, MR, R, EPI_RESID, false, NT, U>, grid, block, s, t, a);
         break;
     case EPI_SWIGLU:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_SWIGLU, true, NT, U>), grid, block, 0, s, a);
+        launch_k(k_linear_valu<TW, MR, R, EPI_SWIGLU, true, NT, U>, grid, block, s, t, a);
         break;
     case EPI_QKV:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_QKV, true, NT, U>), grid, block, 0, s, a);
+        launch_k(k_linear_valu<TW, MR, R, EPI_QKV, true, NT, U>, grid, block, s, t, a);
         break;
     case EPI_HEAD:
-        hipLaunchKernelGGL((k_linear_valu<TW, MR, R, EPI_HEAD, true, NT, U>), grid, block, 0, s, a);
+        launch_k(k_linear_valu<TW, MR, R, EPI_HEAD, true, NT, U>, grid, block, s, t, a);
         break;
     default:
         return hipErrorInvalidValue;
@@ -834,15 +847,16 @@ static hipError_t launch_valu(const LinearArgs &a, int epi, int n_tiles, hipStre
 }
 
 template <typename TW, int MR>
-static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s) {
+static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s,
+                                const LaunchTiming &t) {
     switch (R) {
     case 4:
-        return launch_valu<TW, MR, 4>(a, epi, n_tiles, s);
+        return launch_valu<TW, MR, 4>(a, epi, n_tiles, s, t);
     case 8:
-        return launch_valu<TW, MR, 8>(a, epi, n_tiles, s);
+        return launch_valu<TW, MR, 8>(a, epi, n_tiles, s, t);
     case 16:
         if constexpr (MR <= 4)
-            return launch_valu<TW, MR, 16>(a, epi, n_tiles, s);
+            return launch_valu<TW, MR, 16>(a, epi, n_tiles, s, t);
         return hipErrorInvalidValue;
     default:
         return hipErrorInvalidValue;
@@ -851,41 +865,42 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
 
 // Two rows on one-wave tiles (bf16 weights): loads of two chunks in flight
 // for 4 weight rows, one chunk for 8 (a sweep at the 13B shapes).
-static hipError_t launch_valu_wave2(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s) {
+static hipError_t launch_valu_wave2(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s,
+                                    const LaunchTiming &t) {
     switch (R) {
     case 4:
-        return launch_valu<uint16_t, 2, 4, 64, 2>(a, epi, n_tiles, s);
+        return launch_valu<uint16_t, 2, 4, 64, 2>(a, epi, n_tiles, s, t);
     case 8:
-        return launch_valu<uint16_t, 2, 8, 64, 1>(a, epi, n_tiles, s);
+        return launch_valu<uint16_t, 2, 8, 64, 1>(a, epi, n_tiles, s, t);
     default:
         return hipErrorInvalidValue;
     }
 }
 
 template <int TN, int NW, int NP>
-static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
+static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStream_t s, const LaunchTiming &t) {
     const int groups = (n_tiles + TN - 1) / TN;
     dim3 grid(groups * (epi == EPI_PARTIAL ? a.splits : 1)), block(NW * 64);
     switch (epi) {
     case EPI_PARTIAL:
         if (a.splits < 1 || !a.part)
             return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_linear_mfma<EPI_PARTIAL, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_PARTIAL, TN, NW, NP>, grid, block, s, t, a);
         break;
     case EPI_STORE:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_STORE, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_STORE, TN, NW, NP>, grid, block, s, t, a);
         break;
     case EPI_RESID:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_RESID, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_RESID, TN, NW, NP>, grid, block, s, t, a);
         break;
     case EPI_SWIGLU:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_SWIGLU, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_SWIGLU, TN, NW, NP>, grid, block, s, t, a);
         break;
     case EPI_QKV:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_QKV, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_QKV, TN, NW, NP>, grid, block, s, t, a);
         break;
     case EPI_HEAD:
-        hipLaunchKernelGGL((k_linear_mfma<EPI_HEAD, TN, NW, NP>), grid, block, 0, s, a);
+        launch_k(k_linear_mfma<EPI_HEAD, TN, NW, NP>, grid, block, s, t, a);
         break;
     default:
         return hipErrorInvalidValue;
@@ -895,27 +910,28 @@ static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStre
 
 // The work-group shape follows the output kind and the packing count
 // (mfma_shape_tn / mfma_shape_nw).
-static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipStream_t s) {
+static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipStream_t s,
+                                 const LaunchTiming &t) {
     const int np = mfma_packs(a.max_rows);
     if (epi == EPI_PARTIAL) {
         switch (np) {
         case 1:
-            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 1), mfma_shape_nw(EPI_PARTIAL, 1), 1>(a, epi, n_tiles, s);
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 1), mfma_shape_nw(EPI_PARTIAL, 1), 1>(a, epi, n_tiles, s, t);
         case 2:
-            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 2), mfma_shape_nw(EPI_PARTIAL, 2), 2>(a, epi, n_tiles, s);
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 2), mfma_shape_nw(EPI_PARTIAL, 2), 2>(a, epi, n_tiles, s, t);
         case 3:
-            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 3), mfma_shape_nw(EPI_PARTIAL, 3), 3>(a, epi, n_tiles, s);
+            return launch_mfma<mfma_shape_tn(EPI_PARTIAL, 3), mfma_shape_nw(EPI_PARTIAL, 3), 3>(a, epi, n_tiles, s, t);
         default:
             return hipErrorInvalidValue;
         }
     }
     switch (np) {
     case 1:
-        return launch_mfma<mfma_shape_tn(EPI_STORE, 1), mfma_shape_nw(EPI_STORE, 1), 1>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 1), mfma_shape_nw(EPI_STORE, 1), 1>(a, epi, n_tiles, s, t);
     case 2:
-        return launch_mfma<mfma_shape_tn(EPI_STORE, 2), mfma_shape_nw(EPI_STORE, 2), 2>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 2), mfma_shape_nw(EPI_STORE, 2), 2>(a, epi, n_tiles, s, t);
     case 3:
-        return launch_mfma<mfma_shape_tn(EPI_STORE, 3), mfma_shape_nw(EPI_STORE, 3), 3>(a, epi, n_tiles, s);
+        return launch_mfma<mfma_shape_tn(EPI_STORE, 3), mfma_shape_nw(EPI_STORE, 3), 3>(a, epi, n_tiles, s, t);
     default:
         return hipErrorInvalidValue;
     }
@@ -929,7 +945,7 @@ hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s)
 }
 
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
-                         hipStream_t s) {
+                         hipStream_t s, const LaunchTiming &t) {
     if (n_tiles <= 0)
         return hipSuccess;
     if (path == PATH_MFMA) {
@@ -943,23 +959,23 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
             return hipErrorInvalidValue;
         LinearArgs b = a;
         b.n_tiles = n_tiles;
-        return launch_mfma_np(b, epi, n_tiles, s);
+        return launch_mfma_np(b, epi, n_tiles, s, t);
     }
     if (a.K & 7)
         return hipErrorInvalidValue;
     if (path == PATH_GEMV)
-        return bf16 ? launch_valu_r<uint16_t, 1>(a, epi, rows_per_tile, n_tiles, s)
-                    : launch_valu_r<float, 1>(a, epi, rows_per_tile, n_tiles, s);
+        return bf16 ? launch_valu_r<uint16_t, 1>(a, epi, rows_per_tile, n_tiles, s, t)
+                    : launch_valu_r<float, 1>(a, epi, rows_per_tile, n_tiles, s, t);
     if (path == PATH_VALU4)
-        return bf16 ? launch_valu_r<uint16_t, 4>(a, epi, rows_per_tile, n_tiles, s)
-                    : launch_valu_r<float, 4>(a, epi, rows_per_tile, n_tiles, s);
+        return bf16 ? launch_valu_r<uint16_t, 4>(a, epi, rows_per_tile, n_tiles, s, t)
+                    : launch_valu_r<float, 4>(a, epi, rows_per_tile, n_tiles, s, t);
     if (path == PATH_VALU2)
-        return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s)
-                    : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s);
+        return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s, t)
+                    : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s, t);
     if (path == PATH_WAVE2)
-        return bf16 ? launch_valu_wave2(a, epi, rows_per_tile, n_tiles, s) : hipErrorInvalidValue;
-    return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s)
-                : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s);
+        return bf16 ? launch_valu_wave2(a, epi, rows_per_tile, n_tiles, s, t) : hipErrorInvalidValue;
+    return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s, t)
+                : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s, t);
 }
 
 }  // namespace sdk

@@ -374,15 +374,17 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
                 m->tev.push_back(e);
             }
         }
-        SD_HIP(hipEventRecord(m->tev[m->tev_used], m->stream));
         m->timed_rows_lo = m->timed_rows_lo ? std::min(m->timed_rows_lo, max_rows) : max_rows;
         m->timed_rows_hi = std::max(m->timed_rows_hi, max_rows);
     }
-    SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream), "linear layer"));
+    LaunchTiming lt;
     if (timed) {
-        SD_HIP(hipEventRecord(m->tev[m->tev_used + 1], m->stream));
-        m->tev_used += 2;
+        lt.start = m->tev[m->tev_used];
+        lt.stop = m->tev[m->tev_used + 1];
     }
+    SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream, lt), "linear layer"));
+    if (timed)
+        m->tev_used += 2;
     if (p.epi == EPI_HEAD && epi.head.sampled) {
         SampleArgs sa{};
         sa.sp = m->sp_cur;
@@ -426,10 +428,9 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
                           const HeadSpec &hs) {
     const sd_config &c = m->cfg;
     const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
-    // The measurement hook brackets the timed class in one of every
-    // TIMED_SAMPLE forwards of its regime: an event pair costs about 5 us of
-    // stream time on each side of the launch, which would otherwise inflate
-    // the step it measures.
+    // The measurement hook times the class in one of every TIMED_SAMPLE
+    // forwards of its regime, with events the runtime attaches to the
+    // dispatch (the kernel's own start and end).
     m->timed_now = P[0].regime == m->timed_regime && m->timed_kind >= 0 &&
                    (m->timed_forwards++ % TIMED_SAMPLE) == 0;
     int pending = 0;  // split-K partials not yet folded into h

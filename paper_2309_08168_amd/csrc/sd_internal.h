@@ -281,9 +281,14 @@ hipError_t launch_pf_swiglu_split(const float *gu, int F, int M, uint16_t *out, 
 // PATH_WAVE2: up to two rows on one-wave tiles (bf16 weights).
 enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4, PATH_WAVE2 = 5 };
 
+// Optional events the runtime records at a launch's own start and end.
+struct LaunchTiming {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
-                         hipStream_t s);
+                         hipStream_t s, const LaunchTiming &t = LaunchTiming{});
 // g * h / rms(h), or plain h (gain == null), split into X_TERMS bf16 terms in
 // fragment layout for the MFMA path (K a multiple of 128).  First adds n_part
 // pending split-K partials ([n_part][MAX_ROWS][K]) into h.
