@@ -4,10 +4,11 @@
 //
 // Every step of greedy decoding at batch 1 streams the whole weight set
 // once (Sec. 3.1: model size over memory bandwidth bounds the decode
-// speed), so the three main loops below are built to read each weight byte
+// speed), so the main loops below are built to read each weight byte
 // exactly once with 16-byte loads:
 //   - k_linear_valu, MR == 1: the GEMV of a draft or autoregressive step;
-//   - k_linear_valu, MR == 2 or 4: verification of 1 or up to 3 drafts;
+//   - k_linear_valu, MR == 2: verification of one draft (one-wave tiles for
+//     bf16 weights);
 //   - k_linear_valu, MR == 16: any row count, for float32 weights;
 //   - k_linear_mfma: the verification forward over up to 16 rows (the last
 //     committed token plus the drafts, Algorithm 2) on bf16 MFMA tiles, the
