@@ -698,8 +698,17 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         }
         fin[o] = v;
     }
-    if (tid < 16)
-        inv_s[tid] = 1.0f;  // the activations arrive normalised
+    if (tid < 16) {
+        // RMSNorm: the fragments hold g * h; the slices' sums of h^2, in order
+        float v = 1.0f;
+        if (a.ssq && tid < M) {
+            float ss = 0.0f;
+            for (int sl = 0; sl < a.ssq_slices; ++sl)
+                ss += a.ssq[tid * a.ssq_slices + sl];
+            v = 1.0f / sqrtf(ss / (float)a.K + a.eps);
+        }
+        inv_s[tid] = v;
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -710,32 +719,35 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Activations for the MFMA path: u = g * h / rms(h), or u = h without a
-// gain, split into X_TERMS bf16 terms in fragment layout, after folding
-// pending split-K partials into h.  One work-group per row.
+// Activations for the MFMA path, one work-group per (row, slice of
+// PREP_SLICE elements): the pending split-K partials of the last output
+// projection are added into h (in split order), u = g * h (or h without a
+// gain) is split into X_TERMS bf16 terms in fragment layout, and the
+// slice's sum of h^2 goes to ssq[row][slice].  The consuming kernel sums
+// the slices in order and divides its outputs by rms(h) itself, so no
+// work-group needs the whole row and every slice is one round trip.
 
 template <typename TW>
-__global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const TW *g, float eps, int K,
-                                                    const DevCtl *ctl, uint16_t *xs, const float *part,
-                                                    int n_part) {
-    __shared__ float red[16];
-    const int r = blockIdx.x, M = ctl->m;
+__global__ __launch_bounds__(PREP_SLICE / 4) void k_prep_norm(float *h, int64_t ldh, const TW *g, int K,
+                                                              const DevCtl *ctl, uint16_t *xs, const float *part,
+                                                              int n_part, float *ssq) {
+    __shared__ float red[PREP_SLICE / 256];
+    const int r = blockIdx.x, sl = blockIdx.y, M = ctl->m;
     if (r >= M)
         return;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, k4 = sl * (PREP_SLICE / 4) + tid;
+    const bool ok = 4 * k4 < K;
     float4 *hr = reinterpret_cast<float4 *>(h + (int64_t)r * ldh);
-    const int K4 = K >> 2;
-    // pending split-K partials of the last output projection, added in
-    // split order; every load of an element is issued before the adds
-    float ss = 0.0f;
-    for (int k = tid; k < K4; k += 1024) {
-        float4 v = hr[k];
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (ok) {
+        v = hr[k4];
         if (n_part > 0) {
+            // every load of the element is issued before the adds
             float4 p[8];
 #pragma unroll
             for (int sp = 0; sp < 8; ++sp)
                 if (sp < n_part)
-                    p[sp] = reinterpret_cast<const float4 *>(part + ((int64_t)sp * MAX_ROWS + r) * K)[k];
+                    p[sp] = reinterpret_cast<const float4 *>(part + ((int64_t)sp * MAX_ROWS + r) * K)[k4];
 #pragma unroll
             for (int sp = 0; sp < 8; ++sp)
                 if (sp < n_part) {
@@ -744,63 +756,64 @@ __global__ __launch_bounds__(1024) void k_prep_norm(float *h, int64_t ldh, const
                     v.z += p[sp].z;
                     v.w += p[sp].w;
                 }
-            hr[k] = v;
+            hr[k4] = v;
         }
-        ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
     }
-    float inv = 1.0f;
     if (g) {
+        float ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, v.w * v.w)));
         ss = wave_sum(ss);
         if ((tid & 63) == 0)
             red[tid >> 6] = ss;
         __syncthreads();
-        float t = 0.0f;
-        for (int w = 0; w < 16; ++w)
-            t += red[w];
-        inv = 1.0f / sqrtf(t / (float)K + eps);
+        if (tid == 0) {
+            float t = 0.0f;
+            for (int w = 0; w < PREP_SLICE / 256; ++w)
+                t += red[w];
+            ssq[r * gridDim.y + sl] = t;
+        }
     }
-    for (int k = tid; k < K4; k += 1024) {
-        const float4 v = hr[k];
-        float u[4] = {v.x, v.y, v.z, v.w};
-        uint16_t t[X_TERMS][4];
+    if (!ok)
+        return;
+    float u[4] = {v.x, v.y, v.z, v.w};
+    uint16_t t[X_TERMS][4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if (g) {
-                float gk;
-                if constexpr (sizeof(TW) == 2)
-                    gk = bf2f(g[4 * k + e]);
-                else
-                    gk = g[4 * k + e];
-                u[e] = gk * (u[e] * inv);
-            }
-            const uint16_t hi = bf16_rne_bits(u[e]);
-            const float r1 = u[e] - bf2f(hi);
-            const uint16_t mid = bf16_rne_bits(r1);
-            t[0][e] = hi;
-            t[1][e] = mid;
-            t[2][e] = bf16_rne_bits(r1 - bf2f(mid));
+    for (int e = 0; e < 4; ++e) {
+        if (g) {
+            float gk;
+            if constexpr (sizeof(TW) == 2)
+                gk = bf2f(g[4 * k4 + e]);
+            else
+                gk = g[4 * k4 + e];
+            u[e] *= gk;
         }
-        // four consecutive k stay contiguous in the fragment layout
+        const uint16_t hi = bf16_rne_bits(u[e]);
+        const float r1 = u[e] - bf2f(hi);
+        const uint16_t mid = bf16_rne_bits(r1);
+        t[0][e] = hi;
+        t[1][e] = mid;
+        t[2][e] = bf16_rne_bits(r1 - bf2f(mid));
+    }
+    // four consecutive k stay contiguous in the fragment layout
 #pragma unroll
-        for (int i = 0; i < X_TERMS; ++i) {
-            uint2 pk;
-            pk.x = t[i][0] | ((uint32_t)t[i][1] << 16);
-            pk.y = t[i][2] | ((uint32_t)t[i][3] << 16);
-            *reinterpret_cast<uint2 *>(xs + xfrag_off(i, r, 4 * k, M)) = pk;
-        }
+    for (int i = 0; i < X_TERMS; ++i) {
+        uint2 pk;
+        pk.x = t[i][0] | ((uint32_t)t[i][1] << 16);
+        pk.y = t[i][2] | ((uint32_t)t[i][3] << 16);
+        *reinterpret_cast<uint2 *>(xs + xfrag_off(i, r, 4 * k4, M)) = pk;
     }
 }
 
-hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K, const DevCtl *ctl,
-                            uint16_t *xs, const float *part, int n_part, hipStream_t s) {
-    if ((K & 127) || (ldh & 3) || n_part > 8)
+hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, int K, const DevCtl *ctl,
+                            uint16_t *xs, const float *part, int n_part, float *ssq, hipStream_t s) {
+    if ((K & 127) || (ldh & 3) || n_part > 8 || (gain && !ssq))
         return hipErrorInvalidValue;
+    const dim3 grid(MAX_ROWS, prep_slices(K)), block(PREP_SLICE / 4);
     if (bf16)
-        hipLaunchKernelGGL(k_prep_norm<uint16_t>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const uint16_t *>(gain), eps, K, ctl, xs, part, n_part);
+        hipLaunchKernelGGL(k_prep_norm<uint16_t>, grid, block, 0, s, h, ldh, reinterpret_cast<const uint16_t *>(gain),
+                           K, ctl, xs, part, n_part, ssq);
     else
-        hipLaunchKernelGGL(k_prep_norm<float>, dim3(MAX_ROWS), dim3(1024), 0, s, h, ldh,
-                           reinterpret_cast<const float *>(gain), eps, K, ctl, xs, part, n_part);
+        hipLaunchKernelGGL(k_prep_norm<float>, grid, block, 0, s, h, ldh, reinterpret_cast<const float *>(gain), K,
+                           ctl, xs, part, n_part, ssq);
     return hipGetLastError();
 }
 

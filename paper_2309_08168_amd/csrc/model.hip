@@ -88,6 +88,7 @@ struct sd_model {
     Plan plan2[LK_COUNT];  // up to 2 rows (verification of one draft)
     Plan planm[LK_COUNT];  // up to 16 rows (longer verification, prefill)
     float *part = nullptr;  // split-K partials of the MFMA output projections
+    float *ssq = nullptr;   // sums of h^2 per row and slice for the next normed MFMA layer
 
     float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
     // MFMA-path activations split into X_TERMS bf16 terms in fragment layout
@@ -341,8 +342,8 @@ sd_status launch(hipError_t e, const char *what) {
 
 // One linear layer over up to max_rows rows.  X (float32, with the RMSNorm
 // gain folded in by the VALU kernels) feeds the VALU paths; the MFMA path
-// reads the bf16 term planes xs (already normalised by k_prep_norm or split
-// by the producer).
+// reads the bf16 term planes xs (g * h from k_prep_norm, the layer dividing
+// by rms(h) itself, or split by the producer for the output projections).
 sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, const float *X, int64_t ldx,
                      const void *gain, const EpiArgs &epi, const uint16_t *xs) {
     LinearArgs a{};
@@ -352,6 +353,10 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
     if (p.path == PATH_MFMA) {
         a.Xs = xs;
         a.max_rows = max_rows;
+        if (gain) {  // the fragments hold g * h; 1/rms(h) from the slices' sums
+            a.ssq = m->ssq;
+            a.ssq_slices = prep_slices(p.K);
+        }
     } else {
         a.X = X;
         a.ldx = ldx;
@@ -403,12 +408,13 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
 }
 
 // The MFMA operand of a normed layer into xa (MFMA path only), after folding
-// the pending split-K partials of the last output projection: g * h / rms(h).
+// the pending split-K partials of the last output projection: g * h, with
+// the sums of h^2 per slice in ssq for the layer's 1/rms(h).
 sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
     if (p.path != PATH_MFMA)
         return SD_OK;
-    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, m->cfg.rms_eps, p.K, m->ctl, m->xa, m->part,
-                                   pending, m->stream),
+    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, p.K, m->ctl, m->xa, m->part, pending, m->ssq,
+                                   m->stream),
                   "norm"));
     pending = 0;
     return SD_OK;
@@ -993,6 +999,7 @@ void destroy_model(sd_model *m) {
     dev_free(m->o);
     dev_free(m->mbuf);
     dev_free(m->part);
+    dev_free(m->ssq);
     dev_free(m->xa);
     dev_free(m->xb);
     dev_free(m->head_part);
@@ -1079,6 +1086,7 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     chain(dev_alloc(&m->o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
     chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
     chain(dev_alloc(&m->part, (size_t)8 * MAX_ROWS * c.d_model));
+    chain(dev_alloc(&m->ssq, (size_t)MAX_ROWS * prep_slices(c.d_model)));
     m->xld = std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
     chain(dev_alloc(&m->xa, (size_t)X_TERMS * MAX_ROWS * m->xld));
     chain(dev_alloc(&m->xb, (size_t)X_TERMS * MAX_ROWS * m->xld));

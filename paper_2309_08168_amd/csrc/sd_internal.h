@@ -94,11 +94,11 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
 __host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * max_rows + 15) / 16; }
 
 // MFMA work-group shape (16-row tiles per work-group, waves per work-group)
-// by output kind and packing count, from a sweep at the 13B shapes: two
-// tiles for one packing and for the split-K output projections, four tiles
-// for two or three packings; four waves throughout.
+// by output kind and packing count, from sweeps at the 13B shapes: two
+// tiles for the split-K output projections, four otherwise (at 4, 8 and 13
+// rows); four waves throughout.
 __host__ __device__ constexpr int mfma_shape_tn(int epi, int np) {
-    return epi == EPI_PARTIAL ? 2 : (np == 1 ? 2 : 4);
+    return (void)np, epi == EPI_PARTIAL ? 2 : 4;
 }
 __host__ __device__ constexpr int mfma_shape_nw(int epi, int np) { return (void)epi, (void)np, 4; }
 
@@ -208,6 +208,9 @@ struct LinearArgs {
     int32_t max_rows;      // MFMA path: host bound on ctl->m, sets the MFMAs per k-step
     int64_t ldx;
     const void *gain;      // VALU paths: RMSNorm gain [K] (weight dtype), or null: no norm
+    const float *ssq;      // MFMA path with RMSNorm: the slices' sums of h^2 [MAX_ROWS][ssq_slices]
+                           // (the fragments then hold gain * h), or null: no norm
+    int32_t ssq_slices;
     float eps;
     const DevCtl *ctl;
     EpiArgs epi;
@@ -289,11 +292,16 @@ struct LaunchTiming {
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s, const LaunchTiming &t = LaunchTiming{});
-// g * h / rms(h), or plain h (gain == null), split into X_TERMS bf16 terms in
-// fragment layout for the MFMA path (K a multiple of 128).  First adds n_part
-// pending split-K partials ([n_part][MAX_ROWS][K]) into h.
-hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, float eps, int K,
-                            const DevCtl *ctl, uint16_t *xs, const float *part, int n_part, hipStream_t s);
+// Elements per work-group of the MFMA-path input preparation.
+constexpr int PREP_SLICE = 512;
+__host__ __device__ constexpr int prep_slices(int K) { return (K + PREP_SLICE - 1) / PREP_SLICE; }
+// g * h, or plain h (gain == null), split into X_TERMS bf16 terms in fragment
+// layout for the MFMA path (K a multiple of 128), with the sums of h^2 of
+// each PREP_SLICE-element slice in ssq [MAX_ROWS][prep_slices(K)] (gain set)
+// for the consumer's 1/rms(h).  First adds n_part pending split-K partials
+// ([n_part][MAX_ROWS][K]) into h.
+hipError_t launch_prep_norm(float *h, int64_t ldh, const void *gain, bool bf16, int K, const DevCtl *ctl,
+                            uint16_t *xs, const float *part, int n_part, float *ssq, hipStream_t s);
 // After a head linear: combines its n_tiles partials and takes the decoding decision.
 hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s);
 // Sampling variant, after a head linear that wrote the logits: the nucleus
