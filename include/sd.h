@@ -297,10 +297,10 @@ sd_status sd_search_skip_set(sd_model *model, const int32_t *prompts, int32_t n_
  * output, 2 = gate/up, 3 = down, 4 = lm-head; rows = 1, 2 or 16 selects the
  * kernel family used for forwards of one row, up to two rows, or more rows.
  * layer = -1 turns timing off.  The launches of the class in one of every
- * 16 forwards of that row regime are timed (an event pair adds about 10 us
- * of stream time around its launch, so timing every forward would slow the
- * steps being measured); at most 65536 launches per call are timed.  Resets
- * the totals and the forward count.  Errors: INVALID_ARG. */
+ * 16 forwards of that row regime are timed, with start/stop events the
+ * runtime attaches to the dispatch itself (the kernel's own start and end);
+ * at most 65536 launches per call are timed.  Resets the totals and the
+ * forward count.  Errors: INVALID_ARG. */
 sd_status sd_model_time_kernel(sd_model *model, int32_t layer, int32_t rows);
 
 /* Totals of the timed class since sd_model_time_kernel: launches, summed
