@@ -642,6 +642,81 @@ def run_summarize_pmc(args):
     print(json.dumps(out, indent=1))
 
 
+def _dispatches(path):
+    """Counter values per dispatch, in dispatch order: [(kernel, {counter: value}, ns)]."""
+    d = {}
+    for r in _read_csv(path):
+        i = int(r["Dispatch_Id"])
+        e = d.setdefault(i, [r["Kernel_Name"], {}, int(r["End_Timestamp"]) - int(r["Start_Timestamp"])])
+        e[1][r["Counter_Name"]] = float(r["Counter_Value"])
+    return [tuple(d[i]) for i in sorted(d)]
+
+
+def _forwards(disp):
+    """The dispatches of each sd_forward (a forward of up to 16 rows starts with
+    the control-block kernel); runtime copies and torch kernels are left out."""
+    out, cur = [], None
+    for name, c, ns in disp:
+        if "k_set_ctl" in name:
+            cur = []
+            out.append(cur)
+        elif cur is not None and "copyBuffer" not in name and "at::native" not in name:
+            cur.append((name, c, ns))
+    return out
+
+
+def run_summarize_step_counters(args):
+    """HBM bytes per verification forward from FETCH_SIZE / WRITE_SIZE (all
+    kernels of the forward, calibrated by the 1 GiB copy) against the
+    algorithmic bytes, and MFMA busy cycles and issued bf16 flops per kernel of
+    the 13-row forward.  Inputs: the counter CSVs of
+    --verify-micro --micro-rows 1,2,13 --micro-ctx 512 --micro-iters 1 --with-copy
+    (FETCH_SIZE, WRITE_SIZE) and of --micro-rows 13 (MFMA counters)."""
+    fetch_csv, write_csv, mfma_csv = args.summarize_step_counters
+    cfg = S.MODELS["13b"]
+    fd, wd = _dispatches(fetch_csv), _dispatches(write_csv)
+
+    def calib(disp, counter):
+        cp = [c[counter] for name, c, _ in disp if "copybuffer" in name.lower() and counter in c]
+        return args.copy_bytes / (max(cp) * 1024.0) if cp else 1.0
+
+    cf, cw = calib(fd, "FETCH_SIZE"), calib(wd, "WRITE_SIZE")
+    ff, wf = _forwards(fd), _forwards(wd)
+    rows_list = [1, 2, 13]
+    lines = ["# HBM bytes per 13B forward (FETCH_SIZE + WRITE_SIZE over all its kernels) and MFMA counters",
+             f"# command: {args.command}",
+             f"# copy calibration: FETCH_SIZE x{cf:.4f}, WRITE_SIZE x{cw:.4f}", "",
+             f"{'rows':>4} {'kernels':>7} {'fetch_GB':>9} {'write_GB':>9} {'total_GB':>9} {'algorithmic_GB':>15} {'ratio':>6}"]
+    for j, M in enumerate(rows_list):
+        idx = 2 * j + 1  # the timed forward of each row count (after one warm-up)
+        if idx >= len(ff) or idx >= len(wf):
+            break
+        fb = sum(c.get("FETCH_SIZE", 0.0) for _, c, _ in ff[idx]) * 1024.0 * cf
+        wb = sum(c.get("WRITE_SIZE", 0.0) for _, c, _ in wf[idx]) * 1024.0 * cw
+        alg = step_bytes(cfg, None, 512, M)
+        lines.append(f"{M:4d} {len(ff[idx]):7d} {fb / 1e9:9.3f} {wb / 1e9:9.3f} {(fb + wb) / 1e9:9.3f} "
+                     f"{alg / 1e9:15.3f} {(fb + wb) / alg:6.3f}")
+    md = _forwards(_dispatches(mfma_csv))
+    if len(md) >= 2:
+        lines += ["", "# 13-row forward, MFMA kernels: busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x duration x 2.4 GHz);",
+                  "# issued = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops (three bf16 terms per row in 16 columns per packing)",
+                  f"{'calls':>5} {'avg_us':>7} {'busy':>6} {'issued_TFLOPs':>13}  kernel"]
+        per = {}
+        for name, c, ns in md[1]:
+            if "k_linear_mfma" not in name:
+                continue
+            e = per.setdefault(name, [0, 0.0, 0.0, 0.0])
+            e[0] += 1
+            e[1] += ns
+            e[2] += c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            e[3] += c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512.0
+        for name, (n, ns, busy, flops) in sorted(per.items(), key=lambda kv: -kv[1][1]):
+            lines.append(f"{n:5d} {ns / n / 1e3:7.2f} {busy / (1024 * ns * 2.4):6.3f} {flops / ns / 1e3:13.1f}  {name}")
+    os.makedirs(os.path.dirname(args.out), exist_ok=True)
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -676,6 +751,7 @@ def main():
     ap.add_argument("--summarize-stats", default=None, help="rocprofv3 kernel_stats.csv to summarize")
     ap.add_argument("--summarize-pmc", nargs=2, default=None, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--kernels", default="", help="';'-separated kernel symbols for --summarize-pmc")
+    ap.add_argument("--summarize-step-counters", nargs=3, default=None, metavar=("FETCH_CSV", "WRITE_CSV", "MFMA_CSV"))
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles", "kernel_stats.txt"))
     ap.add_argument("--top", type=int, default=20)
     ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
@@ -685,6 +761,8 @@ def main():
         return run_summarize_stats(args)
     if args.summarize_pmc:
         return run_summarize_pmc(args)
+    if args.summarize_step_counters:
+        return run_summarize_step_counters(args)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: --gpus {args.gpus} is not supported (the decode path is "
               "batch-1 on a single MI355X; DESIGN.md describes how it would shard)", file=sys.stderr)
