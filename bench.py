@@ -765,7 +765,7 @@ def main():
         return run_summarize_step_counters(args)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: --gpus {args.gpus} is not supported (the decode path is "
-              "batch-1 on a single MI355X; DESIGN.md describes how it would shard)", file=sys.stderr)
+              "batch-1 on a single MI355X; independent requests would run one model copy per GPU)", file=sys.stderr)
         sys.exit(2)
     import torch
 
