@@ -10,7 +10,7 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (runs the HIP library on cuda:0)")
-    config.addinivalue_line("markers", "big: full-size model shapes (minutes; GPU box only)")
+    config.addinivalue_line("markers", "big: full-size model shapes (minutes on an MI355X)")
 
 
 @pytest.fixture(scope="session", autouse=True)
