@@ -50,11 +50,11 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4, LK_COUNT = 5 };
 
-// How one linear layer is launched for one row regime.
 // Forwards of the timed regime per forward whose launches the measurement
 // hook brackets with events.
 constexpr int64_t TIMED_SAMPLE = 16;
 
+// How one linear layer is launched for one row regime.
 struct Plan {
     int kind;     // LinearKind
     int regime;   // 1, 2 or 16: the row counts the plan serves
