@@ -68,6 +68,40 @@ __device__ inline uint64_t wave_sum_u64(uint64_t v) {
     return v;
 }
 
+// Sums of 16 per-lane values over the 64 lanes of a wave by a transposing
+// butterfly.  At the step over lane bit b (b = 5, 4, 3, 2) each lane keeps
+// the half of its values selected by that bit and adds its partner's copy
+// of them (8 + 4 + 2 + 1 shuffles); two plain steps over bits 1 and 0 then
+// add the four lanes that hold the same value.  Lane l returns the wave's
+// sum of value (l >> 2) & 15: 17 shuffles instead of 16 x 6.  Integer sums
+// are exact in any order.
+__device__ inline uint64_t wave_sum16_u64(const uint64_t (&acc)[16], int lane) {
+    uint64_t a8[8], a4[4], a2[2];
+    {
+        const bool h = lane & 32;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            a8[j] = (h ? acc[8 + j] : acc[j]) + __shfl_xor(h ? acc[j] : acc[8 + j], 32, 64);
+    }
+    {
+        const bool h = lane & 16;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            a4[j] = (h ? a8[4 + j] : a8[j]) + __shfl_xor(h ? a8[j] : a8[4 + j], 16, 64);
+    }
+    {
+        const bool h = lane & 8;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            a2[j] = (h ? a4[2 + j] : a4[j]) + __shfl_xor(h ? a4[j] : a4[2 + j], 8, 64);
+    }
+    const bool h = lane & 4;
+    uint64_t a1 = (h ? a2[1] : a2[0]) + __shfl_xor(h ? a2[0] : a2[1], 4, 64);
+    a1 += __shfl_xor(a1, 2, 64);
+    a1 += __shfl_xor(a1, 1, 64);
+    return a1;
+}
+
 // Block sum over NT threads; red is LDS scratch of NT / 64 words.  Integer:
 // any order is exact.
 template <int NT = SW>
@@ -258,11 +292,10 @@ __global__ __launch_bounds__(NT) void k_warp_rows(SampleArgs a, int mode) {
                 for (int x = tid; x < V; x += NT)
                     add(__float_as_uint(warp_w(lg[x], mx, T)));
             }
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const uint64_t v = wave_sum_u64(acc[i]);
-                if (lane == 0)
-                    bins[wave][i] = v;
+            {
+                const uint64_t v = wave_sum16_u64(acc, lane);
+                if ((lane & 3) == 0)
+                    bins[wave][lane >> 2] = v;
             }
             __syncthreads();
             if (tid < 16) {
