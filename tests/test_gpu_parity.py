@@ -30,7 +30,10 @@ def _need_gpu():
         pytest.skip("no GPU")
 
 
-MODELS = {"tiny": S.MODELS["tiny"], "mini_bf16": U.MINI_BF16, "micro_gqa": U.MICRO_GQA}
+# d_model 640: the MFMA-path input preparation covers one full 512-element
+# slice and one partial slice per row
+SLICES_BF16 = S.ModelConfig("slices_bf16", 2, 640, 5, 5, 128, 1280, 1000, "bf16")
+MODELS = {"tiny": S.MODELS["tiny"], "mini_bf16": U.MINI_BF16, "micro_gqa": U.MICRO_GQA, "slices_bf16": SLICES_BF16}
 _cache = {}
 
 
