@@ -456,33 +456,45 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
     if (grp == 0)
         red_ml[wave][col] = make_float2(mx, ls);
     __syncthreads();
-    // merge the waves in wave order; one (query, element) per thread
+    // merge the waves in wave order: the weight of each wave's state per
+    // query column first (16 threads), then one (query, element) per thread.
+    // A wave whose keys are all masked has weight 0 and an all-zero output.
+    __shared__ float wts[MW][16];
+    __shared__ float2 mls[16];
+    if (threadIdx.x < 16) {
+        const int qc = threadIdx.x;
+        float m = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < MW; ++w)
+            m = fmaxf(m, red_ml[w][qc].x);
+        float L = 0.0f;
+#pragma unroll
+        for (int w = 0; w < MW; ++w) {
+            const float2 ml = red_ml[w][qc];
+            float wt = 0.0f;
+            if (m != -INFINITY && ml.x != -INFINITY) {
+                wt = expf(ml.x - m);
+                L = fmaf(wt, ml.y, L);
+            }
+            wts[w][qc] = wt;
+        }
+        mls[qc] = make_float2(m, L);
+    }
+    __syncthreads();
     for (int t = threadIdx.x; t < 16 * DH; t += MW * 64) {
         const int qc = t / DH, e = t - qc * DH;
         const int qj = qt * 16 + qc;
         if (qj >= Q)
             break;  // t only grows
-        float m = -INFINITY;
+        float O = 0.0f;
 #pragma unroll
         for (int w = 0; w < MW; ++w)
-            m = fmaxf(m, red_ml[w][qc].x);
-        float L = 0.0f, O = 0.0f;
-        if (m != -INFINITY) {
-#pragma unroll
-            for (int w = 0; w < MW; ++w) {
-                const float2 ml = red_ml[w][qc];
-                if (ml.x != -INFINITY) {
-                    const float wt = expf(ml.x - m);
-                    L = fmaf(wt, ml.y, L);
-                    O = fmaf(wt, reinterpret_cast<const float *>(tile[w])[e * OP + qc], O);
-                }
-            }
-        }
+            O = fmaf(wts[w][qc], reinterpret_cast<const float *>(tile[w])[e * OP + qc], O);
         const int rj = qj / G, hj = g * G + (qj - rj * G);
         const int64_t slot = ((int64_t)split * H + hj) * MAX_ROWS + rj;
         a.part_o[slot * DH + e] = O;
         if (e == 0)
-            a.part_ml[slot] = make_float2(m, L);
+            a.part_ml[slot] = mls[qc];
     }
 }
 
