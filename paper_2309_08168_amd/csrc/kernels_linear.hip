@@ -980,9 +980,6 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
     if (path == PATH_GEMV)
         return bf16 ? launch_valu_r<uint16_t, 1>(a, epi, rows_per_tile, n_tiles, s, t)
                     : launch_valu_r<float, 1>(a, epi, rows_per_tile, n_tiles, s, t);
-    if (path == PATH_VALU4)
-        return bf16 ? launch_valu_r<uint16_t, 4>(a, epi, rows_per_tile, n_tiles, s, t)
-                    : launch_valu_r<float, 4>(a, epi, rows_per_tile, n_tiles, s, t);
     if (path == PATH_VALU2)
         return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s, t)
                     : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s, t);

@@ -1160,7 +1160,7 @@ std::string kernel_symbol(const sd_model *m, const Plan &p) {
     }
     const int mr = p.path == PATH_GEMV
                        ? 1
-                       : ((p.path == PATH_VALU2 || p.path == PATH_WAVE2) ? 2 : (p.path == PATH_VALU4 ? 4 : 16));
+                       : ((p.path == PATH_VALU2 || p.path == PATH_WAVE2) ? 2 : 16);
     const bool wave = p.path == PATH_WAVE2;
     const int nt = wave ? 64 : 256, u = wave && p.rows == 4 ? 2 : 1;
     return std::string("void sdk::k_linear_valu<") + tw + ", " + std::to_string(mr) + ", " + std::to_string(p.rows) +

@@ -282,7 +282,7 @@ hipError_t launch_pf_swiglu_split(const float *gu, int F, int M, uint16_t *out, 
 
 // Kernel paths of the linear layers.
 // PATH_WAVE2: up to two rows on one-wave tiles (bf16 weights).
-enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU4 = 3, PATH_VALU2 = 4, PATH_WAVE2 = 5 };
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU2 = 3, PATH_WAVE2 = 4 };
 
 // Optional events the runtime records at a launch's own start and end.
 struct LaunchTiming {
