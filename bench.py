@@ -77,10 +77,11 @@ def step_bytes(cfg, skip, ctx: float, rows: float = 1):
     return total
 
 
-def kernel_bytes(n: int, k: int, rows: float, es: int = 2) -> float:
-    """Algorithmic bytes of one linear launch: the n x k weights once, the
-    float32 input rows and output rows."""
-    return n * k * es + rows * k * 4 + rows * n * 4
+def gate_up_bytes(n: int, k: int, rows: float, es: int = 2) -> float:
+    """Algorithmic bytes of one gate/up launch with the RMSNorm folded in:
+    the n x k weights (gate and up rows) and the norm gain once, the float32
+    input rows, and the float32 SwiGLU outputs (n / 2 per row)."""
+    return n * k * es + k * es + rows * k * 4 + rows * (n // 2) * 4
 
 
 def source_hash() -> str:
@@ -255,7 +256,7 @@ def run_bench(args):
     if kt["launches"]:
         avg_ms = kt["total_ms"] / kt["launches"]
         rows = regime if regime == 2 else vrows
-        nbytes = kernel_bytes(kt["n"], kt["k"], rows)
+        nbytes = gate_up_bytes(kt["n"], kt["k"], rows)
         achieved = nbytes / (avg_ms / 1e3) / 1e9
         roofline = {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
