@@ -195,6 +195,53 @@ def test_cache_load_matches_written_cache():
     assert not np.allclose(m.forward(c3, [4, 5, 6])["logits"], a)
 
 
+MICRO_BF16_GQA = S.micro_config(n_layers=2, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16, ffn_dim=96,
+                                vocab=97, dtype="bf16", name="micro_bf16_gqa")
+
+
+def kv_layout(kv_pairs, length: int) -> np.ndarray:
+    """K/V pairs of the library-built model ([T, KVH, dh] per layer) in the
+    cache-load layout [L][2 (K, V)][KVH][length][dh]."""
+    return np.stack([np.stack([k[:length].transpose(1, 0, 2), v[:length].transpose(1, 0, 2)]) for k, v in kv_pairs])
+
+
+def check_cache_load(lib_path=oracle.LIB_PATH):
+    """K/V written by the library-built float64 model for positions [0, P),
+    loaded into an oracle cache, then an oracle forward of the remaining rows:
+    its logits equal the library-built model's over the whole sequence.
+
+    The loaded values come from a different implementation (torch SDPA
+    model), so a layout mistake in the loader (K and V swapped, heads before
+    K/V, positions and head_dim transposed, a dropped layer) changes what the
+    rows attend to and fails.  Both a bf16 model (bf16 bits, the verify
+    microbenchmark's case) and a float32 model (float32 values) are loaded."""
+    for cfg, dt in ((MICRO_BF16_GQA, "bf16"), (MICRO_GQA, "f32")):
+        w = S.make_weights(cfg, 9)
+        toks = S.prompt(cfg, 14, seed=10)
+        P = 9
+        pairs = []
+        ref = torch_ref.forward(cfg, S.weights_as_f64(cfg, w), toks, kv_out=pairs)
+        assert len(pairs) == cfg.n_layers
+        kv = kv_layout(pairs, P)
+        if dt == "bf16":
+            kvs = S.f32_to_bf16_bits(kv.astype(np.float32))
+            assert np.array_equal(S.bf16_bits_to_f32(kvs), kv)  # exact: the model rounded them to bf16
+        else:
+            kvs = kv.astype(np.float32)
+        m = oracle.Model(cfg, w, lib_path=lib_path)
+        c = m.cache(16)
+        c.load(kvs, P, dt)
+        assert c.length == P
+        got = m.forward(c, toks[P:])["logits"]
+        # float32 model: the loaded values were rounded to float32, the oracle's own are exact
+        tol = 1e-10 if dt == "bf16" else 1e-6
+        assert _rel(got, ref[P:]) < tol, (cfg.name, _rel(got, ref[P:]))
+
+
+def test_cache_load_matches_library_built_kv():
+    check_cache_load()
+
+
 # --------------------------------------------------------------------------
 # decoding invariants (losslessness, acceptance, stage counts)
 

@@ -45,6 +45,14 @@ MUTATIONS = {
     "adapt_no_init": ("ar = n_updates == 0 ? ar_e : ad->beta1 * ar", "ar = n_updates < 0 ? ar_e : ad->beta1 * ar"),
     "adapt_rate_with_bonus": ("const double ar_e = (double)na / (double)k;",
                               "const double ar_e = (double)na / (double)(k + 1);"),
+    # loader of externally filled caches ([L][2][KVH][len][dh])
+    "cache_load_kv_swapped": ("double *dst = c->kv + kv_index(c, l, kvi, g, p);",
+                              "double *dst = c->kv + kv_index(c, l, 1 - kvi, g, p);"),
+    "cache_load_heads_first": ("for (int kvi = 0; kvi < 2; ++kvi)\n            for (int g = 0; g < cf->n_kv_heads; ++g)",
+                               "for (int g = 0; g < cf->n_kv_heads; ++g)\n            for (int kvi = 0; kvi < 2; ++kvi)"),
+    "cache_load_transposed": ("dst[e] = kv_dtype == 1 ? bf16_to_double(((const uint16_t *)kv)[src])",
+                              "dst[e] = kv_dtype == 1 ? bf16_to_double(((const uint16_t *)kv)"
+                              "[src - (size_t)p * cf->head_dim - (size_t)e + (size_t)e * (size_t)len + (size_t)p])"),
 }
 
 
@@ -118,6 +126,10 @@ def _pins_hold(lib_path) -> bool:
                         return False
                     i += kk
                     emitted += nn + 1
+        # loading an externally filled cache
+        from tests import test_oracle as O
+
+        O.check_cache_load(lib_path)
         # adaptive draft exit (the pins of test_oracle_adaptive.py)
         from tests import test_oracle_adaptive as A
 

@@ -19,10 +19,13 @@ import torch
 import torch.nn.functional as F
 
 
-def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0, hide_key=None):
+def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0, hide_key=None, kv_out=None):
     """Logits [T, vocab] (float64) of a causal forward over tokens.  hide_key
     (a row index) removes that key from every other row's attention, a planted
-    mistake for measuring how far logits move when attention loses a key."""
+    mistake for measuring how far logits move when attention loses a key.
+    kv_out (a list): receives one (k, v) pair per layer, float64 arrays
+    [T, n_kv_heads, head_dim], k rotated, both rounded to bf16 values for a
+    bf16 model (what a KV cache holds)."""
     tok = torch.as_tensor(np.asarray(tokens, dtype=np.int64))
     T = tok.numel()
     n_full = T if (skip is None or n_full is None) else n_full
@@ -60,6 +63,8 @@ def forward(cfg, w64, tokens, skip=None, n_full=None, start_pos=0, hide_key=None
             if cfg.dtype == "bf16":  # the KV cache of a bf16 model holds bf16 values
                 k = k.to(torch.bfloat16).to(torch.float64)
                 v = v.to(torch.bfloat16).to(torch.float64)
+            if kv_out is not None:
+                kv_out.append((k.numpy().copy(), v.numpy().copy()))
             k = k.repeat_interleave(grp, dim=1)
             v = v.repeat_interleave(grp, dim=1)
             if hide_key is None:
