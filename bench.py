@@ -126,19 +126,101 @@ def prefill_roofline(cfg, M: int, ms: float):
             "frac_issued": round(3 * useful / MFMA_BF16_PEAK_TFLOPS, 4)}
 
 
-def cpu_baseline(cfg, weights, prompt, wl, skip, sample_prompt=16, sample_new=4):
+def host_cpu() -> dict:
+    """The host the oracle runs on: CPU model, logical CPUs, OpenMP setting."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(), "omp_num_threads_env": os.environ.get("OMP_NUM_THREADS")}
+
+
+def oracle_decode_rates(cfg, weights, prompt, wl, skip, prefix=8, n_tokens=4) -> dict:
+    """The oracle at the workload's model shape, decode separated from prefill.
+
+    The prefill of prompt[:prefix] is timed alone; each generate call
+    (prefill + n_tokens) is timed whole and the prefill time subtracted,
+    which leaves the decode-only time of n_tokens greedy autoregressive
+    tokens and of n_tokens self-speculative tokens (same mask, K_max and
+    gamma).  The oracle's per-token cost is its weight passes (one float64
+    matrix-vector product per weight), so a short context stands in for the
+    workload's: attention over the workload's mean context adds
+    2 * ctx * n_kv_heads * head_dim multiply-adds per attention sublayer,
+    reported as attn_share_at_workload_ctx."""
     import oracle
 
     om = oracle.Model(cfg, weights)
-    pr = prompt[:sample_prompt]
+    pr = np.asarray(prompt[:prefix], np.int32)
+    c = om.cache(prefix)
     t0 = time.perf_counter()
-    om.generate_sd(pr, sample_new, skip, wl.k_max, wl.gamma)
-    dt = time.perf_counter() - t0
+    om.forward(c, pr[:-1], want_logits=False)
+    t_pf = time.perf_counter() - t0
+    del c
+    t0 = time.perf_counter()
+    om.generate_ar(pr, n_tokens)
+    t_ar = time.perf_counter() - t0 - t_pf
+    t0 = time.perf_counter()
+    sd = om.generate_sd(pr, n_tokens, skip, wl.k_max, wl.gamma)
+    t_sd = time.perf_counter() - t0 - t_pf
+    d, L = cfg.d_model, cfg.n_layers
+    macs_w = cfg.param_count() - cfg.vocab * d  # the embedding is gathered
+    ctx = wl.prompt_len + wl.max_new / 2
+    macs_attn = L * 2 * ctx * cfg.n_heads * cfg.head_dim
     return {
-        "value": round(sample_new / dt, 4), "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-        "sample": (f"oracle self-speculative decode of {sample_new} tokens after the first {sample_prompt} prompt "
-                   f"tokens (prefill included), same model, mask, K_max and gamma; {dt:.1f} s"),
+        "sd_tokens_per_s": round(n_tokens / t_sd, 4), "ar_tokens_per_s": round(n_tokens / t_ar, 4),
+        "prefill_s": round(t_pf, 3), "prefill_rows": int(prefix - 1), "decode_tokens": n_tokens,
+        "sd_stages": int(sd["n_stages"]), "sd_drafted": int(sd["n_drafted"]),
+        "context": f"{prefix - 1}..{prefix - 2 + n_tokens} positions",
+        "attn_share_at_workload_ctx": round(macs_attn / (macs_w + macs_attn), 4),
+        "threads": oracle.num_threads(), "seconds": round(t_pf * 3 + t_ar + t_sd, 1),
     }
+
+
+def cpu_baseline(cfg, weights, prompt, wl, skip):
+    r = oracle_decode_rates(cfg, weights, prompt, wl, skip)
+    return {
+        "value": r["sd_tokens_per_s"], "unit": "tokens/s", "cores": r["threads"], "kind": "oracle",
+        "sample": (f"oracle decode-only tokens/s of the {cfg.name} model ({wl.mask}, K_max {wl.k_max}, gamma "
+                   f"{wl.gamma}): {r['decode_tokens']} self-speculative and {r['decode_tokens']} autoregressive "
+                   f"tokens after a {r['prefill_rows'] + 1}-token prefix of the workload's prompt (context "
+                   f"{r['context']}); prefill of {r['prefill_rows']} rows timed alone and reported apart; "
+                   f"{r['seconds']} s of CPU work"),
+        "ar_value": r["ar_tokens_per_s"], "prefill_s": r["prefill_s"], "prefill_rows": r["prefill_rows"],
+        "attn_share_at_workload_ctx": r["attn_share_at_workload_ctx"], **host_cpu(),
+    }
+
+
+def run_cpu_table(args):
+    """Oracle decode rates per workload on this host, with every OpenMP
+    thread and with one thread (tiny and 7B), each in a child process so
+    that OMP_NUM_THREADS takes effect.  One JSON line."""
+    import subprocess
+
+    rows = []
+    for name, threads in (("tiny", None), ("tiny", 1), ("7b", None), ("7b", 1), ("13b", None)):
+        env = dict(os.environ)
+        if threads:
+            env["OMP_NUM_THREADS"] = str(threads)
+        out = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-rates-child", name],
+                             env=env, capture_output=True, text=True, check=True).stdout
+        r = json.loads(out.strip().splitlines()[-1])
+        log(f"oracle {name} x {r['threads']} threads: SD {r['sd_tokens_per_s']} tok/s, AR {r['ar_tokens_per_s']} tok/s")
+        rows.append({"workload": name, **r})
+    print(json.dumps({"mode": "cpu-table", "kind": "oracle", **host_cpu(), "rows": rows}), flush=True)
+
+
+def run_cpu_rates_child(name):
+    wl = S.WORKLOADS[name]
+    cfg = S.MODELS[wl.model]
+    w = S.make_weights(cfg, 0)
+    pr = S.prompt(cfg, wl.prompt_len, 0)
+    z = S.skip_mask(cfg, wl.mask, 0)
+    kw = {"prefix": 8, "n_tokens": 16} if name == "tiny" else {"prefix": 4, "n_tokens": 2}
+    print(json.dumps(oracle_decode_rates(cfg, w, pr, wl, z, **kw)), flush=True)
 
 
 def load_model(cfg, seed):
@@ -727,6 +809,9 @@ def main():
     ap.add_argument("--max-new", type=int, default=None, help="override the workload's generated tokens")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-table", action="store_true",
+                    help="oracle decode rates on this host per workload, all threads and one thread")
+    ap.add_argument("--cpu-rates-child", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--no-ar", action="store_true", help="skip the autoregressive comparison")
     ap.add_argument("--verify-micro", action="store_true")
     ap.add_argument("--micro-rows", default="1,4,8,13,16")
@@ -764,6 +849,10 @@ def main():
         return run_summarize_pmc(args)
     if args.summarize_step_counters:
         return run_summarize_step_counters(args)
+    if args.cpu_rates_child:
+        return run_cpu_rates_child(args.cpu_rates_child)
+    if args.cpu_table:
+        return run_cpu_table(args)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: --gpus {args.gpus} is not supported (the decode path is "
               "batch-1 on a single MI355X; independent requests would run one model copy per GPU)", file=sys.stderr)

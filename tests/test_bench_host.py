@@ -138,3 +138,15 @@ def test_more_than_one_gpu_is_refused_before_touching_a_device():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_cpu_baseline_reports_decode_rates_and_the_host():
+    """The oracle baseline separates prefill from decode and names the host."""
+    wl = S.WORKLOADS["tiny"]
+    cfg = S.MODELS["tiny"]
+    w = S.make_weights(cfg, 0)
+    r = bench.cpu_baseline(cfg, w, S.prompt(cfg, wl.prompt_len), wl, S.skip_mask(cfg, wl.mask))
+    assert r["kind"] == "oracle" and r["unit"] == "tokens/s" and r["value"] > 0 and r["ar_value"] > 0
+    assert r["prefill_rows"] == 7 and r["prefill_s"] >= 0
+    assert r["cores"] >= 1 and r["nproc"] == os.cpu_count() and "cpu_model" in r
+    assert 0 < r["attn_share_at_workload_ctx"] < 1
