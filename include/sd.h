@@ -152,6 +152,24 @@ sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len);
 sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
                      sd_kv_cache *cache, float *logits);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * forward as sd_forward for n <= 16 rows, with identical results, calling no
+ * hipMalloc, hipFree or other allocating routine and copying nothing from
+ * host memory (the tokens travel as a kernel argument).  Its scratch
+ * (activations, split partials, attention partials, lm-head partials, the
+ * control block) lives in a static device array of 32 MiB that each GPU the
+ * library runs on holds until the process ends; a model and cache capacity
+ * that need more (about 16 MiB at the 13B shape over 4096 positions, 30 MiB
+ * at the 70B shape) are refused.  Every call on one GPU shares that GPU's
+ * array: calls that overlap on one GPU (other streams, other threads, other
+ * models) race and must not be made.  The model's workspace and the cache
+ * are the caller's, created beforehand (those calls allocate); the call
+ * waits for its stream like sd_forward.  Errors: INVALID_ARG (also n > 16),
+ * CAPACITY (cache full, or scratch above 32 MiB; nothing enqueued), DEVICE. */
+sd_status sd_forward_static(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
+                            sd_kv_cache *cache, float *logits);
+
 /* Greedy self-speculative decoding (Algorithm 2, static gamma exit of
  * Sec. 3.4) of max_new tokens after a HOST prompt of prompt_len >= 1 ids.
  * The prompt minus its last token is prefilled; every stage drafts at

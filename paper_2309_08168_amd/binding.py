@@ -22,7 +22,7 @@ SD_F32, SD_BF16 = 0, 1
 # Every entry point declared in include/sd.h.
 EXPORTS = (
     "sd_model_create", "sd_model_destroy", "sd_kv_cache_bytes", "sd_kv_cache_create", "sd_kv_cache_destroy",
-    "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward",
+    "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward", "sd_forward_static",
     "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
     "sd_self_spec_sample", "sd_autoregressive_sample", "sd_search_skip_set_fn", "sd_search_skip_set",
     "sd_model_time_kernel", "sd_model_kernel_time",
@@ -124,6 +124,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_kv_cache_truncate": ([vp, i32], ctypes.c_int),
         "sd_kv_cache_set_length": ([vp, i32], ctypes.c_int),
         "sd_forward": ([vp, vp, i32, vp, vp, vp], ctypes.c_int),
+        "sd_forward_static": ([vp, vp, i32, vp, vp, vp], ctypes.c_int),
         "sd_self_spec_generate": ([vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(sd_stats)], ctypes.c_int),
         "sd_self_spec_generate_adaptive": ([vp, vp, i32, i32, vp, i32, p(sd_adaptive), vp, p(sd_stats)],
                                            ctypes.c_int),
@@ -259,6 +260,15 @@ class Model:
         sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
         lp = None if logits is None else ctypes.c_void_p(logits.data_ptr())
         check(load().sd_forward(self._h, _ptr(tok), tok.size, _ptr(sk), cache._h, lp))
+        return logits
+
+    def forward_static(self, tokens, cache: "KVCache", skip=None, logits=None):
+        """sd_forward_static: sd_forward for up to 16 rows, its scratch in the
+        library's static device array (no allocation)."""
+        tok = np.ascontiguousarray(tokens, dtype=np.int32)
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        lp = None if logits is None else ctypes.c_void_p(logits.data_ptr())
+        check(load().sd_forward_static(self._h, _ptr(tok), tok.size, _ptr(sk), cache._h, lp))
         return logits
 
     def _sd_call(self, fn, prompt, max_new, skip, k_max, rule, log_cap):

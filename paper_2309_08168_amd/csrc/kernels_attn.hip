@@ -906,6 +906,32 @@ hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *de
     return hipGetLastError();
 }
 
+// The control block from host values passed by value (no copy from host
+// memory): up to MAX_ROWS tokens.
+struct CtlTokens {
+    int32_t t[MAX_ROWS];
+};
+
+__global__ void k_set_ctl_value(DevCtl *ctl, int32_t pos, int32_t m, CtlTokens tokens) {
+    const int i = threadIdx.x;
+    if (i == 0) {
+        ctl->pos = pos;
+        ctl->m = m;
+    }
+    if (i < m)
+        ctl->tokens[i] = tokens.t[i];
+}
+
+hipError_t launch_set_ctl_host(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *host_tokens, hipStream_t s) {
+    if (m < 1 || m > MAX_ROWS)
+        return hipErrorInvalidValue;
+    CtlTokens t{};
+    for (int i = 0; i < m; ++i)
+        t.t[i] = host_tokens[i];
+    hipLaunchKernelGGL(k_set_ctl_value, dim3(1), dim3(64), 0, s, ctl, pos, m, t);
+    return hipGetLastError();
+}
+
 // State at the start of decoding: the cache holds the prompt minus its last
 // token; the first stage drafts from that last token.
 __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *last,

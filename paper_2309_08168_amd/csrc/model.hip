@@ -11,6 +11,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -66,6 +67,26 @@ struct Plan {
     int N, K, epi;
 };
 
+// Scratch of one decode-path forward (up to MAX_ROWS rows): the residual
+// stream, the attention and MLP activations, split-K and attention
+// partials, the lm-head partials and the control block.  A model owns one
+// (allocated at creation); the allocation-free forward carves another out
+// of a static device array.
+struct Workspace {
+    float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
+    float *part = nullptr;  // split-K partials of the MFMA output projections
+    float *ssq = nullptr;   // sums of h^2 per row and slice for the next normed MFMA layer
+    // MFMA-path activations split into X_TERMS bf16 terms in fragment layout
+    // (48 xld elements each): xa holds normalised inputs and the attention
+    // output, xb the SwiGLU output.
+    uint16_t *xa = nullptr, *xb = nullptr;
+    int64_t xld = 0;
+    float4 *head_part = nullptr;
+    float *attn_o = nullptr;    // [splits][n_heads][MAX_ROWS][head_dim]
+    float2 *attn_ml = nullptr;  // [splits][n_heads][MAX_ROWS]
+    DevCtl *ctl = nullptr;
+};
+
 }  // namespace
 
 struct sd_kv_cache {
@@ -87,24 +108,14 @@ struct sd_model {
     Plan plan1[LK_COUNT];  // one row (draft / autoregressive step)
     Plan plan2[LK_COUNT];  // up to 2 rows (verification of one draft)
     Plan planm[LK_COUNT];  // up to 16 rows (longer verification, prefill)
-    float *part = nullptr;  // split-K partials of the MFMA output projections
-    float *ssq = nullptr;   // sums of h^2 per row and slice for the next normed MFMA layer
-
-    float *h = nullptr, *q = nullptr, *o = nullptr, *mbuf = nullptr;
-    // MFMA-path activations split into X_TERMS bf16 terms in fragment layout
-    // (48 xld elements each): xa holds normalised inputs and the attention
-    // output, xb the SwiGLU output.
-    uint16_t *xa = nullptr, *xb = nullptr;
-    int64_t xld = 0;
-    float4 *head_part = nullptr;
+    Workspace ws;           // scratch of the decode-path forwards
+    int max_head_tiles = 1; // lm-head tiles of the widest plan
     // sampling variant: logits of the verification / autoregressive rows and
     // of the stage's drafts, the rows' nucleus statistics, the parameters
     float *slog_v = nullptr, *slog_d = nullptr;
     RowStat *svstat = nullptr, *sdstat = nullptr;
     SampleParams sp_cur{};
-    float *attn_o = nullptr;
-    float2 *attn_ml = nullptr;
-    int attn_splits_cap = 0;
+    int attn_splits_cap = 0;  // key chunks ws.attn_o / ws.attn_ml hold
     float2 *rope = nullptr;
     int rope_cap = 0;
     // large-M forward (bfloat16 models): residual stream, GEMM output,
@@ -113,7 +124,6 @@ struct sd_model {
     float *pf_h = nullptr, *pf_c = nullptr, *pf_q = nullptr, *pf_part = nullptr;
     uint16_t *pf_x = nullptr;
     int64_t pf_term = 0;
-    DevCtl *ctl = nullptr;
     DevState *st = nullptr;
     Mailbox *mb_host = nullptr;
     Mailbox *mb_dev = nullptr;
@@ -142,6 +152,11 @@ struct sd_model {
 namespace {
 
 int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Elements per term of the MFMA-path activation buffers (xa, xb).
+int64_t xld_of(const sd_config &c) {
+    return std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
+}
 
 // Tile rows for the QKV layer must hold whole rotary pairs of one head.
 int qkv_gemv_rows(int head_dim, int want) {
@@ -313,10 +328,10 @@ sd_status ensure_attn(sd_model *m, int cap) {
         dev_free(po);
         return SD_ERR_OOM;
     }
-    dev_free(m->attn_o);
-    dev_free(m->attn_ml);
-    m->attn_o = po;
-    m->attn_ml = pml;
+    dev_free(m->ws.attn_o);
+    dev_free(m->ws.attn_ml);
+    m->ws.attn_o = po;
+    m->ws.attn_ml = pml;
     m->attn_splits_cap = splits;
     return SD_OK;
 }
@@ -344,8 +359,8 @@ sd_status launch(hipError_t e, const char *what) {
 // gain folded in by the VALU kernels) feeds the VALU paths; the MFMA path
 // reads the bf16 term planes xs (g * h from k_prep_norm, the layer dividing
 // by rms(h) itself, or split by the producer for the output projections).
-sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, const float *X, int64_t ldx,
-                     const void *gain, const EpiArgs &epi, const uint16_t *xs) {
+sd_status run_linear(sd_model *m, const Workspace &w, const Plan &p, int max_rows, const void *W, const float *X,
+                     int64_t ldx, const void *gain, const EpiArgs &epi, const uint16_t *xs) {
     LinearArgs a{};
     a.W = W;
     a.N = p.N;
@@ -354,7 +369,7 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
         a.Xs = xs;
         a.max_rows = max_rows;
         if (gain) {  // the fragments hold g * h; 1/rms(h) from the slices' sums
-            a.ssq = m->ssq;
+            a.ssq = w.ssq;
             a.ssq_slices = prep_slices(p.K);
         }
     } else {
@@ -363,11 +378,11 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
         a.gain = gain;
     }
     a.eps = m->cfg.rms_eps;
-    a.ctl = m->ctl;
+    a.ctl = w.ctl;
     a.epi = epi;
     a.waves = p.waves;
     a.splits = p.splits;
-    a.part = m->part;
+    a.part = w.part;
     a.n_tiles = p.n_tiles;
     const bool timed = m->timed_now && p.kind == m->timed_kind && p.regime == m->timed_regime &&
                        m->tev_used + 2 <= 2 * 65536;
@@ -394,7 +409,7 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
         SampleArgs sa{};
         sa.sp = m->sp_cur;
         sa.vocab = m->cfg.vocab;
-        sa.ctl = m->ctl;
+        sa.ctl = w.ctl;
         sa.vlog = m->slog_v;
         sa.dlog = m->slog_d;
         sa.vstat = m->svstat;
@@ -410,10 +425,10 @@ sd_status run_linear(sd_model *m, const Plan &p, int max_rows, const void *W, co
 // The MFMA operand of a normed layer into xa (MFMA path only), after folding
 // the pending split-K partials of the last output projection: g * h, with
 // the sums of h^2 per slice in ssq for the layer's 1/rms(h).
-sd_status prep_norm(sd_model *m, const Plan &p, const void *gain, int &pending) {
+sd_status prep_norm(sd_model *m, const Workspace &w, const Plan &p, const void *gain, int &pending) {
     if (p.path != PATH_MFMA)
         return SD_OK;
-    SD_TRY(launch(launch_prep_norm(m->h, m->cfg.d_model, gain, m->bf16, p.K, m->ctl, m->xa, m->part, pending, m->ssq,
+    SD_TRY(launch(launch_prep_norm(w.h, m->cfg.d_model, gain, m->bf16, p.K, w.ctl, w.xa, w.part, pending, w.ssq,
                                    m->stream),
                   "norm"));
     pending = 0;
@@ -430,7 +445,7 @@ struct HeadSpec {
 // One decoder forward over the rows described by the device control block.
 // max_rows (known to the host) bounds the row count and picks the kernels;
 // skip is a host mask or null.
-sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
+sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
                           const HeadSpec &hs) {
     const sd_config &c = m->cfg;
     const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
@@ -443,13 +458,13 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
-    SD_TRY(launch(launch_embed(m->tok_emb, m->bf16, c.d_model, m->ctl, m->h, ldh, m->stream), "embedding"));
+    SD_TRY(launch(launch_embed(m->tok_emb, m->bf16, c.d_model, w.ctl, w.h, ldh, m->stream), "embedding"));
     for (int l = 0; l < c.n_layers; ++l) {
         if (!(skip && skip[2 * l])) {
             char *kbase = static_cast<char *>(kv) + (size_t)(2 * l) * c.n_kv_heads * head_stride * ksz;
             char *vbase = static_cast<char *>(kv) + (size_t)(2 * l + 1) * c.n_kv_heads * head_stride * ksz;
             EpiArgs e{};
-            e.q = m->q;
+            e.q = w.q;
             e.ld_q = ldq;
             e.kcache = kbase;
             e.vcache = vbase;
@@ -459,50 +474,50 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             e.n_kv_heads = c.n_kv_heads;
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
-            SD_TRY(prep_norm(m, P[LK_QKV], m->attn_norm[l], pending));
-            SD_TRY(run_linear(m, P[LK_QKV], max_rows, m->w_qkv[l], m->h, ldh, m->attn_norm[l], e, m->xa));
+            SD_TRY(prep_norm(m, w, P[LK_QKV], m->attn_norm[l], pending));
+            SD_TRY(run_linear(m, w, P[LK_QKV], max_rows, m->w_qkv[l], w.h, ldh, m->attn_norm[l], e, w.xa));
             AttnArgs at{};
-            at.q = m->q;
+            at.q = w.q;
             at.ld_q = ldq;
             at.kcache = kbase;
             at.vcache = vbase;
             at.kv_head_stride = head_stride;
-            at.part_o = m->attn_o;
-            at.part_ml = m->attn_ml;
-            at.out = m->o;
+            at.part_o = w.attn_o;
+            at.part_ml = w.attn_ml;
+            at.out = w.o;
             at.ld_out = ldq;
             if (P[LK_O].path == PATH_MFMA) {
-                at.out_x = m->xa;
-                at.ld_out = m->xld;
+                at.out_x = w.xa;
+                at.ld_out = w.xld;
             }
             at.n_heads = c.n_heads;
             at.n_kv_heads = c.n_kv_heads;
             at.head_dim = c.head_dim;
             at.splits = cdiv(cap, ATTN_CHUNK);
-            at.ctl = m->ctl;
+            at.ctl = w.ctl;
             SD_TRY(launch(launch_attention(at, m->bf16, max_rows, m->stream), "attention"));
             EpiArgs eo{};
-            eo.out = m->h;
+            eo.out = w.h;
             eo.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_O], max_rows, m->w_o[l], m->o, ldq, nullptr, eo, m->xa));
+            SD_TRY(run_linear(m, w, P[LK_O], max_rows, m->w_o[l], w.o, ldq, nullptr, eo, w.xa));
             if (P[LK_O].epi == EPI_PARTIAL)
                 pending = P[LK_O].splits;
         }
         if (!(skip && skip[2 * l + 1])) {
             EpiArgs eg{};
-            eg.out = m->mbuf;
+            eg.out = w.mbuf;
             eg.ld_out = c.ffn_dim;
             eg.ffn = c.ffn_dim;
             if (P[LK_DOWN].path == PATH_MFMA) {
-                eg.out_x = m->xb;
-                eg.ld_out = m->xld;
+                eg.out_x = w.xb;
+                eg.ld_out = w.xld;
             }
-            SD_TRY(prep_norm(m, P[LK_GATE_UP], m->mlp_norm[l], pending));
-            SD_TRY(run_linear(m, P[LK_GATE_UP], max_rows, m->w_gate_up[l], m->h, ldh, m->mlp_norm[l], eg, m->xa));
+            SD_TRY(prep_norm(m, w, P[LK_GATE_UP], m->mlp_norm[l], pending));
+            SD_TRY(run_linear(m, w, P[LK_GATE_UP], max_rows, m->w_gate_up[l], w.h, ldh, m->mlp_norm[l], eg, w.xa));
             EpiArgs ed{};
-            ed.out = m->h;
+            ed.out = w.h;
             ed.ld_out = ldh;
-            SD_TRY(run_linear(m, P[LK_DOWN], max_rows, m->w_down[l], m->mbuf, c.ffn_dim, nullptr, ed, m->xb));
+            SD_TRY(run_linear(m, w, P[LK_DOWN], max_rows, m->w_down[l], w.mbuf, c.ffn_dim, nullptr, ed, w.xb));
             if (P[LK_DOWN].epi == EPI_PARTIAL)
                 pending = P[LK_DOWN].splits;
         }
@@ -512,7 +527,7 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
         eh.head.mode = hs.mode;
         eh.head.logits = hs.logits;
         eh.head.ld_logits = c.vocab;
-        eh.head.partials = m->head_part;
+        eh.head.partials = w.head_part;
         eh.head.st = m->st;
         eh.head.mb = m->mb_dev;
         eh.head.out_tokens = m->d_out;
@@ -524,8 +539,8 @@ sd_status enqueue_forward(sd_model *m, void *kv, int32_t cap, const uint8_t *ski
             eh.head.logits = hs.mode == HEAD_DRAFT ? m->slog_d : m->slog_v;
             eh.head.logits_by_draft = hs.mode == HEAD_DRAFT;
         }
-        SD_TRY(prep_norm(m, P[LK_HEAD], m->final_norm, pending));
-        SD_TRY(run_linear(m, P[LK_HEAD], max_rows, m->lm_head, m->h, ldh, m->final_norm, eh, m->xa));
+        SD_TRY(prep_norm(m, w, P[LK_HEAD], m->final_norm, pending));
+        SD_TRY(run_linear(m, w, P[LK_HEAD], max_rows, m->lm_head, w.h, ldh, m->final_norm, eh, w.xa));
     }
     return SD_OK;
 }
@@ -713,8 +728,8 @@ sd_status enqueue_prefill(sd_model *m, sd_kv_cache *kc, const int32_t *dev_token
     }
     for (int32_t c = 0; c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
-        SD_TRY(launch(launch_set_ctl(m->ctl, start + c, rows, dev_tokens + c, m->stream), "control block"));
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, rows, HeadSpec{}));
+        SD_TRY(launch(launch_set_ctl(m->ws.ctl, start + c, rows, dev_tokens + c, m->stream), "control block"));
+        SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, nullptr, rows, HeadSpec{}));
     }
     return SD_OK;
 }
@@ -835,7 +850,7 @@ sd_status start_generate(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     m->gen_cache->len = prompt_len - 1;
     SD_HIP(hipEventRecord(m->ev[1], m->stream));
     __atomic_store_n(&m->mb_host->word, mb_pack(-1, 0, 0, 0), __ATOMIC_RELEASE);
-    SD_TRY(launch(launch_init_decode(m->st, m->ctl, m->mb_dev, prompt_len - 1, m->d_tokens + prompt_len - 1,
+    SD_TRY(launch(launch_init_decode(m->st, m->ws.ctl, m->mb_dev, prompt_len - 1, m->d_tokens + prompt_len - 1,
                                      max_new, k_max, rule, m->stream),
                   "decode setup"));
     return SD_OK;
@@ -889,11 +904,11 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
         hs.sampled = sp != nullptr;
         if (phase == PHASE_DRAFT) {
             hs.mode = HEAD_DRAFT;
-            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, 1, hs));
+            SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, skip, 1, hs));
             ++stage_k;
         } else {
             hs.mode = HEAD_VERIFY;
-            SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, stage_k + 1, hs));
+            SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, nullptr, stage_k + 1, hs));
             stage_k = 0;
         }
         SD_HIP(hipEventRecord(e1, m->stream));
@@ -937,7 +952,7 @@ sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len,
     hs.mode = HEAD_AR;
     hs.sampled = sp != nullptr;
     for (int32_t i = 0; i < max_new; ++i)
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, nullptr, 1, hs));
+        SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, nullptr, 1, hs));
     SD_HIP(hipEventRecord(m->ev[2], m->stream));
     SD_TRY(copy_results(m, max_new, out_tokens, stats));
     if (stats) {
@@ -973,15 +988,130 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
                                      kc->len + c, logits ? logits + (size_t)c * m->cfg.vocab : nullptr));
     for (int32_t c = 0; !(m->pf_ok && n > MAX_ROWS) && c < n; c += MAX_ROWS) {
         const int32_t rows = std::min<int32_t>(MAX_ROWS, n - c);
-        SD_TRY(launch(launch_set_ctl(m->ctl, kc->len + c, rows, m->d_tokens + c, m->stream), "control block"));
+        SD_TRY(launch(launch_set_ctl(m->ws.ctl, kc->len + c, rows, m->d_tokens + c, m->stream), "control block"));
         HeadSpec hs;
         hs.run = logits != nullptr;
         hs.mode = HEAD_NONE;
         hs.logits = logits ? logits + (size_t)c * m->cfg.vocab : nullptr;
-        SD_TRY(enqueue_forward(m, kc->buf, kc->cap, skip, rows, hs));
+        SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, skip, rows, hs));
     }
     SD_HIP(hipStreamSynchronize(m->stream));
     collect_timing(m);
+    kc->len += n;
+    return SD_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Allocation-free forward (sd_forward_static).  Its scratch lives in this
+// file-scope device array: each GPU the library runs on holds its own copy
+// until the process ends.  Host code never passes the array's name to a
+// kernel (on the host it only names a stand-in): the device address comes
+// from hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t STATIC_SCRATCH_BYTES = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+char *g_scratch[MAX_SCRATCH_DEVICES] = {};
+
+// Device address of the scratch array on the device of stream s.
+sd_status scratch_base(hipStream_t s, char **out) {
+    int cur = -1;
+    SD_HIP(hipGetDevice(&cur));
+    int dev = cur;
+    if (s)
+        SD_HIP(hipStreamGetDevice(s, &dev));
+    if (dev < 0 || dev >= MAX_SCRATCH_DEVICES)
+        return fail(SD_ERR_DEVICE, "device index " + std::to_string(dev) + " out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        if (dev != cur)
+            SD_HIP(hipSetDevice(dev));
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (dev != cur)
+            (void)hipSetDevice(cur);
+        if (e != hipSuccess || !p)
+            return fail(SD_ERR_DEVICE, std::string("scratch address: ") + hipGetErrorString(e));
+        g_scratch[dev] = static_cast<char *>(p);
+    }
+    *out = g_scratch[dev];
+    return SD_OK;
+}
+
+// Lays out a forward's scratch for model m over a cache of capacity cap at
+// base (or only sizes it when base is null); returns the bytes used.  Every
+// buffer starts on a 256-byte boundary.
+size_t carve_workspace(const sd_model *m, int32_t cap, char *base, Workspace *w) {
+    const sd_config &c = m->cfg;
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char * {
+        char *p = base ? base + off : nullptr;
+        off += (bytes + 255) & ~(size_t)255;
+        return p;
+    };
+    const size_t hd = (size_t)c.n_heads * c.head_dim, splits = (size_t)cdiv(cap, ATTN_CHUNK);
+    w->xld = xld_of(c);
+    w->h = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * c.d_model));
+    w->q = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * hd));
+    w->o = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * hd));
+    w->mbuf = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * c.ffn_dim));
+    w->part = reinterpret_cast<float *>(take(sizeof(float) * 8 * MAX_ROWS * c.d_model));
+    w->ssq = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * prep_slices(c.d_model)));
+    w->xa = reinterpret_cast<uint16_t *>(take(sizeof(uint16_t) * X_TERMS * MAX_ROWS * w->xld));
+    w->xb = reinterpret_cast<uint16_t *>(take(sizeof(uint16_t) * X_TERMS * MAX_ROWS * w->xld));
+    w->head_part = reinterpret_cast<float4 *>(take(sizeof(float4) * m->max_head_tiles * MAX_ROWS));
+    w->attn_o = reinterpret_cast<float *>(take(sizeof(float) * splits * c.n_heads * MAX_ROWS * c.head_dim));
+    w->attn_ml = reinterpret_cast<float2 *>(take(sizeof(float2) * splits * c.n_heads * MAX_ROWS));
+    w->ctl = reinterpret_cast<DevCtl *>(take(sizeof(DevCtl)));
+    return off;
+}
+
+sd_status forward_static(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *skip, sd_kv_cache *kc,
+                         float *logits) {
+    if (!m || !kc)
+        return fail(SD_ERR_INVALID_ARG, "model or cache is null");
+    if (kc->model != m)
+        return fail(SD_ERR_INVALID_ARG, "cache belongs to another model");
+    if (n < 1 || n > MAX_ROWS)
+        return fail(SD_ERR_INVALID_ARG, "n must be in [1, " + std::to_string(MAX_ROWS) + "]");
+    SD_TRY(check_tokens(m, tokens, n, "tokens"));
+    SD_TRY(check_mask(m, skip));
+    if ((int64_t)kc->len + n > kc->cap)
+        return fail(SD_ERR_CAPACITY, "cache of capacity " + std::to_string(kc->cap) + " holds " +
+                                         std::to_string(kc->len) + " positions; " + std::to_string(n) +
+                                         " more do not fit");
+    Workspace w;
+    const size_t need = carve_workspace(m, kc->cap, nullptr, &w);
+    if (need > STATIC_SCRATCH_BYTES)
+        return fail(SD_ERR_CAPACITY, "this model over a cache of " + std::to_string(kc->cap) + " positions needs " +
+                                         std::to_string(need) + " bytes of scratch; the static array holds " +
+                                         std::to_string(STATIC_SCRATCH_BYTES));
+    char *base = nullptr;
+    SD_TRY(scratch_base(m->stream, &base));
+    carve_workspace(m, kc->cap, base, &w);
+    // The array keeps the previous call's contents: the activation rows
+    // start at zero, as a model's own workspace does.
+    SD_TRY(launch(launch_fill_zero(w.h, sizeof(float) * MAX_ROWS * m->cfg.d_model, m->stream), "scratch clear"));
+    SD_TRY(launch(launch_fill_zero(w.o, sizeof(float) * MAX_ROWS * m->cfg.n_heads * m->cfg.head_dim, m->stream),
+                  "scratch clear"));
+    SD_TRY(launch(launch_fill_zero(w.mbuf, sizeof(float) * MAX_ROWS * m->cfg.ffn_dim, m->stream), "scratch clear"));
+    SD_TRY(launch(launch_set_ctl_host(w.ctl, kc->len, n, tokens, m->stream), "control block"));
+    HeadSpec hs;
+    hs.run = logits != nullptr;
+    hs.mode = HEAD_NONE;
+    hs.logits = logits;
+    // the measurement hook's events stay out of this path
+    const int timed = m->timed_kind;
+    m->timed_kind = -1;
+    const sd_status st = enqueue_forward(m, w, kc->buf, kc->cap, skip, n, hs);
+    m->timed_kind = timed;
+    SD_TRY(st);
+    SD_HIP(hipStreamSynchronize(m->stream));
     kc->len += n;
     return SD_OK;
 }
@@ -994,28 +1124,28 @@ void destroy_model(sd_model *m) {
     for (sd_kv_cache *c : m->caches)
         c->model = nullptr;
     destroy_cache(m->gen_cache);
-    dev_free(m->h);
-    dev_free(m->q);
-    dev_free(m->o);
-    dev_free(m->mbuf);
-    dev_free(m->part);
-    dev_free(m->ssq);
-    dev_free(m->xa);
-    dev_free(m->xb);
-    dev_free(m->head_part);
+    dev_free(m->ws.h);
+    dev_free(m->ws.q);
+    dev_free(m->ws.o);
+    dev_free(m->ws.mbuf);
+    dev_free(m->ws.part);
+    dev_free(m->ws.ssq);
+    dev_free(m->ws.xa);
+    dev_free(m->ws.xb);
+    dev_free(m->ws.head_part);
     dev_free(m->slog_v);
     dev_free(m->slog_d);
     dev_free(m->svstat);
     dev_free(m->sdstat);
-    dev_free(m->attn_o);
-    dev_free(m->attn_ml);
+    dev_free(m->ws.attn_o);
+    dev_free(m->ws.attn_ml);
     dev_free(m->rope);
     dev_free(m->pf_h);
     dev_free(m->pf_c);
     dev_free(m->pf_q);
     dev_free(m->pf_part);
     dev_free(m->pf_x);
-    dev_free(m->ctl);
+    dev_free(m->ws.ctl);
     dev_free(m->st);
     dev_free(m->d_tokens);
     dev_free(m->d_out);
@@ -1081,21 +1211,23 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
         if (st == SD_OK)
             st = s;
     };
-    chain(dev_alloc(&m->h, (size_t)MAX_ROWS * c.d_model));
-    chain(dev_alloc(&m->q, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
-    chain(dev_alloc(&m->o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
-    chain(dev_alloc(&m->mbuf, (size_t)MAX_ROWS * c.ffn_dim));
-    chain(dev_alloc(&m->part, (size_t)8 * MAX_ROWS * c.d_model));
-    chain(dev_alloc(&m->ssq, (size_t)MAX_ROWS * prep_slices(c.d_model)));
-    m->xld = std::max<int64_t>({c.d_model, (int64_t)c.n_heads * c.head_dim, c.ffn_dim});
-    chain(dev_alloc(&m->xa, (size_t)X_TERMS * MAX_ROWS * m->xld));
-    chain(dev_alloc(&m->xb, (size_t)X_TERMS * MAX_ROWS * m->xld));
-    chain(dev_alloc(&m->head_part, (size_t)max_head_tiles * MAX_ROWS));
+    Workspace &ws = m->ws;
+    m->max_head_tiles = max_head_tiles;
+    chain(dev_alloc(&ws.h, (size_t)MAX_ROWS * c.d_model));
+    chain(dev_alloc(&ws.q, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
+    chain(dev_alloc(&ws.o, (size_t)MAX_ROWS * c.n_heads * c.head_dim));
+    chain(dev_alloc(&ws.mbuf, (size_t)MAX_ROWS * c.ffn_dim));
+    chain(dev_alloc(&ws.part, (size_t)8 * MAX_ROWS * c.d_model));
+    chain(dev_alloc(&ws.ssq, (size_t)MAX_ROWS * prep_slices(c.d_model)));
+    ws.xld = xld_of(c);
+    chain(dev_alloc(&ws.xa, (size_t)X_TERMS * MAX_ROWS * ws.xld));
+    chain(dev_alloc(&ws.xb, (size_t)X_TERMS * MAX_ROWS * ws.xld));
+    chain(dev_alloc(&ws.head_part, (size_t)max_head_tiles * MAX_ROWS));
     chain(dev_alloc(&m->slog_v, (size_t)MAX_ROWS * c.vocab));
     chain(dev_alloc(&m->slog_d, (size_t)MAX_ROWS * c.vocab));
     chain(dev_alloc(&m->svstat, (size_t)MAX_ROWS));
     chain(dev_alloc(&m->sdstat, (size_t)MAX_ROWS));
-    chain(dev_alloc(&m->ctl, 1));
+    chain(dev_alloc(&ws.ctl, 1));
     chain(dev_alloc(&m->st, 1));
     m->pf_ok = m->bf16 && (c.head_dim == 32 || c.head_dim == 64 || c.head_dim == 128);
     if (m->pf_ok) {
@@ -1130,9 +1262,9 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
         }
     // activations start at zero (rows beyond the current forward are read
     // as zeros by the 16-row kernels' padding lanes only through masks)
-    if (hipMemsetAsync(m->h, 0, sizeof(float) * (size_t)MAX_ROWS * c.d_model, m->stream) != hipSuccess ||
-        hipMemsetAsync(m->mbuf, 0, sizeof(float) * (size_t)MAX_ROWS * c.ffn_dim, m->stream) != hipSuccess ||
-        hipMemsetAsync(m->o, 0, sizeof(float) * (size_t)MAX_ROWS * c.n_heads * c.head_dim, m->stream) !=
+    if (hipMemsetAsync(ws.h, 0, sizeof(float) * (size_t)MAX_ROWS * c.d_model, m->stream) != hipSuccess ||
+        hipMemsetAsync(ws.mbuf, 0, sizeof(float) * (size_t)MAX_ROWS * c.ffn_dim, m->stream) != hipSuccess ||
+        hipMemsetAsync(ws.o, 0, sizeof(float) * (size_t)MAX_ROWS * c.n_heads * c.head_dim, m->stream) !=
             hipSuccess ||
         hipStreamSynchronize(m->stream) != hipSuccess) {
         destroy_model(m);
@@ -1243,6 +1375,11 @@ sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len) {
 sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
                      sd_kv_cache *cache, float *logits) {
     SD_GUARD(return forward(model, tokens, n, skip_mask, cache, logits);)
+}
+
+sd_status sd_forward_static(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
+                            sd_kv_cache *cache, float *logits) {
+    SD_GUARD(return forward_static(model, tokens, n, skip_mask, cache, logits);)
 }
 
 sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,

@@ -313,6 +313,8 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
 hipError_t launch_embed(const void *emb, bool bf16, int d, const DevCtl *ctl, float *h, int64_t ldh,
                         hipStream_t s);
 hipError_t launch_set_ctl(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *dev_tokens, hipStream_t s);
+// The same from m <= MAX_ROWS host tokens, passed as a kernel argument.
+hipError_t launch_set_ctl_host(DevCtl *ctl, int32_t pos, int32_t m, const int32_t *host_tokens, hipStream_t s);
 // Threshold rule of a generate call: fixed gamma (adaptive = 0) or the
 // adaptive rule starting at gamma0.
 struct ExitRule {
