@@ -315,6 +315,9 @@ def run_bench(args):
         "verify_mean_rows": round(vrows, 3),
         "verify_step_GBps": round(b_verify / (verify_ms / 1e3) / 1e9, 1),
         "verify_step_frac_hbm": round(b_verify / (verify_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "host_gap_us_per_step": round(1e3 * sum(s["decode_ms"] - s["draft_ms"] - s["verify_ms"] - s["noop_ms"]
+                                                for s in sd_stats) / max(steps_d + stages, 1), 2),
+        "cancelled_steps": sum(s["n_guarded_noop_steps"] for s in sd_stats) / args.steps,
         "prefill_ms": round(sum(s["prefill_ms"] for s in sd_stats) / args.steps, 2),
         "prefill": prefill_roofline(cfg, wl.prompt_len - 1, sum(s["prefill_ms"] for s in sd_stats) / args.steps),
     }
@@ -465,8 +468,9 @@ def run_supplementary(args):
              "draft_step_ms": round(sd["draft_ms"] / n_dr, 4),
              "verify_step_ms": round(sd["verify_ms"] / n_st, 4),
              "verify_mean_rows": round((sd["n_drafted"] + sd["n_stages"]) / n_st, 3),
-             "host_gap_ms_per_step": round((sd["decode_ms"] - sd["draft_ms"] - sd["verify_ms"]) /
-                                           (sd["n_stages"] + sd["n_draft_steps"]), 4),
+             "host_gap_us_per_step": round(1e3 * (sd["decode_ms"] - sd["draft_ms"] - sd["verify_ms"] - sd["noop_ms"]) /
+                                           (sd["n_stages"] + sd["n_draft_steps"]), 2),
+             "cancelled_steps": sd["n_guarded_noop_steps"], "cancelled_ms": round(sd["noop_ms"], 3),
              "ar_step_ms": round(ar["decode_ms"] / max_new, 4),
              "tokens_equal": int(np.sum(sd_tok == ar_tok))}
         # the same planted model with the adaptive exit (the paper's settings)

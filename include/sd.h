@@ -92,6 +92,13 @@ typedef struct {
     int32_t *stage_log;
     int32_t stage_log_cap;
     float *gamma_log;      /* HOST float [stage_log_cap] or NULL: the threshold each stage drafted with */
+    /* Self-speculative calls enqueue the first part of the next step ahead,
+     * on a prediction of the device's decision, so that the GPU does not
+     * wait for the host between steps; a part the decision does not confirm
+     * is cancelled on the device (its kernels return at once). */
+    int64_t n_guarded_noop_steps; /* parts enqueued ahead and cancelled */
+    double noop_ms;               /* their GPU time; decode_ms - draft_ms - verify_ms - noop_ms is the
+                                   * time the GPU waited for the host */
 } sd_stats;
 
 /* Parameters of the adaptive draft exit (Sec. 3.4, Eqs. 2-4).  After every

@@ -60,6 +60,7 @@ class sd_stats(ctypes.Structure):
         ("decode_ms", ctypes.c_double), ("total_ms", ctypes.c_double),
         ("stage_log", ctypes.POINTER(ctypes.c_int32)), ("stage_log_cap", ctypes.c_int32),
         ("gamma_log", ctypes.POINTER(ctypes.c_float)),
+        ("n_guarded_noop_steps", ctypes.c_int64), ("noop_ms", ctypes.c_double),
     ]
 
 

@@ -2,7 +2,9 @@
 // head and the sampling variant.  Each runs on one thread after a step's
 // tokens are decided; it writes the emitted tokens, the control block of the
 // next step (positions, rows, input tokens) and, for self-speculative steps,
-// posts the outcome to the host's mailbox.
+// posts the outcome to the host's mailbox.  A self-speculative decision sets
+// the next step's rows in ctl->m_next; that step's guard kernel moves them to
+// ctl->m if the step the host enqueued is the one decided.
 #pragma once
 
 #include "sd_internal.h"
@@ -39,12 +41,12 @@ __device__ inline void draft_commit(const HeadArgs &h, DevCtl *ctl, int d, float
     const bool exit_now = (pmax < st->gamma) || (j + 1 >= st->kcap);
     if (!exit_now) {
         ctl->pos = st->lc + j + 1;
-        ctl->m = 1;
+        ctl->m_next = 1;
         ctl->tokens[0] = d;
     } else {
         st->phase = PHASE_VERIFY;
         ctl->pos = st->lc;
-        ctl->m = j + 2;
+        ctl->m_next = j + 2;
         ctl->tokens[0] = st->last;
         for (int i = 0; i <= j; ++i)
             ctl->tokens[i + 1] = st->drafts[i];
@@ -100,7 +102,7 @@ __device__ inline void stage_commit(const HeadArgs &h, DevCtl *ctl, int n, int t
         st->phase = kcap > 0 ? PHASE_DRAFT : PHASE_VERIFY;
     }
     ctl->pos = st->lc;
-    ctl->m = 1;
+    ctl->m_next = 1;
     ctl->tokens[0] = st->last;
     post_mailbox(st, h.mb);
 }

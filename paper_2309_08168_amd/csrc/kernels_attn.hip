@@ -109,8 +109,8 @@ __global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
     const int pos = a.ctl->pos, M = a.ctl->m;
     const int ctx = pos + M;
     const int c0 = split * ATTN_CHUNK;
-    if (c0 >= ctx)
-        return;  // uniform over the work-group
+    if (M == 0 || c0 >= ctx)
+        return;  // uniform over the work-group (M = 0: a cancelled step)
     const int dh = a.head_dim, H = a.n_heads;
     const int G = H / a.n_kv_heads;
     const int Q = G * M;
@@ -334,8 +334,8 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
     const int ctx = pos + M;
     const int H = a.n_heads, G = H / a.n_kv_heads, Q = G * M;
     const int c0 = split * ATTN_CHUNK;
-    if (c0 >= ctx || qt * 16 >= Q)
-        return;  // uniform over the work-group
+    if (M == 0 || c0 >= ctx || qt * 16 >= Q)
+        return;  // uniform over the work-group (M = 0: a cancelled step)
     const int cw = c0 + wave * MKW;  // first key of this wave
     const int col = lane & 15, grp = lane >> 4;
     const uint16_t *Kg = reinterpret_cast<const uint16_t *>(a.kcache) + (int64_t)g * a.kv_head_stride;
@@ -516,6 +516,8 @@ __global__ __launch_bounds__(NWV * 64) void k_attn_head(AttnArgs a) {
     const int g = blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int pos = a.ctl->pos, M = a.ctl->m;
+    if (M == 0)
+        return;  // a cancelled step
     const int ctx = pos + M;
     const int dh = a.head_dim, H = a.n_heads;
     const int G = H / a.n_kv_heads;
@@ -962,6 +964,7 @@ __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc
     st->n_stages = st->n_drafted = st->n_accepted = st->n_draft_steps = 0;
     ctl->pos = lc;
     ctl->m = 1;
+    ctl->m_next = 1;
     ctl->tokens[0] = tok;
     if (mb)
         __hip_atomic_store(&mb->word, mb_pack(0, st->phase, st->gen_done, 0), __ATOMIC_RELAXED,
@@ -971,6 +974,22 @@ __global__ void k_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc
 hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,
                               int32_t max_new, int32_t k_max, const ExitRule &rule, hipStream_t s) {
     hipLaunchKernelGGL(k_init_decode, dim3(1), dim3(64), 0, s, st, ctl, mb, lc, dev_last, max_new, k_max, rule);
+    return hipGetLastError();
+}
+
+__global__ void k_step_guard(DevCtl *ctl, const DevState *st, int32_t phase, int32_t max_rows) {
+    if (threadIdx.x != 0)
+        return;
+    // the host and the device agree on a step's kind and rows exactly
+    const int mn = ctl->m_next;
+    const bool ok = !st->gen_done && st->phase == phase && mn == max_rows;
+    ctl->m = ok ? mn : 0;
+}
+
+hipError_t launch_step_guard(DevCtl *ctl, const DevState *st, int32_t phase, int32_t max_rows, hipStream_t s) {
+    if (max_rows < 1 || max_rows > MAX_ROWS)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_step_guard, dim3(1), dim3(64), 0, s, ctl, st, phase, max_rows);
     return hipGetLastError();
 }
 

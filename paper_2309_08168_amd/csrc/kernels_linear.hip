@@ -329,7 +329,10 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
 // One work-group after the head: combine the partials of all tiles and take
 // the decoding decision.
 __global__ __launch_bounds__(HF_THREADS) void k_head_finalize(LinearArgs a) {
-    head_finalize(a, a.n_tiles, a.ctl->m);
+    const int M = a.ctl->m;
+    if (M == 0)
+        return;  // a cancelled step takes no decision
+    head_finalize(a, a.n_tiles, M);
 }
 
 // ---------------------------------------------------------------------------
@@ -551,7 +554,11 @@ __global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
         inv_s[tid] = v;
     }
     __syncthreads();
-    run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, M);
+    // A cancelled step (ctl->m = 0) streams its weights and writes nothing.
+    // The one-row path reads ctl->m only here and only when the launch may
+    // be cancelled: a branch on it before the first loads delays every
+    // launch.
+    run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, (MR == 1 && a.guarded) ? a.ctl->m : M);
 }
 
 // ---------------------------------------------------------------------------
@@ -590,7 +597,7 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
     const int grp = blockIdx.x / S, sp = blockIdx.x - grp * S;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r16 = lane & 15, kg = lane >> 4;
-    const int M = a.ctl->m;
+    const int M = a.ctl->m;  // 0 in a cancelled step: nothing is written
     const int n_tiles = a.n_tiles;
     uint16_t *wl = reinterpret_cast<uint16_t *>(smem) + wave * WL;
     // coalesced loads: instruction ii of tile j reads rows 4 ii + lane / 16,

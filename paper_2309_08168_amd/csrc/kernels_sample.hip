@@ -539,6 +539,8 @@ __global__ __launch_bounds__(SW) void k_sample_decide(SampleArgs a, int mode) {
     const int tid = threadIdx.x, V = a.vocab;
     DevState *st = a.head.st;
     DevCtl *ctl = const_cast<DevCtl *>(a.ctl);
+    if (ctl->m == 0)
+        return;  // a cancelled step takes no decision
     const float T = a.sp.temperature;
     const uint64_t seed = a.sp.seed;
     const int e = st->emitted;

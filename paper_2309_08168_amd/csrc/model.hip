@@ -51,6 +51,10 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 enum LinearKind { LK_QKV = 0, LK_O = 1, LK_GATE_UP = 2, LK_DOWN = 3, LK_HEAD = 4, LK_COUNT = 5 };
 
+// Event pairs timing the steps of a self-speculative decode (a ring; at
+// most four steps are unread at a time).
+constexpr int STEP_EVENT_PAIRS = 8;
+
 // Forwards of the timed regime per forward whose launches the measurement
 // hook brackets with events.
 constexpr int64_t TIMED_SAMPLE = 16;
@@ -137,7 +141,8 @@ struct sd_model {
     int d_glog_cap = 0;
     sd_kv_cache *gen_cache = nullptr;
     std::vector<sd_kv_cache *> caches;  // caller-created caches, detached on destroy
-    hipEvent_t ev[6] = {};
+    // ev[0], ev[1]: prefill; then STEP_EVENT_PAIRS pairs for the decode steps
+    hipEvent_t ev[2 + 2 * STEP_EVENT_PAIRS] = {};
     // measurement hook (sd_model_time_kernel)
     int timed_kind = -1, timed_regime = 0;
     int64_t timed_forwards = 0;  // forwards of the timed regime since the hook was set
@@ -360,8 +365,9 @@ sd_status launch(hipError_t e, const char *what) {
 // reads the bf16 term planes xs (g * h from k_prep_norm, the layer dividing
 // by rms(h) itself, or split by the producer for the output projections).
 sd_status run_linear(sd_model *m, const Workspace &w, const Plan &p, int max_rows, const void *W, const float *X,
-                     int64_t ldx, const void *gain, const EpiArgs &epi, const uint16_t *xs) {
+                     int64_t ldx, const void *gain, const EpiArgs &epi, const uint16_t *xs, bool guarded = false) {
     LinearArgs a{};
+    a.guarded = guarded ? 1 : 0;
     a.W = W;
     a.N = p.N;
     a.K = p.K;
@@ -442,24 +448,43 @@ struct HeadSpec {
     bool sampled = false;  // sampling variant (parameters in sd_model::sp_cur)
 };
 
-// One decoder forward over the rows described by the device control block.
-// max_rows (known to the host) bounds the row count and picks the kernels;
-// skip is a host mask or null.
-sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
-                          const HeadSpec &hs) {
-    const sd_config &c = m->cfg;
+// One decoder forward over the rows described by the device control block,
+// enqueued in pieces: forward_begin (embedding), forward_layers (layers up
+// to a bound; several calls continue one forward), forward_head.  max_rows
+// (known to the host) bounds the row count and picks the kernels; skip is a
+// host mask or null.
+struct ForwardCursor {
+    const Plan *P = nullptr;
+    int max_rows = 0;
+    int next_layer = 0;
+    int pending = 0;       // split-K partials not yet folded into h
+    bool guarded = false;  // launches may find the step cancelled (ctl->m = 0)
+};
+
+sd_status forward_begin(sd_model *m, const Workspace &w, int max_rows, ForwardCursor *cur) {
     const Plan *P = max_rows <= 1 ? m->plan1 : (max_rows <= 2 ? m->plan2 : m->planm);
     // The measurement hook times the class in one of every TIMED_SAMPLE
     // forwards of its regime, with events the runtime attaches to the
     // dispatch (the kernel's own start and end).
     m->timed_now = P[0].regime == m->timed_regime && m->timed_kind >= 0 &&
                    (m->timed_forwards++ % TIMED_SAMPLE) == 0;
-    int pending = 0;  // split-K partials not yet folded into h
+    *cur = ForwardCursor{};
+    cur->P = P;
+    cur->max_rows = max_rows;
+    return launch(launch_embed(m->tok_emb, m->bf16, m->cfg.d_model, w.ctl, w.h, m->cfg.d_model, m->stream),
+                  "embedding");
+}
+
+sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap, const uint8_t *skip,
+                         ForwardCursor *cur, int layer_end) {
+    const sd_config &c = m->cfg;
+    const Plan *P = cur->P;
+    const int max_rows = cur->max_rows;
+    int &pending = cur->pending;
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
-    SD_TRY(launch(launch_embed(m->tok_emb, m->bf16, c.d_model, w.ctl, w.h, ldh, m->stream), "embedding"));
-    for (int l = 0; l < c.n_layers; ++l) {
+    for (int l = cur->next_layer; l < layer_end; ++l) {
         if (!(skip && skip[2 * l])) {
             char *kbase = static_cast<char *>(kv) + (size_t)(2 * l) * c.n_kv_heads * head_stride * ksz;
             char *vbase = static_cast<char *>(kv) + (size_t)(2 * l + 1) * c.n_kv_heads * head_stride * ksz;
@@ -475,7 +500,7 @@ sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
             SD_TRY(prep_norm(m, w, P[LK_QKV], m->attn_norm[l], pending));
-            SD_TRY(run_linear(m, w, P[LK_QKV], max_rows, m->w_qkv[l], w.h, ldh, m->attn_norm[l], e, w.xa));
+            SD_TRY(run_linear(m, w, P[LK_QKV], max_rows, m->w_qkv[l], w.h, ldh, m->attn_norm[l], e, w.xa, cur->guarded));
             AttnArgs at{};
             at.q = w.q;
             at.ld_q = ldq;
@@ -499,7 +524,7 @@ sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap
             EpiArgs eo{};
             eo.out = w.h;
             eo.ld_out = ldh;
-            SD_TRY(run_linear(m, w, P[LK_O], max_rows, m->w_o[l], w.o, ldq, nullptr, eo, w.xa));
+            SD_TRY(run_linear(m, w, P[LK_O], max_rows, m->w_o[l], w.o, ldq, nullptr, eo, w.xa, cur->guarded));
             if (P[LK_O].epi == EPI_PARTIAL)
                 pending = P[LK_O].splits;
         }
@@ -513,36 +538,50 @@ sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap
                 eg.ld_out = w.xld;
             }
             SD_TRY(prep_norm(m, w, P[LK_GATE_UP], m->mlp_norm[l], pending));
-            SD_TRY(run_linear(m, w, P[LK_GATE_UP], max_rows, m->w_gate_up[l], w.h, ldh, m->mlp_norm[l], eg, w.xa));
+            SD_TRY(run_linear(m, w, P[LK_GATE_UP], max_rows, m->w_gate_up[l], w.h, ldh, m->mlp_norm[l], eg, w.xa, cur->guarded));
             EpiArgs ed{};
             ed.out = w.h;
             ed.ld_out = ldh;
-            SD_TRY(run_linear(m, w, P[LK_DOWN], max_rows, m->w_down[l], w.mbuf, c.ffn_dim, nullptr, ed, w.xb));
+            SD_TRY(run_linear(m, w, P[LK_DOWN], max_rows, m->w_down[l], w.mbuf, c.ffn_dim, nullptr, ed, w.xb, cur->guarded));
             if (P[LK_DOWN].epi == EPI_PARTIAL)
                 pending = P[LK_DOWN].splits;
         }
     }
-    if (hs.run) {
-        EpiArgs eh{};
-        eh.head.mode = hs.mode;
-        eh.head.logits = hs.logits;
-        eh.head.ld_logits = c.vocab;
-        eh.head.partials = w.head_part;
-        eh.head.st = m->st;
-        eh.head.mb = m->mb_dev;
-        eh.head.out_tokens = m->d_out;
-        eh.head.stage_log = m->d_log;
-        eh.head.gamma_log = m->d_glog;
-        eh.head.stage_log_cap = std::min(m->d_log_cap / 2, m->d_glog_cap);
-        if (hs.sampled) {
-            eh.head.sampled = 1;
-            eh.head.logits = hs.mode == HEAD_DRAFT ? m->slog_d : m->slog_v;
-            eh.head.logits_by_draft = hs.mode == HEAD_DRAFT;
-        }
-        SD_TRY(prep_norm(m, w, P[LK_HEAD], m->final_norm, pending));
-        SD_TRY(run_linear(m, w, P[LK_HEAD], max_rows, m->lm_head, w.h, ldh, m->final_norm, eh, w.xa));
-    }
+    cur->next_layer = std::max(cur->next_layer, layer_end);
     return SD_OK;
+}
+
+sd_status forward_head(sd_model *m, const Workspace &w, ForwardCursor *cur, const HeadSpec &hs) {
+    if (!hs.run)
+        return SD_OK;
+    const sd_config &c = m->cfg;
+    const Plan *P = cur->P;
+    EpiArgs eh{};
+    eh.head.mode = hs.mode;
+    eh.head.logits = hs.logits;
+    eh.head.ld_logits = c.vocab;
+    eh.head.partials = w.head_part;
+    eh.head.st = m->st;
+    eh.head.mb = m->mb_dev;
+    eh.head.out_tokens = m->d_out;
+    eh.head.stage_log = m->d_log;
+    eh.head.gamma_log = m->d_glog;
+    eh.head.stage_log_cap = std::min(m->d_log_cap / 2, m->d_glog_cap);
+    if (hs.sampled) {
+        eh.head.sampled = 1;
+        eh.head.logits = hs.mode == HEAD_DRAFT ? m->slog_d : m->slog_v;
+        eh.head.logits_by_draft = hs.mode == HEAD_DRAFT;
+    }
+    SD_TRY(prep_norm(m, w, P[LK_HEAD], m->final_norm, cur->pending));
+    return run_linear(m, w, P[LK_HEAD], cur->max_rows, m->lm_head, w.h, c.d_model, m->final_norm, eh, w.xa);
+}
+
+sd_status enqueue_forward(sd_model *m, const Workspace &w, void *kv, int32_t cap, const uint8_t *skip, int max_rows,
+                          const HeadSpec &hs) {
+    ForwardCursor cur;
+    SD_TRY(forward_begin(m, w, max_rows, &cur));
+    SD_TRY(forward_layers(m, w, kv, cap, skip, &cur, m->cfg.n_layers));
+    return forward_head(m, w, &cur, hs);
 }
 
 size_t kv_bytes(const sd_config &c, int32_t cap) {
@@ -886,55 +925,150 @@ sd_status self_spec(sd_model *m, const int32_t *prompt, int32_t prompt_len, int3
     SD_TRY(use_sampling(m, sp));
     SD_TRY(start_generate(m, prompt, prompt_len, max_new, k_max, rule));
     sd_kv_cache *kc = m->gen_cache;
+    const Workspace &w = m->ws;
+    const int L = m->cfg.n_layers;
 
-    // The host mirrors the phase and waits for each step's decision in the
-    // pinned mailbox before enqueueing the next step.
-    int phase = std::min(k_max, max_new - 1) > 0 ? PHASE_DRAFT : PHASE_VERIFY;
-    bool done = max_new <= 0;
-    int32_t seq = 0;
-    double draft_ms = 0.0, verify_ms = 0.0;
-    int prev_phase = -1;
-    int cur = 0;       // event pair in use: ev[2 + 2 cur], ev[3 + 2 cur]
-    int stage_k = 0;   // drafts of the current stage, counted from the mailbox
-    while (!done) {
-        hipEvent_t e0 = m->ev[2 + 2 * cur], e1 = m->ev[3 + 2 * cur];
-        SD_HIP(hipEventRecord(e0, m->stream));
+    // The device decides every step (draft or verification, and how many
+    // rows) and posts the decision to the pinned mailbox.  So that the GPU
+    // never waits for the host, the host keeps the first part of the next
+    // step enqueued ahead on a prediction while it waits for the current
+    // step's decision: a guard kernel, the embedding and the layers up to
+    // the step's first sublayer.  If the decision asks for another step,
+    // the guard has cancelled the part (every kernel sees zero rows and
+    // writes nothing) and the host enqueues the right step in full.
+    struct Step {
+        int phase, rows;
+    };
+    auto split_layer = [&](const uint8_t *sk) {
+        int run = 0;
+        for (int l = 0; l < L; ++l) {
+            run += (sk && sk[2 * l] ? 0 : 1) + (sk && sk[2 * l + 1] ? 0 : 1);
+            if (run >= 1)
+                return l + 1;
+        }
+        return L;
+    };
+    const int split_draft = split_layer(skip), split_verify = split_layer(nullptr);
+
+    // GPU time per slot: each enqueued step, or cancelled part, is bracketed
+    // by two events from a ring; a slot is read once it has surely finished.
+    struct Slot {
+        int kind;  // PHASE_DRAFT, PHASE_VERIFY, or -1: cancelled
+        hipEvent_t a, b;
+    };
+    std::vector<Slot> open_slots;
+    int ring = 0;
+    double draft_ms = 0.0, verify_ms = 0.0, noop_ms = 0.0;
+    int64_t n_noop = 0;
+    hipEvent_t last_end = nullptr;
+    auto slot_open = [&]() -> sd_status {
+        Slot sl{-2, m->ev[2 + 2 * ring], m->ev[3 + 2 * ring]};
+        ring = (ring + 1) % STEP_EVENT_PAIRS;
+        SD_HIP(hipEventRecord(sl.a, m->stream));
+        open_slots.push_back(sl);
+        return SD_OK;
+    };
+    auto slot_close = [&](int kind) -> sd_status {
+        Slot &sl = open_slots.back();
+        sl.kind = kind;
+        SD_HIP(hipEventRecord(sl.b, m->stream));
+        last_end = sl.b;
+        return SD_OK;
+    };
+    auto account = [&](size_t keep) {  // all but the last `keep` slots have finished
+        size_t n = open_slots.size() > keep ? open_slots.size() - keep : 0;
+        for (size_t i = 0; i < n; ++i) {
+            const Slot &sl = open_slots[i];
+            const float ms = elapsed(sl.a, sl.b);
+            (sl.kind == PHASE_DRAFT ? draft_ms : sl.kind == PHASE_VERIFY ? verify_ms : noop_ms) += ms;
+        }
+        open_slots.erase(open_slots.begin(), open_slots.begin() + (ptrdiff_t)n);
+    };
+    auto begin_step = [&](const Step &st, ForwardCursor *cur) -> sd_status {
+        SD_TRY(slot_open());
+        SD_TRY(launch(launch_step_guard(w.ctl, m->st, st.phase, st.rows, m->stream), "step guard"));
+        SD_TRY(forward_begin(m, w, st.rows, cur));
+        cur->guarded = true;
+        return forward_layers(m, w, kc->buf, kc->cap, st.phase == PHASE_DRAFT ? skip : nullptr, cur,
+                              st.phase == PHASE_DRAFT ? split_draft : split_verify);
+    };
+    auto finish_step = [&](const Step &st, ForwardCursor *cur) -> sd_status {
+        cur->guarded = false;  // the host has seen the decision: the step runs
+        SD_TRY(forward_layers(m, w, kc->buf, kc->cap, st.phase == PHASE_DRAFT ? skip : nullptr, cur, L));
         HeadSpec hs;
         hs.run = true;
         hs.sampled = sp != nullptr;
-        if (phase == PHASE_DRAFT) {
-            hs.mode = HEAD_DRAFT;
-            SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, skip, 1, hs));
+        hs.mode = st.phase == PHASE_DRAFT ? HEAD_DRAFT : HEAD_VERIFY;
+        SD_TRY(forward_head(m, w, cur, hs));
+        return slot_close(st.phase);
+    };
+
+    // The host mirrors the stage: drafts enqueued in it, the draft budget
+    // (from the tokens emitted before it), and the previous stage's length,
+    // which predicts where this one ends.
+    int stage_k = 0, prev_stage_k = 1;
+    int kcap = std::min(k_max, max_new - 1);
+    auto apply = [&](const Step &st) {
+        if (st.phase == PHASE_DRAFT) {
             ++stage_k;
         } else {
-            hs.mode = HEAD_VERIFY;
-            SD_TRY(enqueue_forward(m, m->ws, kc->buf, kc->cap, nullptr, stage_k + 1, hs));
+            prev_stage_k = std::max(stage_k, 1);
             stage_k = 0;
         }
-        SD_HIP(hipEventRecord(e1, m->stream));
-        ++seq;
-        uint64_t word = 0;
-        SD_TRY(wait_mailbox(m, seq, &word));
-        // the previous step's events have completed: account for them
-        if (prev_phase >= 0) {
-            const float ms = elapsed(m->ev[2 + 2 * (1 - cur)], m->ev[3 + 2 * (1 - cur)]);
-            (prev_phase == PHASE_DRAFT ? draft_ms : verify_ms) += ms;
+    };
+    auto predict = [&](const Step &prev) -> Step {
+        if (prev.phase == PHASE_DRAFT && (stage_k >= kcap || stage_k >= prev_stage_k))
+            return Step{PHASE_VERIFY, stage_k + 1};
+        return Step{PHASE_DRAFT, 1};
+    };
+    if (max_new > 0) {
+        Step cur_step{kcap > 0 ? PHASE_DRAFT : PHASE_VERIFY, 1};
+        ForwardCursor cur, ahead;
+        SD_TRY(begin_step(cur_step, &cur));
+        SD_TRY(finish_step(cur_step, &cur));
+        apply(cur_step);
+        int32_t seq = 1;
+        Step pred = predict(cur_step);
+        size_t tev_mark = m->tev_used;
+        SD_TRY(begin_step(pred, &ahead));
+        for (;;) {
+            uint64_t word = 0;
+            SD_TRY(wait_mailbox(m, seq, &word));
+            account(2);  // the current step's end event and the part ahead may still be pending
+            if (cur_step.phase == PHASE_VERIFY)
+                kcap = std::min(k_max, max_new - mb_emitted(word) - 1);
+            const bool done = mb_done(word);
+            const Step truth{mb_phase(word), mb_phase(word) == PHASE_DRAFT ? 1 : stage_k + 1};
+            if (!done && truth.phase == pred.phase && truth.rows == pred.rows) {
+                SD_TRY(finish_step(pred, &ahead));
+            } else {
+                // cancelled on the device by its guard; its timed launches
+                // (measurement hook) are dropped
+                SD_TRY(slot_close(-1));
+                m->tev_used = tev_mark;
+                ++n_noop;
+                if (done)
+                    break;
+                SD_TRY(begin_step(truth, &cur));
+                SD_TRY(finish_step(truth, &cur));
+            }
+            cur_step = truth;
+            apply(cur_step);
+            ++seq;
+            pred = predict(cur_step);
+            tev_mark = m->tev_used;
+            SD_TRY(begin_step(pred, &ahead));
         }
-        prev_phase = phase;
-        cur = 1 - cur;
-        phase = mb_phase(word);
-        done = mb_done(word);
     }
     SD_TRY(copy_results(m, max_new, out_tokens, stats));
-    if (prev_phase >= 0) {
-        const float ms = elapsed(m->ev[2 + 2 * (1 - cur)], m->ev[3 + 2 * (1 - cur)]);
-        (prev_phase == PHASE_DRAFT ? draft_ms : verify_ms) += ms;
-    }
+    account(0);
     if (stats) {
         stats->draft_ms = draft_ms;
         stats->verify_ms = verify_ms;
+        stats->noop_ms = noop_ms;
+        stats->n_guarded_noop_steps = n_noop;
         stats->prefill_ms = elapsed(m->ev[0], m->ev[1]);
-        stats->total_ms = prev_phase >= 0 ? elapsed(m->ev[0], m->ev[3 + 2 * (1 - cur)]) : stats->prefill_ms;
+        stats->total_ms = last_end ? elapsed(m->ev[0], last_end) : stats->prefill_ms;
         stats->decode_ms = stats->total_ms - stats->prefill_ms;
     }
     kc->len = 0;
@@ -962,6 +1096,8 @@ sd_status autoregressive(sd_model *m, const int32_t *prompt, int32_t prompt_len,
         stats->draft_ms = 0.0;
         stats->verify_ms = stats->decode_ms;
         stats->n_stages = 0;
+        stats->n_guarded_noop_steps = 0;
+        stats->noop_ms = 0.0;
     }
     kc->len = 0;
     return SD_OK;

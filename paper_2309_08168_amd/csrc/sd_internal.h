@@ -22,8 +22,9 @@ constexpr int MAX_SPLITS = 512;
 // the host never needs token ids or positions during decoding.
 struct DevCtl {
     int32_t pos;               // position of row 0
-    int32_t m;                 // rows in this forward, 1..MAX_ROWS
+    int32_t m;                 // rows in this forward, 1..MAX_ROWS; 0: a cancelled step (every kernel returns)
     int32_t tokens[MAX_ROWS];  // input token of every row
+    int32_t m_next;            // self-speculative decoding: rows of the next step, set by the decision
 };
 
 enum Phase : int32_t { PHASE_DRAFT = 0, PHASE_VERIFY = 1 };
@@ -69,6 +70,7 @@ __host__ __device__ inline uint64_t mb_pack(int32_t seq, int32_t phase, int32_t 
 __host__ __device__ inline int32_t mb_seq(uint64_t w) { return (int32_t)(uint32_t)(w & 0xffffffffu); }
 __host__ __device__ inline int32_t mb_phase(uint64_t w) { return (int32_t)((w >> 32) & 15); }
 __host__ __device__ inline bool mb_done(uint64_t w) { return ((w >> 36) & 1) != 0; }
+__host__ __device__ inline int32_t mb_emitted(uint64_t w) { return (int32_t)((w >> 40) & 0xffffff); }
 
 enum HeadMode : int32_t { HEAD_NONE = 0, HEAD_AR = 1, HEAD_DRAFT = 2, HEAD_VERIFY = 3 };
 
@@ -218,6 +220,8 @@ struct LinearArgs {
     int32_t splits;        // EPI_PARTIAL: work-groups splitting the reduction per tile group
     float *part;           // EPI_PARTIAL: [splits][MAX_ROWS][N]
     int32_t n_tiles;       // tiles in the layer (set by launch_linear)
+    int32_t guarded;       // part of a step enqueued ahead, which the step guard may cancel (ctl->m = 0):
+                           // the one-row path then takes its row count from ctl->m too
 };
 
 struct AttnArgs {
@@ -322,6 +326,10 @@ struct ExitRule {
     float gamma;
     double gamma0, alpha, epsilon, beta1, beta2;
 };
+// First kernel of a self-speculative step the host enqueued as (phase,
+// max_rows): the step runs (ctl->m = ctl->m_next) when the device's decision
+// asks for that kind of step, else it is cancelled (ctl->m = 0).
+hipError_t launch_step_guard(DevCtl *ctl, const DevState *st, int32_t phase, int32_t max_rows, hipStream_t s);
 hipError_t launch_init_decode(DevState *st, DevCtl *ctl, Mailbox *mb, int32_t lc, const int32_t *dev_last,
                               int32_t max_new, int32_t k_max, const ExitRule &rule, hipStream_t s);
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);
