@@ -3,7 +3,8 @@ sd_autoregressive_sample) against the oracle.
 
 - Same seed, same tokens: both sides draw the same Philox uniforms, so the
   GPU emits the oracle's tokens and stage trace, up to the first token one
-  of whose decisions the oracle reports within delta of flipping.  delta =
+  of whose decisions the oracle reports within delta of flipping (float32
+  models, and a bf16 model whose measured logit error sets the bound).  delta =
   2 tol / T: a logit error of tol moves a warped probability by at most about
   2 tol / T relative, and so every CDF boundary, acceptance ratio and top-p
   cut by at most that in probability units.  The models have a planted
@@ -100,6 +101,73 @@ def test_sample_matches_oracle(name, mask, k_max, gamma, T, top_p, t, max_new, s
     assert np.all((sd >= 0) & (sd < cfg.vocab))
     print(f"{name} T={T} top_p={top_p}: SD equal for {n_sd}/{max_new}, AR for {n_ar}/{max_new}; "
           f"acceptance {st['n_accepted']}/{st['n_drafted']}")
+
+
+# bfloat16 model (planted like the cases above): same seed, same tokens.  The
+# bf16 tolerance (3e-2 std of a row) would flag nearly every draw of a
+# peaked distribution, so the test first measures the GPU's logit error on
+# this model over the oracle's own sampled sequence, through the decode-path
+# kernels (1-, 2- and 5-row forwards, full model and draft mask), requires
+# it within BF16_SAMPLE_TOL absolute, and takes delta = 2 BF16_SAMPLE_TOL / T.
+BF16_SAMPLE_TOL = 1e-4
+# Seeds chosen (on the CPU, with the oracle alone) so that the oracle's first
+# decision within delta comes late, and the comparison covers most tokens.
+BF16_CASES = [
+    ("mini_bf16", "random2", 4, 0.6, 1.0, 0.9, 16, 40, 19),
+    ("mini_bf16", "random2", 6, None, 0.6, 1.0, 16, 40, 29),
+    ("mini_bf16", "random2", 5, 0.0, 0.5, 1.0, 12, 32, 9),
+]
+
+
+def _decode_path_error(cfg, om, dm, seq, start, z):
+    """max |GPU - oracle| over the logits of rows start.. of seq, forwarded
+    in chunks of 1, 2 and 5 rows, with the full model and with mask z."""
+    worst = 0.0
+    for skip in (None, z):
+        oc, gc = om.cache(len(seq)), dm.cache(len(seq))
+        om.forward(oc, seq[:start], want_logits=False)
+        dm.forward(seq[:start], gc)
+        i, sizes = start, [1, 2, 5]
+        while i < len(seq):
+            n = min(sizes[(i - start) % 3], len(seq) - i)
+            ref = om.forward(oc, seq[i:i + n], skip=skip)["logits"]
+            got = torch.empty((n, cfg.vocab), dtype=torch.float32, device="cuda")
+            dm.forward(seq[i:i + n], gc, skip=skip, logits=got)
+            worst = max(worst, float(np.abs(got.cpu().numpy().astype(np.float64) - ref).max()))
+            i += n
+    return worst
+
+
+@pytest.mark.parametrize("name,mask,k_max,gamma,T,top_p,t,max_new,seed", BF16_CASES)
+def test_sample_matches_oracle_bf16(name, mask, k_max, gamma, T, top_p, t, max_new, seed):
+    cfg, w, om, dm = _pair(name, mask)
+    T, top_p = _f32(T), _f32(top_p)
+    pr = S.prompt(cfg, t, seed=t)
+    z = S.skip_mask(cfg, mask, seed=11)
+    kw = dict(adaptive={}) if gamma is None else dict(gamma=gamma)
+    ref = om.generate_sd_sample(pr, max_new, z, k_max, T, top_p, seed, **kw)
+    ar_ref, ar_margin = om.generate_ar_sample(pr, max_new, T, top_p, seed)
+    seq = np.concatenate([pr, ref["tokens"]]).astype(np.int32)
+    err = _decode_path_error(cfg, om, dm, seq, t - 1, z)
+    # the bf16 parity bar holds, and this model's error is within the bound delta assumes
+    assert err <= BF16_SAMPLE_TOL, f"GPU logit error {err:.3g} above {BF16_SAMPLE_TOL}"
+    sd, st = dm.generate_sd_sample(pr, max_new, z, k_max, T, top_p, seed, **kw)
+    ar, _ = dm.generate_ar_sample(pr, max_new, T, top_p, seed)
+    delta = 2 * BF16_SAMPLE_TOL / T
+    n_sd = _first_flag(ref["margin"], delta)
+    n_ar = _first_flag(ar_margin, delta)
+    assert np.array_equal(sd[:n_sd], ref["tokens"][:n_sd]), (sd.tolist(), ref["tokens"].tolist())
+    assert np.array_equal(ar[:n_ar], ar_ref[:n_ar]), (ar.tolist(), ar_ref.tolist())
+    if ref["min_gamma_gap"] > delta:
+        ends = np.cumsum(ref["stages"][:, 1] + 1)
+        n_st = int(np.sum(ends <= n_sd))
+        assert np.array_equal(st["stages"][:n_st], ref["stages"][:n_st])
+        if gamma is None:
+            assert np.array_equal(st["gammas"][:n_st], ref["gammas"][:n_st])
+    # the comparison must cover most of the run, else the case says little
+    assert n_sd >= max_new // 2 and n_ar >= max_new // 2, (n_sd, n_ar)
+    print(f"{name} bf16 T={T} top_p={top_p}: logit error {err:.2e}; SD equal for {n_sd}/{max_new}, "
+          f"AR for {n_ar}/{max_new}; acceptance {st['n_accepted']}/{st['n_drafted']}")
 
 
 def test_speculative_sampling_distribution_on_gpu():
