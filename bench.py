@@ -665,6 +665,51 @@ def run_search(args):
 # profiler helpers
 
 
+def run_stream_probe(args):
+    """Achievable HBM read bandwidth: the library's streaming-read probe
+    (sd_measure_read_bandwidth) over a 4 GiB device buffer, at the byte
+    counts of the 13B decode layers and at 4 GiB, for 1-16 work-groups per
+    compute unit.  Consecutive reads of one size start at different offsets,
+    so a read never finds its bytes in the 256 MB last-level cache.  Also
+    fits t = bytes / B + t0 over the layer sizes at each size's best shape."""
+    import torch
+
+    from paper_2309_08168_amd import binding
+
+    total = 4 << 30
+    buf = torch.ones(total, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    cfg = S.MODELS["13b"]
+    d, F = cfg.d_model, cfg.ffn_dim
+    sizes = {"o_proj_13b": d * d * 2, "down_13b": d * F * 2, "qkv_13b": cfg.qkv_rows * d * 2,
+             "gate_up_13b": 2 * F * d * 2, "lm_head_13b": cfg.vocab * d * 2, "4GiB": total}
+    reps = args.probe_reps
+    rows, best = [], {}
+    for name, n in sizes.items():
+        n = n // 256 * 256
+        span = max(total - n, 0)
+        for wg, lif in [(w_, l_) for w_ in (1, 2, 4, 8, 16) for l_ in (2, 4, 8, 16)]:
+            ms = []
+            for it in range(reps):
+                off = 0 if span == 0 else (it * n) % span // 256 * 256
+                ms.append(binding.measure_read_bandwidth(buf, n, wg, 1, sink, offset=off, loads_in_flight=lif))
+            med = float(np.median(ms))
+            r = {"size": name, "bytes": n, "wg_per_cu": wg, "loads_in_flight": lif, "median_us": round(med * 1e3, 2),
+                 "min_us": round(min(ms) * 1e3, 2), "GBps": round(n / (med / 1e3) / 1e9, 1)}
+            rows.append(r)
+            if name not in best or r["GBps"] > best[name]["GBps"]:
+                best[name] = r
+            log(json.dumps(r))
+    layer = [b for k, b in best.items() if k != "4GiB"]
+    x = np.array([b["bytes"] for b in layer], float)
+    y = np.array([b["median_us"] for b in layer], float)
+    slope, t0 = np.polyfit(x, y, 1)
+    out = {"mode": "stream-probe", "kernel": "k_read_probe (16-byte non-temporal loads, 256 threads)",
+           "best": best, "fit_layer_sizes": {"GBps": round(1e-3 / slope, 1), "t0_us": round(float(t0), 2)},
+           "peak_GBps": HBM_PEAK_GBPS, "rows": rows}
+    print(json.dumps(out), flush=True)
+
+
 def run_calibrate_copy(args):
     import torch
 
@@ -755,10 +800,11 @@ def _forwards(disp):
 def run_summarize_step_counters(args):
     """HBM bytes per verification forward from FETCH_SIZE / WRITE_SIZE (all
     kernels of the forward, calibrated by the 1 GiB copy) against the
-    algorithmic bytes, and MFMA busy cycles and issued bf16 flops per kernel of
-    the 13-row forward.  Inputs: the counter CSVs of
-    --verify-micro --micro-rows 1,2,13 --micro-ctx 512 --micro-iters 1 --with-copy
-    (FETCH_SIZE, WRITE_SIZE) and of --micro-rows 13 (MFMA counters)."""
+    algorithmic bytes, and the MFMA use of the forward's matrix-core linear
+    layers, for every (context, rows) pair of --micro-ctx x --micro-rows.
+    Inputs: the counter CSVs of --verify-micro --micro-iters 1 --with-copy
+    with --pmc FETCH_SIZE, --pmc WRITE_SIZE and --pmc
+    SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 GRBM_GUI_ACTIVE."""
     fetch_csv, write_csv, mfma_csv = args.summarize_step_counters
     cfg = S.MODELS["13b"]
     fd, wd = _dispatches(fetch_csv), _dispatches(write_csv)
@@ -768,28 +814,53 @@ def run_summarize_step_counters(args):
         return args.copy_bytes / (max(cp) * 1024.0) if cp else 1.0
 
     cf, cw = calib(fd, "FETCH_SIZE"), calib(wd, "WRITE_SIZE")
-    ff, wf = _forwards(fd), _forwards(wd)
-    rows_list = [1, 2, 13]
-    lines = ["# HBM bytes per 13B forward (FETCH_SIZE + WRITE_SIZE over all its kernels) and MFMA counters",
+    ff, wf, md = _forwards(fd), _forwards(wd), _forwards(_dispatches(mfma_csv))
+    rows_list = [int(x) for x in args.micro_rows.split(",")]
+    ctx_list = [int(x) for x in args.micro_ctx.split(",")]
+    pairs = [(ctx, M) for ctx in ctx_list for M in rows_list]
+    lines = ["# HBM bytes per 13B forward (FETCH_SIZE + WRITE_SIZE over all its kernels) and MFMA use",
              f"# command: {args.command}",
              f"# copy calibration: FETCH_SIZE x{cf:.4f}, WRITE_SIZE x{cw:.4f}", "",
-             f"{'rows':>4} {'kernels':>7} {'fetch_GB':>9} {'write_GB':>9} {'total_GB':>9} {'algorithmic_GB':>15} {'ratio':>6}"]
-    for j, M in enumerate(rows_list):
-        idx = 2 * j + 1  # the timed forward of each row count (after one warm-up)
+             f"{'rows':>4} {'ctx':>5} {'kernels':>7} {'fetch_GB':>9} {'write_GB':>9} {'total_GB':>9} "
+             f"{'algorithmic_GB':>15} {'ratio':>6}"]
+    for j, (ctx, M) in enumerate(pairs):
+        idx = 2 * j + 1  # the timed forward of each pair (after one warm-up)
         if idx >= len(ff) or idx >= len(wf):
             break
         fb = sum(c.get("FETCH_SIZE", 0.0) for _, c, _ in ff[idx]) * 1024.0 * cf
         wb = sum(c.get("WRITE_SIZE", 0.0) for _, c, _ in wf[idx]) * 1024.0 * cw
-        alg = step_bytes(cfg, None, 512, M)
-        lines.append(f"{M:4d} {len(ff[idx]):7d} {fb / 1e9:9.3f} {wb / 1e9:9.3f} {(fb + wb) / 1e9:9.3f} "
+        alg = step_bytes(cfg, None, ctx, M)
+        lines.append(f"{M:4d} {ctx:5d} {len(ff[idx]):7d} {fb / 1e9:9.3f} {wb / 1e9:9.3f} {(fb + wb) / 1e9:9.3f} "
                      f"{alg / 1e9:15.3f} {(fb + wb) / alg:6.3f}")
-    md = _forwards(_dispatches(mfma_csv))
-    if len(md) >= 2:
-        lines += ["", "# 13-row forward, MFMA kernels: busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x duration x 2.4 GHz);",
-                  "# issued = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops (three bf16 terms per row in 16 columns per packing)",
+    lines += ["", "# MFMA use per forward (rows > 2: matrix-core linear layers).  busy = SQ_VALU_MFMA_BUSY_CYCLES /",
+              "# (1024 SIMDs x 2.4 GHz x time); issued = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops (three bf16 terms",
+              "# per row, 16 columns per packing); useful = 2 x rows x weights; over the MFMA kernels' time and over",
+              "# the whole forward (all its kernels, measured under counter collection)",
+              f"{'rows':>4} {'ctx':>5} {'mfma_us':>8} {'busy':>6} {'issued_TF':>9} {'useful_TF':>9} {'fwd_us':>8} "
+              f"{'issued_TF_fwd':>13} {'useful_frac_peak':>16}"]
+    params = cfg.param_count() - cfg.vocab * cfg.d_model
+    for j, (ctx, M) in enumerate(pairs):
+        idx = 2 * j + 1
+        if M <= 2 or idx >= len(md):
+            continue
+        ks = [(n, c, ns) for n, c, ns in md[idx] if "k_linear_mfma" in n]
+        t_m = sum(ns for _, _, ns in ks)
+        t_f = sum(ns for _, _, ns in md[idx])
+        busy = sum(c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) for _, c, _ in ks)
+        flops = sum(c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) for _, c, _ in ks) * 512.0
+        useful = 2.0 * M * params
+        if t_m <= 0:
+            continue
+        lines.append(f"{M:4d} {ctx:5d} {t_m / 1e3:8.1f} {busy / (1024 * t_m * 2.4):6.3f} {flops / t_m / 1e3:9.1f} "
+                     f"{useful / t_m / 1e3:9.1f} {t_f / 1e3:8.1f} {flops / t_f / 1e3:13.1f} "
+                     f"{useful / t_f / 1e3 / MFMA_BF16_PEAK_TFLOPS:16.4f}")
+    # per kernel at the largest row count and the first context
+    sel = [j for j, (ctx, M) in enumerate(pairs) if ctx == ctx_list[0] and M == max(rows_list)]
+    if sel and 2 * sel[0] + 1 < len(md):
+        lines += ["", f"# {max(rows_list)}-row forward at {ctx_list[0]} keys, per MFMA kernel",
                   f"{'calls':>5} {'avg_us':>7} {'busy':>6} {'issued_TFLOPs':>13}  kernel"]
         per = {}
-        for name, c, ns in md[1]:
+        for name, c, ns in md[2 * sel[0] + 1]:
             if "k_linear_mfma" not in name:
                 continue
             e = per.setdefault(name, [0, 0.0, 0.0, 0.0])
@@ -835,6 +906,8 @@ def main():
     ap.add_argument("--search-new", type=int, default=32)
     ap.add_argument("--search-init", type=int, default=16)
     ap.add_argument("--search-iters", type=int, default=144)
+    ap.add_argument("--stream-probe", action="store_true", help="achievable HBM read bandwidth (read probe)")
+    ap.add_argument("--probe-reps", type=int, default=10)
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--with-copy", action="store_true", help="also run the calibration copy after the bench")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
@@ -866,6 +939,8 @@ def main():
     torch.cuda.set_device(0)
     if args.calibrate_copy:
         return run_calibrate_copy(args)
+    if args.stream_probe:
+        return run_stream_probe(args)
     if args.verify_micro:
         run_verify_micro(args)
     elif args.supplementary:

@@ -336,6 +336,21 @@ sd_status sd_model_kernel_time(sd_model *model, int64_t *launches, double *total
                                int32_t name_cap, int64_t *n, int64_t *k);
 
 /* Message of the last non-OK status returned to this thread ("" if none). */
+/* Measurement (the achievable ceiling beside the 8 TB/s peak): decoding is
+ * bound by memory bandwidth (Sec. 1, 3.1), so the GB/s of the decoding
+ * kernels are also read against what a plain streaming read reaches on this
+ * GPU.  Reads `bytes` (a positive multiple of 16) of the DEVICE buffer buf
+ * (16-byte aligned) `iters` times with 16-byte non-temporal loads, the
+ * pattern of the weight-streaming layers, loads_in_flight (2, 4, 8 or 16)
+ * per thread, on wg_per_cu x (compute units) work-groups of 256 threads on
+ * hip_stream (NULL: the null stream).  *ms_out
+ * receives the mean duration of one read, from events attached to each
+ * dispatch.  sink is a DEVICE buffer of at least 4 bytes that the probe may
+ * write (it keeps the loads from being optimised away).  Errors:
+ * INVALID_ARG, DEVICE. */
+sd_status sd_measure_read_bandwidth(const void *buf, size_t bytes, int32_t wg_per_cu, int32_t loads_in_flight,
+                                    int32_t iters, void *sink, void *hip_stream, double *ms_out);
+
 const char *sd_last_error(void);
 
 /* Library version string. */

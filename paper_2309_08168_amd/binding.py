@@ -25,7 +25,7 @@ EXPORTS = (
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward", "sd_forward_static",
     "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
     "sd_self_spec_sample", "sd_autoregressive_sample", "sd_search_skip_set_fn", "sd_search_skip_set",
-    "sd_model_time_kernel", "sd_model_kernel_time",
+    "sd_model_time_kernel", "sd_model_kernel_time", "sd_measure_read_bandwidth",
     "sd_last_error", "sd_version",
 )
 
@@ -140,6 +140,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
         "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
                                   p(ctypes.c_int64), p(ctypes.c_int64)], ctypes.c_int),
+        "sd_measure_read_bandwidth": ([vp, ctypes.c_size_t, i32, i32, i32, vp, vp, p(ctypes.c_double)], ctypes.c_int),
         "sd_last_error": ([], ctypes.c_char_p),
         "sd_version": ([], ctypes.c_char_p),
     }
@@ -354,6 +355,21 @@ class Model:
         check(load().sd_autoregressive_sample(self._h, _ptr(pr), pr.size, max_new, ctypes.byref(sp), _ptr(out),
                                               ctypes.byref(st)))
         return out[:max_new], _stats(st, None)
+
+
+def measure_read_bandwidth(buf, nbytes: int, wg_per_cu: int, iters: int, sink, stream=None, offset: int = 0,
+                           loads_in_flight: int = 4) -> float:
+    """sd_measure_read_bandwidth over nbytes of a torch device buffer from
+    byte offset; returns the mean milliseconds of one read."""
+    import torch
+
+    st = stream if stream is not None else torch.cuda.current_stream()
+    ms = ctypes.c_double()
+    check(load().sd_measure_read_bandwidth(ctypes.c_void_p(buf.data_ptr() + offset), nbytes, wg_per_cu,
+                                           loads_in_flight, iters,
+                                           ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(st.cuda_stream),
+                                           ctypes.byref(ms)))
+    return ms.value
 
 
 def _search_call(call, n_dims: int, objective: int, cost, params: dict) -> dict:

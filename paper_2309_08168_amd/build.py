@@ -12,7 +12,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libsd.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["kernels_linear.hip", "kernels_attn.hip", "kernels_sample.hip", "kernels_prefill.hip", "model.hip", "skip_search.cpp"]
+SOURCES = ["kernels_linear.hip", "kernels_attn.hip", "kernels_sample.hip", "kernels_prefill.hip", "model.hip",
+           "skip_search.cpp", "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
