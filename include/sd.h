@@ -129,7 +129,12 @@ sd_status sd_model_destroy(sd_model *model);
  * n_layers * 2 * n_kv_heads * capacity * head_dim * sizeof(dtype). */
 size_t sd_kv_cache_bytes(const sd_config *config, int32_t capacity);
 
-/* Creates a KV cache of capacity positions (1..65536), length 0.  device_buf, when
+/* KV caches.  Both decoding stages attend over the cache of the tokens so
+ * far (Sec. 3.2): the draft of the full model's prefix, the verification of
+ * the committed prefix plus the drafts it scores in one forward; rejected
+ * drafts are rolled back by truncation (Algorithm 2).
+ *
+ * Creates a KV cache of capacity positions (1..65536), length 0.  device_buf, when
  * not NULL, is a caller-owned device buffer of sd_kv_cache_bytes() bytes
  * (borrowed), laid out [n_layers][2 (K, V)][n_kv_heads][capacity][head_dim]
  * in the model dtype, with rotary position embedding already applied to K;
@@ -146,7 +151,12 @@ sd_status sd_kv_cache_truncate(sd_kv_cache *cache, int32_t len);
  * (0 <= len <= capacity). */
 sd_status sd_kv_cache_set_length(sd_kv_cache *cache, int32_t len);
 
-/* One forward of n tokens (HOST int32 [n], each in [0, vocab)) at positions
+/* The decoder forward of both stages (Sec. 3.2): with skip_mask the draft
+ * model, which bypasses the chosen attention and MLP sublayers (Sec. 3.3),
+ * without it the original model, which verifies several tokens in one
+ * forward (Algorithm 2).
+ *
+ * One forward of n tokens (HOST int32 [n], each in [0, vocab)) at positions
  * [len, len + n) of cache; writes K/V of every attention sublayer that
  * skip_mask keeps and sets len += n.  skip_mask is a HOST uint8
  * [2 n_layers] (entry 2l: attention of layer l, 2l+1: its MLP; 1 = bypass,

@@ -317,3 +317,35 @@ def test_verify_micro_logits(name, ctx):
     cache.close()
     del buf
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name", ["7b", "13b"])
+def test_kv_rounding_drift_report(name, tmp_path):
+    """Report, not a gate: the paper's models run in bf16, so both the oracle
+    and the GPU store bf16 K/V for a bf16 model.  This measures how far the
+    GPU's 13-row logits sit from an oracle variant that keeps K/V unrounded
+    (float64), in units of the bf16 tolerance, next to the distance from
+    the oracle itself."""
+    cfg, w, om, dm = _pair(name)
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "sd_oracle.c")).read()
+    anchor = "if (m->c.wdtype != 1 || x == 0.0 || !isfinite(x))"
+    assert src.count(anchor) == 1
+    (tmp_path / "sd_oracle.c").write_text(src.replace(anchor, "if (1)"))
+    lib = oracle.build(src=str(tmp_path / "sd_oracle.c"), out=str(tmp_path / "liboracle_kv64.so"))
+    om64 = oracle.Model(cfg, w, lib_path=lib)
+    toks = S.prompt(cfg, 25, seed=21)
+    refs = []
+    for m in (om, om64):
+        c = m.cache(32)
+        m.forward(c, toks[:12], want_logits=False)
+        refs.append(m.forward(c, toks[12:25])["logits"])
+    gc = dm.cache(32)
+    dm.forward(toks[:12], gc)
+    got = _gpu_logits(dm, toks[12:25], gc).astype(np.float64)
+    tol = U.BF16_REL_TOL * refs[0].std(axis=-1)
+    r_bf16 = float((np.abs(got - refs[0]).max(axis=-1) / tol).max())
+    r_f64 = float((np.abs(got - refs[1]).max(axis=-1) / tol).max())
+    r_def = float((np.abs(refs[0] - refs[1]).max(axis=-1) / tol).max())
+    _say(f"{name}: 13 rows after 12, max |d|/tol: GPU vs oracle (bf16 KV) {r_bf16:.3f}, GPU vs float64-KV "
+         f"oracle {r_f64:.3f}, the two oracles {r_def:.3f}")
+    assert np.isfinite(r_f64)
