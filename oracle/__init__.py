@@ -109,6 +109,12 @@ def _load(path: str = LIB_PATH):
         lib.orc_generate_ar_sample.argtypes = [vp, vp, i32, i32, p(Sampling), vp, vp]
         lib.orc_generate_sd_sample.argtypes = [vp, vp, i32, i32, vp, i32, ctypes.c_float, vp, p(Sampling), vp, vp,
                                                p(SDStats), vp, vp, vp]
+        lib.orc_fp8_value.argtypes = [ctypes.c_uint8]
+        lib.orc_fp8_value.restype = ctypes.c_double
+        lib.orc_quantize_fp8_rows.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, vp]
+        lib.orc_set_draft_fp8.argtypes = [vp, vp]
+        for fn in ("orc_quantize_fp8_rows", "orc_set_draft_fp8"):
+            getattr(lib, fn).restype = ctypes.c_int
         for fn in ("orc_cache_truncate", "orc_cache_load", "orc_forward", "orc_generate_ar", "orc_generate_sd",
                    "orc_generate_sd_adaptive", "orc_generate_ar_sample", "orc_generate_sd_sample"):
             getattr(lib, fn).restype = ctypes.c_int
@@ -142,6 +148,24 @@ def warp(logits, temperature: float, top_p: float, lib_path: str = LIB_PATH):
     if kept < 0:
         raise OracleError(f"orc_warp failed with status {kept}")
     return pi, int(kept), cm.value
+
+
+def fp8_value(b: int, lib_path: str = LIB_PATH) -> float:
+    """The value of an OCP FP8 E4M3 byte."""
+    return float(_load(lib_path).orc_fp8_value(int(b)))
+
+
+def quantize_fp8_rows(w_bf16: np.ndarray, lib_path: str = LIB_PATH):
+    """(bytes uint8 [N][K], exponents int32 [N]) of a bf16 matrix [N][K]: the
+    nearest E4M3 value of W[n][k] * 2^-e[n], e[n] the smallest exponent that
+    keeps the row's largest magnitude within 448."""
+    w = np.ascontiguousarray(w_bf16, dtype=np.uint16)
+    n, k = w.shape
+    q = np.empty((n, k), np.uint8)
+    e = np.empty(n, np.int32)
+    _check(_load(lib_path).orc_quantize_fp8_rows(w.ctypes.data, n, k, q.ctypes.data, e.ctypes.data),
+           "orc_quantize_fp8_rows")
+    return q, e
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -184,6 +208,11 @@ class Model:
         if getattr(self, "_h", None):
             self._lib.orc_destroy(self._h)
             self._h = None
+
+    def set_draft_fp8(self, skip):
+        """Quantize the draft's weights (the sublayers skip keeps) to FP8; None removes them."""
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        _check(self._lib.orc_set_draft_fp8(self._h, _ptr(sk)), "orc_set_draft_fp8")
 
     def cache(self, capacity: int) -> "Cache":
         return Cache(self, capacity)

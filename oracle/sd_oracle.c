@@ -23,10 +23,16 @@
 #include <omp.h>
 #endif
 
+enum { FP8_QKV = 0, FP8_O = 1, FP8_GATE_UP = 2, FP8_DOWN = 3, FP8_KINDS = 4 };
+
 struct orc_model {
     orc_config c;
     const void *tok_emb, *final_norm, *lm_head;
     const void **attn_norm, **w_qkv, **w_o, **mlp_norm, **w_gate_up, **w_down;
+    /* FP8 draft copies (orc_set_draft_fp8): per kind and layer, the E4M3
+     * bytes [N][K] and the per-row scale exponents [N], or NULL */
+    uint8_t **fp8_q[FP8_KINDS];
+    int32_t **fp8_e[FP8_KINDS];
 };
 
 struct orc_cache {
@@ -107,10 +113,13 @@ orc_model *orc_create(const orc_config *cfg, const orc_weights *w)
     return m;
 }
 
+static void free_draft_fp8(orc_model *m);
+
 void orc_destroy(orc_model *m)
 {
     if (!m)
         return;
+    free_draft_fp8(m);
     free((void *)m->attn_norm);
     free((void *)m->w_qkv);
     free((void *)m->w_o);
@@ -219,6 +228,41 @@ static void linear(const orc_model *m, const void *W, int64_t N, int64_t K, cons
         }
         free(row);
     }
+}
+
+/* The same with FP8 draft weights: W[n][k] = value(q[n][k]) * 2^e[n], every
+ * output again a sequential sum over k. */
+static void linear_fp8(const uint8_t *q, const int32_t *e, int64_t N, int64_t K, const double *x, int nr, double *y)
+{
+#pragma omp parallel
+    {
+        double *row = (double *)malloc(sizeof(double) * (size_t)K);
+#pragma omp for schedule(static)
+        for (int64_t n = 0; n < N; ++n) {
+            for (int64_t k = 0; k < K; ++k)
+                row[k] = ldexp(orc_fp8_value(q[n * K + k]), e[n]);
+            for (int r = 0; r < nr; ++r) {
+                const double *xr = x + (int64_t)r * K;
+                double acc = 0.0;
+                for (int64_t k = 0; k < K; ++k)
+                    acc += row[k] * xr[k];
+                y[(int64_t)r * N + n] = acc;
+            }
+        }
+        free(row);
+    }
+}
+
+/* A linear layer of a draft forward (skip mask given) reads the FP8 copy
+ * when the model has one for (kind, layer); every other forward reads the
+ * stored weights. */
+static void linear_layer(const orc_model *m, int kind, int l, const uint8_t *skip, const void *W, int64_t N,
+                         int64_t K, const double *x, int nr, double *y)
+{
+    if (skip && m->fp8_q[kind] && m->fp8_q[kind][l])
+        linear_fp8(m->fp8_q[kind][l], m->fp8_e[kind][l], N, K, x, nr, y);
+    else
+        linear(m, W, N, K, x, nr, y);
 }
 
 /* RMSNorm: u = g * h / sqrt(mean(h^2) + eps). */
@@ -366,7 +410,7 @@ int orc_forward(orc_model *m, orc_cache *c, const int32_t *tokens, int32_t n, co
         if (!(skip && skip[2 * l])) {
             for (int r = 0; r < n; ++r)
                 rmsnorm(m, m->attn_norm[l], h + (int64_t)r * d, u + (int64_t)r * d);
-            linear(m, m->w_qkv[l], nqkv, d, u, n, qkv);
+            linear_layer(m, FP8_QKV, l, skip, m->w_qkv[l], nqkv, d, u, n, qkv);
             /* all rows of the block write their K/V first, then attend */
             for (int r = 0; r < n; ++r) {
                 double *row = qkv + (int64_t)r * nqkv;
@@ -389,20 +433,20 @@ int orc_forward(orc_model *m, orc_cache *c, const int32_t *tokens, int32_t n, co
                     attend(c, l, qkv + (int64_t)r * nqkv, start + r, o + (int64_t)r * H * dh, scores);
                 free(scores);
             }
-            linear(m, m->w_o[l], d, (int64_t)H * dh, o, n, t);
+            linear_layer(m, FP8_O, l, skip, m->w_o[l], d, (int64_t)H * dh, o, n, t);
             for (int64_t i = 0; i < (int64_t)n * d; ++i)
                 h[i] += t[i];
         }
         if (!(skip && skip[2 * l + 1])) {
             for (int r = 0; r < n; ++r)
                 rmsnorm(m, m->mlp_norm[l], h + (int64_t)r * d, u + (int64_t)r * d);
-            linear(m, m->w_gate_up[l], 2 * (int64_t)F, d, u, n, gu);
+            linear_layer(m, FP8_GATE_UP, l, skip, m->w_gate_up[l], 2 * (int64_t)F, d, u, n, gu);
             for (int r = 0; r < n; ++r)
                 for (int f = 0; f < F; ++f) {
                     const double *gr = gu + (int64_t)r * 2 * F;
                     mm[(int64_t)r * F + f] = silu(gr[f]) * gr[F + f];
                 }
-            linear(m, m->w_down[l], d, F, mm, n, t);
+            linear_layer(m, FP8_DOWN, l, skip, m->w_down[l], d, F, mm, n, t);
             for (int64_t i = 0; i < (int64_t)n * d; ++i)
                 h[i] += t[i];
         }
@@ -1003,4 +1047,130 @@ int orc_generate_sd_sample(orc_model *m, const int32_t *prompt, int32_t t, int32
     free(p);
     free(lg);
     return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* FP8 draft weights.  The adaptation appendix (Quantization subsection and
+ * table) runs self-speculative decoding on LLM.int8() FP8/FP4 weights to cut
+ * memory.  Here only a copy of the draft's weights is quantized, to stream
+ * half the bytes per draft step; the verification keeps the stored bf16
+ * weights, so the emitted tokens are still exactly those of greedy decoding
+ * of the original model, and only the drafts (hence the stage trace) follow
+ * the quantized copy.
+ *
+ * Format: OCP FP8 E4M3 (1 sign bit, 4 exponent bits with bias 7, 3 mantissa
+ * bits; exponent field 0 subnormal; S.1111.111 NaN; largest value 448), one
+ * power-of-two scale 2^e per output row: e is the smallest integer with
+ * max_k |W[n][k]| * 2^-e <= 448, so scaling is exact and the stored byte is
+ * the nearest E4M3 value (ties to even) of W[n][k] * 2^-e. */
+
+double orc_fp8_value(uint8_t b)
+{
+    const int sgn = b >> 7, f = (b >> 3) & 15, mt = b & 7;
+    if (f == 15 && mt == 7)
+        return NAN;
+    const double v = f == 0 ? ldexp((double)mt, -9) : ldexp(1.0 + (double)mt / 8.0, f - 7);
+    return sgn ? -v : v;
+}
+
+/* The byte of the nearest E4M3 value (ties to even) of v, |v| <= 448. */
+static uint8_t fp8_encode(double v)
+{
+    const uint8_t sgn = signbit(v) ? 0x80 : 0;
+    const double a = fabs(v);
+    if (a == 0.0)
+        return sgn;
+    int e;
+    (void)frexp(a, &e); /* a = f 2^e, 0.5 <= f < 1: floor(log2 a) = e - 1 */
+    const int quantum = e - 1 < -6 ? -9 : e - 1 - 3;
+    const double r = ldexp(rint(ldexp(a, -quantum)), quantum); /* rint: to nearest, ties to even */
+    if (r == 0.0)
+        return sgn;
+    (void)frexp(r, &e);
+    const int ex = e - 1;
+    if (ex < -6)
+        return sgn | (uint8_t)ldexp(r, 9);
+    return sgn | (uint8_t)((ex + 7) << 3) | (uint8_t)(ldexp(r, -ex) * 8.0 - 8.0);
+}
+
+/* The smallest e with amax * 2^-e <= 448 = 0.875 * 2^9; 0 for amax = 0. */
+static int32_t fp8_row_exponent(double amax)
+{
+    if (amax == 0.0)
+        return 0;
+    int e;
+    const double f = frexp(amax, &e);
+    return e - 9 + (f > 0.875 ? 1 : 0);
+}
+
+int orc_quantize_fp8_rows(const uint16_t *w, int64_t n_rows, int64_t n_cols, uint8_t *q, int32_t *e)
+{
+    if (!w || !q || !e || n_rows < 0 || n_cols < 1)
+        return -1;
+    for (int64_t n = 0; n < n_rows; ++n) {
+        double amax = 0.0;
+        for (int64_t k = 0; k < n_cols; ++k) {
+            const double a = fabs(bf16_to_double(w[n * n_cols + k]));
+            if (a > amax)
+                amax = a;
+        }
+        e[n] = fp8_row_exponent(amax);
+        for (int64_t k = 0; k < n_cols; ++k)
+            q[n * n_cols + k] = fp8_encode(ldexp(bf16_to_double(w[n * n_cols + k]), -e[n]));
+    }
+    return 0;
+}
+
+static void free_draft_fp8(orc_model *m)
+{
+    for (int k = 0; k < FP8_KINDS; ++k) {
+        for (int l = 0; m->fp8_q[k] && l < m->c.n_layers; ++l) {
+            free(m->fp8_q[k][l]);
+            free(m->fp8_e[k][l]);
+        }
+        free(m->fp8_q[k]);
+        free(m->fp8_e[k]);
+        m->fp8_q[k] = NULL;
+        m->fp8_e[k] = NULL;
+    }
+}
+
+int orc_set_draft_fp8(orc_model *m, const uint8_t *skip)
+{
+    if (!m || m->c.wdtype != 1)
+        return -1;
+    free_draft_fp8(m);
+    if (!skip)
+        return 0;
+    const int L = m->c.n_layers, d = m->c.d_model, hd = m->c.n_heads * m->c.head_dim, F = m->c.ffn_dim;
+    const int64_t nqkv = (int64_t)(m->c.n_heads + 2 * m->c.n_kv_heads) * m->c.head_dim;
+    for (int i = 0; i < 2 * L; ++i)
+        if (skip[i] > 1)
+            return -1;
+    for (int k = 0; k < FP8_KINDS; ++k) {
+        m->fp8_q[k] = (uint8_t **)calloc((size_t)L, sizeof(uint8_t *));
+        m->fp8_e[k] = (int32_t **)calloc((size_t)L, sizeof(int32_t *));
+        if (!m->fp8_q[k] || !m->fp8_e[k]) {
+            free_draft_fp8(m);
+            return -3;
+        }
+    }
+    for (int l = 0; l < L; ++l) {
+        const void *w[FP8_KINDS] = {m->w_qkv[l], m->w_o[l], m->w_gate_up[l], m->w_down[l]};
+        const int64_t rows[FP8_KINDS] = {nqkv, d, 2 * (int64_t)F, d};
+        const int64_t cols[FP8_KINDS] = {d, hd, d, F};
+        for (int k = 0; k < FP8_KINDS; ++k) {
+            const int run = k < FP8_GATE_UP ? !skip[2 * l] : !skip[2 * l + 1];
+            if (!run)
+                continue;
+            m->fp8_q[k][l] = (uint8_t *)malloc((size_t)(rows[k] * cols[k]));
+            m->fp8_e[k][l] = (int32_t *)malloc(sizeof(int32_t) * (size_t)rows[k]);
+            if (!m->fp8_q[k][l] || !m->fp8_e[k][l]) {
+                free_draft_fp8(m);
+                return -3;
+            }
+            orc_quantize_fp8_rows((const uint16_t *)w[k], rows[k], cols[k], m->fp8_q[k][l], m->fp8_e[k][l]);
+        }
+    }
+    return 0;
 }

@@ -168,6 +168,28 @@ int orc_generate_sd_sample(orc_model *m, const int32_t *prompt, int32_t t, int32
 int orc_generate_ar_sample(orc_model *m, const int32_t *prompt, int32_t t, int32_t max_new,
                            const orc_sampling *sp, int32_t *out, double *margin);
 
+/* ------------------------------------------------------------------------
+ * FP8 draft weights (the adaptation appendix combines self-speculative
+ * decoding with FP8 and FP4 weights; here only a copy of the draft's
+ * weights is quantized, and verification keeps the stored bf16 weights).
+ * OCP FP8 E4M3 with one power-of-two scale 2^e per output row, e the
+ * smallest integer with max|W[n][:]| * 2^-e <= 448; the byte is the nearest
+ * E4M3 value (ties to even) of W[n][k] * 2^-e.
+ */
+
+/* The value of an E4M3 byte (NaN for S.1111.111). */
+double orc_fp8_value(uint8_t b);
+
+/* Quantizes a bf16 matrix [n_rows][n_cols]: bytes q [n_rows][n_cols],
+ * exponents e [n_rows]. */
+int orc_quantize_fp8_rows(const uint16_t *w, int64_t n_rows, int64_t n_cols, uint8_t *q, int32_t *e);
+
+/* bf16 models: quantizes the QKV, output, gate/up and down weights of the
+ * sublayers skip keeps (0 entries); from then on every forward with a skip
+ * mask (a draft forward) reads those copies, and the full model the stored
+ * weights.  skip == NULL removes them.  Errors: -1 argument, -3 memory. */
+int orc_set_draft_fp8(orc_model *m, const uint8_t *skip);
+
 #ifdef __cplusplus
 }
 #endif

@@ -169,6 +169,46 @@ def test_planted_sampling_mistake_is_caught(name, tmp_path):
     assert not _sampling_pins_hold(lib), f"planted mistake {name} passed every sampling pin"
 
 
+# Mistakes in the FP8 draft weights, caught by the pins of test_oracle_fp8.py.
+FP8_MUTATIONS = {
+    "fp8_ties_away": ("const double r = ldexp(rint(ldexp(a, -quantum)), quantum);",
+                      "const double r = ldexp(floor(ldexp(a, -quantum) + 0.5), quantum);"),
+    "fp8_scale_not_smallest": ("return e - 9 + (f > 0.875 ? 1 : 0);", "return e - 8 + (f > 0.875 ? 1 : 0);"),
+    "fp8_subnormal_quantum": ("const int quantum = e - 1 < -6 ? -9 : e - 1 - 3;",
+                              "const int quantum = e - 1 < -6 ? -10 : e - 1 - 3;"),
+    "fp8_exponent_bias": ("ldexp(1.0 + (double)mt / 8.0, f - 7)", "ldexp(1.0 + (double)mt / 8.0, f - 8)"),
+    "fp8_on_full_model": ("if (skip && m->fp8_q[kind] && m->fp8_q[kind][l])", "if (m->fp8_q[kind] && m->fp8_q[kind][l])"),
+    "fp8_sublayer_swap": ("const int run = k < FP8_GATE_UP ? !skip[2 * l] : !skip[2 * l + 1];",
+                          "const int run = k < FP8_GATE_UP ? !skip[2 * l + 1] : !skip[2 * l];"),
+}
+
+
+def _fp8_pins_hold(lib_path) -> bool:
+    from tests import test_oracle_fp8 as P
+
+    try:
+        for check in P.ALL_CHECKS:
+            check(lib_path=lib_path)
+        return True
+    except (oracle.OracleError, AssertionError, IndexError, ValueError):
+        return False
+
+
+def test_unmodified_oracle_passes_fp8_pins():
+    assert _fp8_pins_hold(oracle.LIB_PATH)
+
+
+@pytest.mark.parametrize("name", sorted(FP8_MUTATIONS))
+def test_planted_fp8_mistake_is_caught(name, tmp_path):
+    old, new = FP8_MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    mutated = tmp_path / "sd_oracle.c"
+    mutated.write_text(src.replace(old, new))
+    lib = oracle.build(src=str(mutated), out=str(tmp_path / f"liboracle_{name}.so"))
+    assert not _fp8_pins_hold(lib), f"planted mistake {name} passed every FP8 pin"
+
+
 # Mistakes in the skip-set search, caught by the pins of test_oracle_search.py.
 SEARCH_SRC = os.path.join(os.path.dirname(oracle.__file__), "skip_search.py")
 SEARCH_MUTATIONS = {
