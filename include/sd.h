@@ -187,6 +187,33 @@ sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const ui
 sd_status sd_forward_static(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
                             sd_kv_cache *cache, float *logits);
 
+/* FP8 draft weights.  The adaptation appendix (Quantization subsection and
+ * table) combines self-speculative decoding with FP8 and FP4 weights to cut
+ * memory.  Here only a copy of the draft's weights is quantized, so that a
+ * draft step streams one byte per weight; the verification keeps the
+ * stored bf16 weights, so the emitted tokens are still exactly those of
+ * greedy decoding of the original model (only drafts and stage traces
+ * follow the copy).  This trades the "no extra memory" property of the
+ * plain draft for speed: one byte per quantized weight and four bytes per
+ * row.
+ *
+ * Quantizes the QKV, output, gate/up and down weights of every sublayer
+ * skip_mask (HOST, layout of sd_forward) keeps to OCP FP8 E4M3 with one
+ * power-of-two scale 2^e per output row (e the smallest integer with
+ * max|W[n][:]| 2^-e <= 448; each byte the nearest E4M3 value of
+ * W[n][k] 2^-e, ties to even).  From then on every one-row forward with a
+ * skip mask (the draft steps of the generate calls, sd_forward of one row
+ * with a mask) reads the copy of each sublayer that has one; forwards
+ * without a mask read the bf16 weights, and sd_forward refuses masked
+ * forwards of more than one row.  skip_mask NULL removes the copies.
+ * bfloat16 models only.  Errors: INVALID_ARG, OOM, DEVICE. */
+sd_status sd_model_quantize_draft(sd_model *model, const uint8_t *skip_mask);
+/* The FP8 copy of (layer, kind), kind 0 QKV, 1 output, 2 gate/up, 3 down:
+ * DEVICE bytes [N][K] and exponents int32 [N], or NULL when the sublayer
+ * has none (for inspection). */
+sd_status sd_model_draft_fp8(const sd_model *model, int32_t layer, int32_t kind, const void **q,
+                             const int32_t **exps);
+
 /* Greedy self-speculative decoding (Algorithm 2, static gamma exit of
  * Sec. 3.4) of max_new tokens after a HOST prompt of prompt_len >= 1 ids.
  * The prompt minus its last token is prefilled; every stage drafts at

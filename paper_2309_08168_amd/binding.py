@@ -25,7 +25,8 @@ EXPORTS = (
     "sd_kv_cache_length", "sd_kv_cache_truncate", "sd_kv_cache_set_length", "sd_forward", "sd_forward_static",
     "sd_self_spec_generate", "sd_self_spec_generate_adaptive", "sd_autoregressive_generate",
     "sd_self_spec_sample", "sd_autoregressive_sample", "sd_search_skip_set_fn", "sd_search_skip_set",
-    "sd_model_time_kernel", "sd_model_kernel_time", "sd_measure_read_bandwidth",
+    "sd_model_time_kernel", "sd_model_kernel_time", "sd_measure_read_bandwidth", "sd_model_quantize_draft",
+    "sd_model_draft_fp8",
     "sd_last_error", "sd_version",
 )
 
@@ -140,6 +141,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "sd_model_time_kernel": ([vp, i32, i32], ctypes.c_int),
         "sd_model_kernel_time": ([vp, p(ctypes.c_int64), p(ctypes.c_double), ctypes.c_char_p, i32,
                                   p(ctypes.c_int64), p(ctypes.c_int64)], ctypes.c_int),
+        "sd_model_quantize_draft": ([vp, vp], ctypes.c_int),
+        "sd_model_draft_fp8": ([vp, i32, i32, p(vp), p(vp)], ctypes.c_int),
         "sd_measure_read_bandwidth": ([vp, ctypes.c_size_t, i32, i32, i32, vp, vp, p(ctypes.c_double)], ctypes.c_int),
         "sd_last_error": ([], ctypes.c_char_p),
         "sd_version": ([], ctypes.c_char_p),
@@ -272,6 +275,33 @@ class Model:
         lp = None if logits is None else ctypes.c_void_p(logits.data_ptr())
         check(load().sd_forward_static(self._h, _ptr(tok), tok.size, _ptr(sk), cache._h, lp))
         return logits
+
+    def quantize_draft(self, skip):
+        """sd_model_quantize_draft: FP8 copies of the weights of the sublayers
+        skip keeps (None removes them)."""
+        sk = None if skip is None else np.ascontiguousarray(skip, dtype=np.uint8)
+        check(load().sd_model_quantize_draft(self._h, _ptr(sk)))
+
+    def draft_fp8(self, layer: int, kind: int):
+        """(bytes uint8 [N][K], exponents int32 [N]) of a quantized draft
+        matrix copied to the host, or None; kind 0 QKV, 1 O, 2 gate/up, 3 down."""
+        import torch
+
+        q, e = ctypes.c_void_p(), ctypes.c_void_p()
+        check(load().sd_model_draft_fp8(self._h, layer, kind, ctypes.byref(q), ctypes.byref(e)))
+        if not q.value:
+            return None
+        c = self.cfg
+        rows = [(c.n_heads + 2 * c.n_kv_heads) * c.head_dim, c.d_model, 2 * c.ffn_dim, c.d_model][kind]
+        cols = [c.d_model, c.n_heads * c.head_dim, c.d_model, c.ffn_dim][kind]
+        torch.cuda.synchronize()
+        qb = np.empty((rows, cols), np.uint8)
+        eb = np.empty(rows, np.int32)
+        hip = ctypes.CDLL("libamdhip64.so")
+        hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        if hip.hipMemcpy(qb.ctypes.data, q, qb.nbytes, 2) or hip.hipMemcpy(eb.ctypes.data, e, eb.nbytes, 2):
+            raise RuntimeError("hipMemcpy of the FP8 copy failed")
+        return qb, eb
 
     def _sd_call(self, fn, prompt, max_new, skip, k_max, rule, log_cap):
         pr = np.ascontiguousarray(prompt, dtype=np.int32)

@@ -562,6 +562,181 @@ __global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// FP8 draft weights.  The adaptation appendix runs self-speculative decoding
+// on FP8 and FP4 weights; here a copy of the draft's weights is quantized so
+// that a draft step streams one byte per weight, while verification keeps
+// the stored bf16 weights (the output stays exactly greedy bf16 decoding).
+// Format: OCP FP8 E4M3 (bias 7, largest value 448, S.1111.111 NaN) with one
+// power-of-two scale 2^e per output row, e the smallest integer with
+// max|W[n][:]| 2^-e <= 448; the byte is the nearest E4M3 value (ties to
+// even) of W[n][k] 2^-e.  Scaling by 2^-e is exact, so every step is.
+
+// The E4M3 byte of v, |v| <= 448, to nearest with ties to even.
+__device__ __forceinline__ uint32_t fp8_encode(float v) {
+    const uint32_t sgn = (__float_as_uint(v) >> 24) & 0x80u;
+    const float a = fabsf(v);
+    if (a == 0.0f)
+        return sgn;
+    int e;
+    (void)frexpf(a, &e);  // a = f 2^e, 0.5 <= f < 1
+    const int quantum = e - 1 < -6 ? -9 : e - 4;
+    const float r = ldexpf(rintf(ldexpf(a, -quantum)), quantum);  // rintf: ties to even
+    if (r == 0.0f)
+        return sgn;
+    (void)frexpf(r, &e);
+    const int ex = e - 1;
+    if (ex < -6)
+        return sgn | (uint32_t)ldexpf(r, 9);
+    return sgn | (uint32_t)((ex + 7) << 3) | (uint32_t)(ldexpf(r, -ex) * 8.0f - 8.0f);
+}
+
+// One work-group per row: the row's largest magnitude, its exponent, then
+// the bytes.
+__global__ __launch_bounds__(256) void k_quantize_fp8(const uint16_t *W, int32_t K, uint8_t *Q, int32_t *E) {
+    __shared__ float red[4];
+    const int64_t n = blockIdx.x;
+    const uint16_t *w = W + n * K;
+    float amax = 0.0f;
+    for (int k = threadIdx.x; k < K; k += 256)
+        amax = fmaxf(amax, fabsf(bf2f(w[k])));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+    if ((threadIdx.x & 63) == 0)
+        red[threadIdx.x >> 6] = amax;
+    __syncthreads();
+    amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    int e = 0;
+    if (amax > 0.0f) {
+        int ea;
+        const float f = frexpf(amax, &ea);  // amax = f 2^ea; 448 = 0.875 2^9
+        e = ea - 9 + (f > 0.875f ? 1 : 0);
+    }
+    if (threadIdx.x == 0)
+        E[n] = e;
+    for (int k = threadIdx.x; k < K; k += 256)
+        Q[n * K + k] = (uint8_t)fp8_encode(ldexpf(bf2f(w[k]), -e));
+}
+
+hipError_t launch_quantize_fp8(const uint16_t *W, int32_t N, int32_t K, uint8_t *Q, int32_t *E, hipStream_t s) {
+    if (N < 1 || K < 1)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_quantize_fp8, dim3(N), dim3(256), 0, s, W, K, Q, E);
+    return hipGetLastError();
+}
+
+// One-row GEMV over FP8 weights (draft steps): a tile of R weight rows per
+// work-group of four waves; each thread takes 16 consecutive elements of the
+// reduction per step, one 16-byte load per weight row, converted to float32
+// exactly by the hardware.  RMSNorm is folded in as in k_linear_valu; the
+// row's 2^e scales its dot product before the shared epilogues.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+template <int R, int EPI, bool NORM>
+__global__ __launch_bounds__(256) void k_linear_fp8(LinearArgs a) {
+    constexpr int NV = R + (NORM ? 1 : 0);
+    __shared__ float red[4][NV];
+    __shared__ float fin[R];
+    __shared__ float inv_s[1];
+    const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int K = a.K, nch = K >> 4;
+    const uint8_t *W = reinterpret_cast<const uint8_t *>(a.W);
+    const uint16_t *G = reinterpret_cast<const uint16_t *>(a.gain);
+    int rows[R];
+    int64_t roff[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        rows[i] = row_valid<EPI>(t, i, R, a.N, a.epi) ? tile_row<EPI>(t, i, R, a.epi) : 0;
+        roff[i] = (int64_t)rows[i] * K;
+    }
+    float acc[R], ss = 0.0f;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        acc[i] = 0.0f;
+    for (int c = tid; c < nch; c += 256) {
+        u32x4_t wr[R], gr[2];
+        f32x4_t xr[4];
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            wr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(W + roff[i] + (int64_t)c * 16));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            xr[j] = reinterpret_cast<const f32x4_t *>(a.X + (int64_t)c * 16)[j];
+        if constexpr (NORM) {
+            gr[0] = reinterpret_cast<const u32x4_t *>(G + c * 16)[0];
+            gr[1] = reinterpret_cast<const u32x4_t *>(G + c * 16)[1];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        float x[16];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                x[4 * j + k] = xr[j][k];
+        if constexpr (NORM) {
+            float g[2][8];
+            unpack8(gr[0], g[0]);
+            unpack8(gr[1], g[1]);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                ss = fmaf(x[k], x[k], ss);
+                x[k] *= g[k >> 3][k & 7];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)wr[i][j], false);
+                const f32x2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)wr[i][j], true);
+                acc[i] = fmaf(lo[0], x[4 * j], acc[i]);
+                acc[i] = fmaf(lo[1], x[4 * j + 1], acc[i]);
+                acc[i] = fmaf(hi[0], x[4 * j + 2], acc[i]);
+                acc[i] = fmaf(hi[1], x[4 * j + 3], acc[i]);
+            }
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const float v = wave_sum(acc[i]);
+        if (lane == 0)
+            red[wave][i] = v;
+    }
+    if constexpr (NORM) {
+        const float v = wave_sum(ss);
+        if (lane == 0)
+            red[wave][R] = v;
+    }
+    __syncthreads();
+    auto waves_sum = [&](int j) { return (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]); };
+    if (tid < R)
+        fin[tid] = ldexpf(waves_sum(tid), a.wexp[rows[tid]]);
+    if (tid == 0)
+        inv_s[0] = NORM ? 1.0f / sqrtf(waves_sum(R) / (float)K + a.eps) : 1.0f;
+    __syncthreads();
+    // a cancelled step (ctl->m = 0) writes nothing; see k_linear_valu
+    run_epilogue<uint16_t, EPI>(a, fin, R, 1, inv_s, t, a.guarded ? a.ctl->m : 1);
+}
+
+template <int R>
+static hipError_t launch_fp8_r(const LinearArgs &a, int epi, int n_tiles, hipStream_t s, const LaunchTiming &t) {
+    dim3 grid(n_tiles), block(256);
+    switch (epi) {
+    case EPI_RESID:
+        launch_k(k_linear_fp8<R, EPI_RESID, false>, grid, block, s, t, a);
+        break;
+    case EPI_SWIGLU:
+        launch_k(k_linear_fp8<R, EPI_SWIGLU, true>, grid, block, s, t, a);
+        break;
+    case EPI_QKV:
+        launch_k(k_linear_fp8<R, EPI_QKV, true>, grid, block, s, t, a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // MFMA main loop (bf16 weights, up to 16 rows).  A work-group owns TN tiles
 // of 16 weight rows and the whole reduction dimension (or one of S slices of
 // it); its NW waves take every NW-th 128-element k-step, so at any time the
@@ -981,6 +1156,15 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
         LinearArgs b = a;
         b.n_tiles = n_tiles;
         return launch_mfma_np(b, epi, n_tiles, s, t);
+    }
+    if (path == PATH_GEMV_FP8) {
+        if (!bf16 || (a.K & 15) || !a.wexp)
+            return hipErrorInvalidValue;
+        if (rows_per_tile == 4)
+            return launch_fp8_r<4>(a, epi, n_tiles, s, t);
+        if (rows_per_tile == 8)
+            return launch_fp8_r<8>(a, epi, n_tiles, s, t);
+        return hipErrorInvalidValue;
     }
     if (a.K & 7)
         return hipErrorInvalidValue;

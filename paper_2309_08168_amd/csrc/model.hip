@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -114,6 +115,11 @@ struct sd_model {
     Plan planm[LK_COUNT];  // up to 16 rows (longer verification, prefill)
     Workspace ws;           // scratch of the decode-path forwards
     int max_head_tiles = 1; // lm-head tiles of the widest plan
+    // FP8 copies of the draft's weights (sd_model_quantize_draft), per layer
+    // and kind (QKV, O, gate/up, down): E4M3 bytes and row exponents, or null
+    std::vector<std::array<uint8_t *, 4>> fp8_q;
+    std::vector<std::array<int32_t *, 4>> fp8_e;
+    bool has_fp8 = false;
     // sampling variant: logits of the verification / autoregressive rows and
     // of the stage's drafts, the rows' nucleus statistics, the parameters
     float *slog_v = nullptr, *slog_d = nullptr;
@@ -365,9 +371,11 @@ sd_status launch(hipError_t e, const char *what) {
 // reads the bf16 term planes xs (g * h from k_prep_norm, the layer dividing
 // by rms(h) itself, or split by the producer for the output projections).
 sd_status run_linear(sd_model *m, const Workspace &w, const Plan &p, int max_rows, const void *W, const float *X,
-                     int64_t ldx, const void *gain, const EpiArgs &epi, const uint16_t *xs, bool guarded = false) {
+                     int64_t ldx, const void *gain, const EpiArgs &epi, const uint16_t *xs, bool guarded = false,
+                     const int32_t *wexp = nullptr) {
     LinearArgs a{};
     a.guarded = guarded ? 1 : 0;
+    a.wexp = wexp;
     a.W = W;
     a.N = p.N;
     a.K = p.K;
@@ -391,7 +399,7 @@ sd_status run_linear(sd_model *m, const Workspace &w, const Plan &p, int max_row
     a.part = w.part;
     a.n_tiles = p.n_tiles;
     const bool timed = m->timed_now && p.kind == m->timed_kind && p.regime == m->timed_regime &&
-                       m->tev_used + 2 <= 2 * 65536;
+                       p.path != PATH_GEMV_FP8 && m->tev_used + 2 <= 2 * 65536;
     if (timed) {
         if (m->tev_used + 2 > m->tev.size()) {
             for (int i = 0; i < 256; ++i) {
@@ -484,6 +492,18 @@ sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap,
     const int64_t ldh = c.d_model, ldq = (int64_t)c.n_heads * c.head_dim;
     const size_t ksz = m->wsize;
     const int64_t head_stride = (int64_t)cap * c.head_dim;
+    // one-row draft forwards read the draft's FP8 copy of a layer where it has one
+    const bool fp8 = m->has_fp8 && skip && max_rows == 1;
+    auto lin = [&](int kind, int l, const void *W, const float *X, int64_t ldx, const void *gain, const EpiArgs &e,
+                   const uint16_t *xs) {
+        if (fp8 && m->fp8_q[l][kind]) {
+            Plan q = P[kind];
+            q.path = PATH_GEMV_FP8;
+            return run_linear(m, w, q, max_rows, m->fp8_q[l][kind], X, ldx, gain, e, xs, cur->guarded,
+                              m->fp8_e[l][kind]);
+        }
+        return run_linear(m, w, P[kind], max_rows, W, X, ldx, gain, e, xs, cur->guarded);
+    };
     for (int l = cur->next_layer; l < layer_end; ++l) {
         if (!(skip && skip[2 * l])) {
             char *kbase = static_cast<char *>(kv) + (size_t)(2 * l) * c.n_kv_heads * head_stride * ksz;
@@ -500,7 +520,7 @@ sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap,
             e.head_dim = c.head_dim;
             e.ffn = c.ffn_dim;
             SD_TRY(prep_norm(m, w, P[LK_QKV], m->attn_norm[l], pending));
-            SD_TRY(run_linear(m, w, P[LK_QKV], max_rows, m->w_qkv[l], w.h, ldh, m->attn_norm[l], e, w.xa, cur->guarded));
+            SD_TRY(lin(LK_QKV, l, m->w_qkv[l], w.h, ldh, m->attn_norm[l], e, w.xa));
             AttnArgs at{};
             at.q = w.q;
             at.ld_q = ldq;
@@ -524,7 +544,7 @@ sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap,
             EpiArgs eo{};
             eo.out = w.h;
             eo.ld_out = ldh;
-            SD_TRY(run_linear(m, w, P[LK_O], max_rows, m->w_o[l], w.o, ldq, nullptr, eo, w.xa, cur->guarded));
+            SD_TRY(lin(LK_O, l, m->w_o[l], w.o, ldq, nullptr, eo, w.xa));
             if (P[LK_O].epi == EPI_PARTIAL)
                 pending = P[LK_O].splits;
         }
@@ -538,11 +558,11 @@ sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap,
                 eg.ld_out = w.xld;
             }
             SD_TRY(prep_norm(m, w, P[LK_GATE_UP], m->mlp_norm[l], pending));
-            SD_TRY(run_linear(m, w, P[LK_GATE_UP], max_rows, m->w_gate_up[l], w.h, ldh, m->mlp_norm[l], eg, w.xa, cur->guarded));
+            SD_TRY(lin(LK_GATE_UP, l, m->w_gate_up[l], w.h, ldh, m->mlp_norm[l], eg, w.xa));
             EpiArgs ed{};
             ed.out = w.h;
             ed.ld_out = ldh;
-            SD_TRY(run_linear(m, w, P[LK_DOWN], max_rows, m->w_down[l], w.mbuf, c.ffn_dim, nullptr, ed, w.xb, cur->guarded));
+            SD_TRY(lin(LK_DOWN, l, m->w_down[l], w.mbuf, c.ffn_dim, nullptr, ed, w.xb));
             if (P[LK_DOWN].epi == EPI_PARTIAL)
                 pending = P[LK_DOWN].splits;
         }
@@ -1113,6 +1133,8 @@ sd_status forward(sd_model *m, const int32_t *tokens, int32_t n, const uint8_t *
         return fail(SD_ERR_INVALID_ARG, "n must be >= 1");
     SD_TRY(check_tokens(m, tokens, n, "tokens"));
     SD_TRY(check_mask(m, skip));
+    if (skip && n > 1 && m->has_fp8)
+        return fail(SD_ERR_INVALID_ARG, "while the draft is quantized, forwards with a skip mask take one row");
     if ((int64_t)kc->len + n > kc->cap)
         return fail(SD_ERR_CAPACITY, "cache of capacity " + std::to_string(kc->cap) + " holds " +
                                          std::to_string(kc->len) + " positions; " + std::to_string(n) +
@@ -1217,6 +1239,8 @@ sd_status forward_static(sd_model *m, const int32_t *tokens, int32_t n, const ui
         return fail(SD_ERR_INVALID_ARG, "n must be in [1, " + std::to_string(MAX_ROWS) + "]");
     SD_TRY(check_tokens(m, tokens, n, "tokens"));
     SD_TRY(check_mask(m, skip));
+    if (skip && n > 1 && m->has_fp8)
+        return fail(SD_ERR_INVALID_ARG, "while the draft is quantized, forwards with a skip mask take one row");
     if ((int64_t)kc->len + n > kc->cap)
         return fail(SD_ERR_CAPACITY, "cache of capacity " + std::to_string(kc->cap) + " holds " +
                                          std::to_string(kc->len) + " positions; " + std::to_string(n) +
@@ -1252,6 +1276,65 @@ sd_status forward_static(sd_model *m, const int32_t *tokens, int32_t n, const ui
     return SD_OK;
 }
 
+void free_draft_fp8(sd_model *m) {
+    for (auto &a : m->fp8_q)
+        for (uint8_t *&p : a) {
+            dev_free(p);
+            p = nullptr;
+        }
+    for (auto &a : m->fp8_e)
+        for (int32_t *&p : a) {
+            dev_free(p);
+            p = nullptr;
+        }
+    m->has_fp8 = false;
+}
+
+// FP8 copies of the weights of the sublayers skip keeps (see k_quantize_fp8).
+sd_status quantize_draft(sd_model *m, const uint8_t *skip) {
+    if (!m)
+        return fail(SD_ERR_INVALID_ARG, "model is null");
+    SD_TRY(check_mask(m, skip));
+    if (skip && !m->bf16)
+        return fail(SD_ERR_INVALID_ARG, "FP8 draft weights are made from bfloat16 weights");
+    const sd_config &c = m->cfg;
+    if (skip && (c.d_model % 16 || (c.n_heads * c.head_dim) % 16 || c.ffn_dim % 16))
+        return fail(SD_ERR_INVALID_ARG, "FP8 draft weights need d_model, n_heads * head_dim and ffn_dim multiples of 16");
+    SD_HIP(hipStreamSynchronize(m->stream));
+    free_draft_fp8(m);
+    if (!skip)
+        return SD_OK;
+    const int L = c.n_layers;
+    const int32_t rows[4] = {(c.n_heads + 2 * c.n_kv_heads) * c.head_dim, c.d_model, 2 * c.ffn_dim, c.d_model};
+    const int32_t cols[4] = {c.d_model, c.n_heads * c.head_dim, c.d_model, c.ffn_dim};
+    for (int l = 0; l < L; ++l) {
+        const void *W[4] = {m->w_qkv[l], m->w_o[l], m->w_gate_up[l], m->w_down[l]};
+        for (int k = 0; k < 4; ++k) {
+            if (skip[2 * l + (k < LK_GATE_UP ? 0 : 1)])
+                continue;
+            sd_status st = dev_alloc(&m->fp8_q[l][k], (size_t)rows[k] * cols[k]);
+            if (st == SD_OK)
+                st = dev_alloc(&m->fp8_e[l][k], (size_t)rows[k]);
+            if (st == SD_OK)
+                st = launch(launch_quantize_fp8(static_cast<const uint16_t *>(W[k]), rows[k], cols[k], m->fp8_q[l][k],
+                                                m->fp8_e[l][k], m->stream),
+                            "FP8 quantization");
+            if (st != SD_OK) {
+                (void)hipStreamSynchronize(m->stream);
+                free_draft_fp8(m);
+                return st;
+            }
+            m->has_fp8 = true;
+        }
+    }
+    const hipError_t e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) {
+        free_draft_fp8(m);
+        return fail(SD_ERR_DEVICE, std::string("FP8 quantization: ") + hipGetErrorString(e));
+    }
+    return SD_OK;
+}
+
 void destroy_model(sd_model *m) {
     if (!m)
         return;
@@ -1259,6 +1342,7 @@ void destroy_model(sd_model *m) {
         (void)hipStreamSynchronize(m->stream);
     for (sd_kv_cache *c : m->caches)
         c->model = nullptr;
+    free_draft_fp8(m);
     destroy_cache(m->gen_cache);
     dev_free(m->ws.h);
     dev_free(m->ws.q);
@@ -1329,6 +1413,8 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
     m->mlp_norm.assign(w->mlp_norm, w->mlp_norm + L);
     m->w_gate_up.assign(w->w_gate_up, w->w_gate_up + L);
     m->w_down.assign(w->w_down, w->w_down + L);
+    m->fp8_q.assign(L, {nullptr, nullptr, nullptr, nullptr});
+    m->fp8_e.assign(L, {nullptr, nullptr, nullptr, nullptr});
     m->stream = reinterpret_cast<hipStream_t>(stream);
 
     int max_head_tiles = 1;
@@ -1516,6 +1602,18 @@ sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const ui
 sd_status sd_forward_static(sd_model *model, const int32_t *tokens, int32_t n, const uint8_t *skip_mask,
                             sd_kv_cache *cache, float *logits) {
     SD_GUARD(return forward_static(model, tokens, n, skip_mask, cache, logits);)
+}
+
+sd_status sd_model_quantize_draft(sd_model *model, const uint8_t *skip_mask) {
+    SD_GUARD(return quantize_draft(model, skip_mask);)
+}
+
+sd_status sd_model_draft_fp8(const sd_model *model, int32_t layer, int32_t kind, const void **q,
+                             const int32_t **exps) {
+    SD_GUARD(if (!model || !q || !exps) return fail(SD_ERR_INVALID_ARG, "model, q or exps is null");
+             if (layer < 0 || layer >= model->cfg.n_layers || kind < 0 || kind > 3)
+                 return fail(SD_ERR_INVALID_ARG, "layer or kind out of range");
+             *q = model->fp8_q[layer][kind]; *exps = model->fp8_e[layer][kind]; return SD_OK;)
 }
 
 sd_status sd_self_spec_generate(sd_model *model, const int32_t *prompt, int32_t prompt_len, int32_t max_new,

@@ -220,6 +220,7 @@ struct LinearArgs {
     int32_t splits;        // EPI_PARTIAL: work-groups splitting the reduction per tile group
     float *part;           // EPI_PARTIAL: [splits][MAX_ROWS][N]
     int32_t n_tiles;       // tiles in the layer (set by launch_linear)
+    const int32_t *wexp;   // PATH_GEMV_FP8: per weight row, the exponent e of its 2^e scale
     int32_t guarded;       // part of a step enqueued ahead, which the step guard may cancel (ctl->m = 0):
                            // the one-row path then takes its row count from ctl->m too
 };
@@ -286,7 +287,9 @@ hipError_t launch_pf_swiglu_split(const float *gu, int F, int M, uint16_t *out, 
 
 // Kernel paths of the linear layers.
 // PATH_WAVE2: up to two rows on one-wave tiles (bf16 weights).
-enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU2 = 3, PATH_WAVE2 = 4 };
+// PATH_GEMV_FP8: one row over the draft's FP8 weights (LinearArgs::wexp).
+enum LinearPath : int { PATH_GEMV = 0, PATH_VALU16 = 1, PATH_MFMA = 2, PATH_VALU2 = 3, PATH_WAVE2 = 4,
+                        PATH_GEMV_FP8 = 5 };
 
 // Optional events the runtime records at a launch's own start and end.
 struct LaunchTiming {
@@ -296,6 +299,9 @@ struct LaunchTiming {
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
                          hipStream_t s, const LaunchTiming &t = LaunchTiming{});
+// FP8 E4M3 copy of a bf16 matrix [N][K]: bytes Q [N][K] and the exponent of
+// each row's power-of-two scale E [N] (see k_quantize_fp8).
+hipError_t launch_quantize_fp8(const uint16_t *W, int32_t N, int32_t K, uint8_t *Q, int32_t *E, hipStream_t s);
 // Elements per work-group of the MFMA-path input preparation.
 constexpr int PREP_SLICE = 512;
 __host__ __device__ constexpr int prep_slices(int K) { return (K + PREP_SLICE - 1) / PREP_SLICE; }
