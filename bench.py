@@ -20,7 +20,8 @@ Other modes:
                         output projections scaled down, lm-head scaled up),
                         static and adaptive draft exit; --supp-mask picks
                         another skip set (e.g. random36, the paper's 13B
-                        skip count)
+                        skip count); --fp8-draft adds runs whose draft reads
+                        FP8 copies of its weights
   --sampling            labelled runs of the sampling variant (temperature and
                         top-p as in the paper's appendix) against autoregressive
                         sampling, static and adaptive exit, random and planted
@@ -58,14 +59,20 @@ def log(msg: str):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def step_bytes(cfg, skip, ctx: float, rows: float = 1):
+def step_bytes(cfg, skip, ctx: float, rows: float = 1, fp8: bool = False):
     """Algorithmic HBM bytes of one forward: weights of the sublayers run,
     read once whatever the row count, plus the KV read at ctx positions and
-    written for `rows` new positions in the attention sublayers run."""
+    written for `rows` new positions in the attention sublayers run.  fp8:
+    the sublayers' four weight matrices are FP8 copies (one byte per weight
+    and a 4-byte exponent per output row); norms and the lm-head stay bf16."""
     es = 2 if cfg.dtype == "bf16" else 4
     d, dh, H, KVH, F = cfg.d_model, cfg.head_dim, cfg.n_heads, cfg.n_kv_heads, cfg.ffn_dim
-    attn_w = (cfg.qkv_rows * d + d * H * dh + d) * es
-    mlp_w = (3 * d * F + d) * es
+    if fp8:
+        attn_w = cfg.qkv_rows * d + d * H * dh + 4 * (cfg.qkv_rows + d) + d * es
+        mlp_w = 3 * d * F + 4 * (2 * F + d) + d * es
+    else:
+        attn_w = (cfg.qkv_rows * d + d * H * dh + d) * es
+        mlp_w = (3 * d * F + d) * es
     kv_read = 2 * ctx * KVH * dh * es
     kv_write = 2 * rows * KVH * dh * es
     total = (cfg.vocab * d + d) * es + d * es  # lm head, final norm, one embedding row
@@ -497,12 +504,46 @@ def run_supplementary(args):
             c.close()
             r.update({"first_divergence": d, "gpu_top2_margin": round(float(top2[1] - top2[0]), 5),
                       "near_tie_tau": round(float(2 * 3e-2 * lg.std()), 5)})
+        if args.fp8_draft:
+            r.update(fp8_draft_runs(model, cfg, prompt, max_new, skip, wl, gamma, ar, ar_tok))
         out.append(r)
         log(json.dumps(r))
         model.close()
         del w
     print(json.dumps({"mode": "supplementary (planted redundancy)", "workload": wl.name, "mask": mask,
                       "skipped_sublayers": int(np.sum(skip)), "adaptive": binding.PAPER_ADAPTIVE, "results": out}))
+
+
+def fp8_draft_runs(model, cfg, prompt, max_new, skip, wl, gamma, ar, ar_tok) -> dict:
+    """The same model with FP8 copies of the draft's weights (verification
+    keeps bf16): static and adaptive exit, against the bf16 autoregressive
+    run `ar`.  The quantization time is wall time of the synchronous call,
+    allocation of the copies included."""
+    t0 = time.perf_counter()
+    model.quantize_draft(skip)
+    q_ms = (time.perf_counter() - t0) * 1e3
+    model.generate_sd(prompt, max_new, skip, wl.k_max, gamma)
+    tok, sd = model.generate_sd(prompt, max_new, skip, wl.k_max, gamma)
+    model.generate_sd_adaptive(prompt, max_new, skip, wl.k_max)
+    ad_tok, ad = model.generate_sd_adaptive(prompt, max_new, skip, wl.k_max)
+    model.quantize_draft(None)
+    n_st, n_dr = max(sd["n_stages"], 1), max(sd["n_draft_steps"], 1)
+    draft_ms = sd["draft_ms"] / n_dr
+    nbytes = step_bytes(cfg, skip, wl.prompt_len + max_new / 2, 1, fp8=True)
+    return {"fp8_quantize_ms": round(q_ms, 2),
+            "fp8_sd_tokens_per_s": round(max_new / (sd["decode_ms"] / 1e3), 2),
+            "fp8_speedup": round(ar["decode_ms"] / sd["decode_ms"], 4),
+            "fp8_acceptance": round(sd["n_accepted"] / max(sd["n_drafted"], 1), 4),
+            "fp8_tokens_per_stage": round(max_new / n_st, 3),
+            "fp8_draft_step_ms": round(draft_ms, 4),
+            "fp8_draft_step_GBps": round(nbytes / (draft_ms / 1e3) / 1e9, 1),
+            "fp8_draft_step_frac_hbm": round(nbytes / (draft_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "fp8_verify_step_ms": round(sd["verify_ms"] / n_st, 4),
+            "fp8_tokens_equal": int(np.sum(tok == ar_tok)),
+            "fp8_adaptive_sd_tokens_per_s": round(max_new / (ad["decode_ms"] / 1e3), 2),
+            "fp8_adaptive_speedup": round(ar["decode_ms"] / ad["decode_ms"], 4),
+            "fp8_adaptive_acceptance": round(ad["n_accepted"] / max(ad["n_drafted"], 1), 4),
+            "fp8_adaptive_tokens_equal": int(np.sum(ad_tok == ar_tok))}
 
 
 # ---------------------------------------------------------------------------
@@ -895,6 +936,8 @@ def main():
     ap.add_argument("--supplementary", action="store_true")
     ap.add_argument("--supp-mask", default=None,
                     help="skip mask for --supplementary (default: the workload's; e.g. random36)")
+    ap.add_argument("--fp8-draft", action="store_true",
+                    help="with --supplementary: also decode with FP8 copies of the draft's weights")
     ap.add_argument("--planted", default="0.05:8:0.6,0.05:8:0.0,0.02:16:0.6",
                     help="rho:head_gain:gamma triples for --supplementary")
     ap.add_argument("--sampling", action="store_true",

@@ -626,16 +626,28 @@ hipError_t launch_quantize_fp8(const uint16_t *W, int32_t N, int32_t K, uint8_t 
 }
 
 // One-row GEMV over FP8 weights (draft steps): a tile of R weight rows per
-// work-group of four waves; each thread takes 16 consecutive elements of the
-// reduction per step, one 16-byte load per weight row, converted to float32
-// exactly by the hardware.  RMSNorm is folded in as in k_linear_valu; the
-// row's 2^e scales its dot product before the shared epilogues.
+// work-group of FP8_WAVES waves; each thread takes 16 consecutive elements
+// of the reduction per step, one 16-byte load per weight row, converted to
+// float32 exactly by the hardware.  RMSNorm is folded in as in
+// k_linear_valu; the row's 2^e scales its dot product before the shared
+// epilogues.
+// Measured at the 13B shapes (cold weights, kernel time): two waves per
+// tile against four, QKV 17.2 against 18.1 us, O 7.3 against 7.9, gate/up
+// 26.8 against 26.6, down 14.6 against 15.5; one wave loses on the narrow
+// layers, 16-row tiles and a software-pipelined loop lose everywhere, and
+// a decode through fp16 bits is slower than the conversion instruction.
+// Against a plain read of the same bytes (gate/up 21.1 us), the activation
+// and gain loads cost about 2 us and the arithmetic that does not overlap
+// the loads about 2 us more.
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
+constexpr int FP8_WAVES = 2;
+
 template <int R, int EPI, bool NORM>
-__global__ __launch_bounds__(256) void k_linear_fp8(LinearArgs a) {
+__global__ __launch_bounds__(FP8_WAVES * 64) void k_linear_fp8(LinearArgs a) {
+    constexpr int NT = FP8_WAVES * 64;
     constexpr int NV = R + (NORM ? 1 : 0);
-    __shared__ float red[4][NV];
+    __shared__ float red[FP8_WAVES][NV];
     __shared__ float fin[R];
     __shared__ float inv_s[1];
     const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -653,7 +665,7 @@ __global__ __launch_bounds__(256) void k_linear_fp8(LinearArgs a) {
 #pragma unroll
     for (int i = 0; i < R; ++i)
         acc[i] = 0.0f;
-    for (int c = tid; c < nch; c += 256) {
+    for (int c = tid; c < nch; c += NT) {
         u32x4_t wr[R], gr[2];
         f32x4_t xr[4];
 #pragma unroll
@@ -707,7 +719,13 @@ __global__ __launch_bounds__(256) void k_linear_fp8(LinearArgs a) {
             red[wave][R] = v;
     }
     __syncthreads();
-    auto waves_sum = [&](int j) { return (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]); };
+    auto waves_sum = [&](int j) {
+        float v = red[0][j];
+#pragma unroll
+        for (int w = 1; w < FP8_WAVES; ++w)
+            v += red[w][j];
+        return v;
+    };
     if (tid < R)
         fin[tid] = ldexpf(waves_sum(tid), a.wexp[rows[tid]]);
     if (tid == 0)
@@ -719,7 +737,7 @@ __global__ __launch_bounds__(256) void k_linear_fp8(LinearArgs a) {
 
 template <int R>
 static hipError_t launch_fp8_r(const LinearArgs &a, int epi, int n_tiles, hipStream_t s, const LaunchTiming &t) {
-    dim3 grid(n_tiles), block(256);
+    dim3 grid(n_tiles), block(FP8_WAVES * 64);
     switch (epi) {
     case EPI_RESID:
         launch_k(k_linear_fp8<R, EPI_RESID, false>, grid, block, s, t, a);

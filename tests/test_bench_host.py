@@ -51,6 +51,26 @@ def test_step_bytes_kv_and_skips():
     assert drop == (3 * cfg.d_model * cfg.ffn_dim + cfg.d_model) * 2
 
 
+@pytest.mark.parametrize("name", ["7b", "13b", "70b"])
+def test_fp8_draft_step_bytes(name):
+    """With FP8 draft copies a full-model weight set costs one byte per
+    weight of the four sublayer matrices plus a 4-byte exponent per output
+    row; the lm-head, the norms, the embedding row and the KV stay as they
+    were."""
+    cfg = S.MODELS[name]
+    d, F, L = cfg.d_model, cfg.ffn_dim, cfg.n_layers
+    qkv = (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim
+    matrices = qkv * d + d * cfg.n_heads * cfg.head_dim + 3 * d * F
+    exponent_rows = qkv + d + 2 * F + d
+    for ctx, rows in ((0, 0), (1000, 1)):
+        bf16 = bench.step_bytes(cfg, None, ctx, rows)
+        fp8 = bench.step_bytes(cfg, None, ctx, rows, fp8=True)
+        assert bf16 - fp8 == L * (matrices * 2 - matrices - 4 * exponent_rows)
+    # a skipped sublayer costs nothing either way
+    skip = [1] * cfg.n_sublayers
+    assert bench.step_bytes(cfg, skip, 64, 1, fp8=True) == bench.step_bytes(cfg, skip, 64, 1)
+
+
 def test_gate_up_bytes():
     # 13B, two rows: weights 27648 x 5120, gain 5120, two input rows of 5120
     # and two SwiGLU output rows of 13824

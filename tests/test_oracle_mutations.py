@@ -24,8 +24,8 @@ MUTATIONS = {
     "score_scale": ("double scale = 1.0 / sqrt((double)dh);", "double scale = 1.0 / (double)dh;"),
     "block_not_causal": ("attend(c, l, qkv + (int64_t)r * nqkv, start + r,",
                          "attend(c, l, qkv + (int64_t)r * nqkv, start + n - 1,"),
-    "attn_residual": ("linear(m, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] += t[i];",
-                      "linear(m, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] = t[i];"),
+    "attn_residual": ("linear_layer(m, FP8_O, l, skip, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] += t[i];",
+                      "linear_layer(m, FP8_O, l, skip, m->w_o[l], d, (int64_t)H * dh, o, n, t);\n            for (int64_t i = 0; i < (int64_t)n * d; ++i)\n                h[i] = t[i];"),
     "gate_up_swap": ("mm[(int64_t)r * F + f] = silu(gr[f]) * gr[F + f];", "mm[(int64_t)r * F + f] = silu(gr[F + f]) * gr[f];"),
     "silu_sign": ("return a / (1.0 + exp(-a));", "return a / (1.0 + exp(a));"),
     "norm_mean": ("double inv = 1.0 / sqrt(ss / (double)d + m->c.rms_eps);", "double inv = 1.0 / sqrt(ss + m->c.rms_eps);"),
