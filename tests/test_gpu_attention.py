@@ -3,7 +3,8 @@
 One-layer bf16 models whose residual stream the attention output dominates
 (H * head_dim = 2048 or 512 against d_model = 256), so the logits follow the
 attention closely.  Contexts span several 128-key chunks with a ragged last
-chunk; a forward of 1..16 rows gives up to 8 * 16 = 128 query vectors per kv
+chunk, up to 33 chunks (more than the 16 partials the combine takes in one
+group); a forward of 1..16 rows gives up to 8 * 16 = 128 query vectors per kv
 head (8 tiles of 16 on the matrix-core path); head dims 128, 64 and 32.
 
 Tolerance: TIGHT_REL * std(oracle logits of the row), 30x tighter than the
@@ -29,6 +30,8 @@ CONFIGS = {
     "mha_dh32": S.ModelConfig("mha_dh32", 1, 256, 16, 16, 32, 256, 512, "bf16"),
 }
 CASES = [(name, pre, rows) for name in CONFIGS for pre, rows in [(300, 1), (300, 3), (300, 16), (700, 9)]]
+# past 16 chunks of 128 keys the combine loops over its partials in groups
+CASES += [("gqa8_dh128", 2100, 1), ("gqa4_dh64", 2100, 13), ("mha_dh32", 4100, 16)]
 _models = {}
 
 
