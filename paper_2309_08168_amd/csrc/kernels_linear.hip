@@ -85,6 +85,84 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------------------
+// Wave sums of several values at once, on the VALU.  A butterfly over the
+// lane bits 5, 4, 3, 2 halves the number of values at each level: a lane
+// keeps the half of its values that the lane bit selects and adds its
+// partner's copy of the same half (the pair of lanes 32 and 16 apart swaps
+// halves with one v_permlane32_swap / v_permlane16_swap, the pair 8 apart
+// exchanges through a row rotation, the pair 4 apart through a half-row
+// mirror), then the four lanes of a quad add up by two quad permutations.
+// After that, value j's total is in the lanes whose bits 5, 4, 3, 2 spell
+// j's bits 0, 1, 2, 3 (all four lanes of the quad): 15 swaps or moves and
+// 15 adds for 16 values, against 96 shuffles through LDS (ds_bpermute) one
+// at a time.  A level with a single value left adds the partner's copy.
+// The order of the additions is fixed, so sums are deterministic.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int DPP_ROW_ROR8 = 0x128;
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
+constexpr int DPP_QUAD_XOR2 = 0x4e;  // quad_perm [2, 3, 0, 1]
+constexpr int DPP_QUAD_XOR1 = 0xb1;  // quad_perm [1, 0, 3, 2]
+
+// lanes 0-31 get a's sum over lanes l and l + 32, lanes 32-63 b's
+__device__ __forceinline__ float bfly32(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// rows 0 and 2 (lanes 0-15, 32-47) get a's sum over rows 2i, 2i + 1, rows 1 and 3 b's
+__device__ __forceinline__ float bfly16(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// lanes with bit 3 clear get a's sum over lanes l and l ^ 8, the others b's
+__device__ __forceinline__ float bfly8(float a, float b, int lane) {
+    const bool hi = lane & 8;
+    return (hi ? b : a) + dpp_mov<DPP_ROW_ROR8>(hi ? a : b);
+}
+// lanes with bit 2 clear get a's sum over lanes l and the mirror 7 - l of the half row, the others b's
+__device__ __forceinline__ float bfly4(float a, float b, int lane) {
+    const bool hi = lane & 4;
+    return (hi ? b : a) + dpp_mov<DPP_ROW_HALF_MIRROR>(hi ? a : b);
+}
+
+// Totals over the wave of v[0..N) (N a power of two, at most 16), returned
+// per lane as described above; wave_sums_lane(j) is the first lane holding j.
+template <int N>
+__device__ __forceinline__ float wave_sums(const float (&v)[N], int lane) {
+    static_assert(N >= 1 && N <= 16 && (N & (N - 1)) == 0, "1, 2, 4, 8 or 16 values");
+    float a[16];
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+        a[j] = v[j];
+    // value index bits, low first, follow lane bits 5, 4, 3, 2
+    constexpr int n1 = N >= 2 ? N / 2 : 1;
+#pragma unroll
+    for (int j = 0; j < n1; ++j)
+        a[j] = N >= 2 ? bfly32(a[2 * j], a[2 * j + 1]) : bfly32(a[0], a[0]);
+    constexpr int n2 = n1 >= 2 ? n1 / 2 : 1;
+#pragma unroll
+    for (int j = 0; j < n2; ++j)
+        a[j] = n1 >= 2 ? bfly16(a[2 * j], a[2 * j + 1]) : bfly16(a[0], a[0]);
+    constexpr int n3 = n2 >= 2 ? n2 / 2 : 1;
+#pragma unroll
+    for (int j = 0; j < n3; ++j)
+        a[j] = n2 >= 2 ? bfly8(a[2 * j], a[2 * j + 1], lane) : a[0] + dpp_mov<DPP_ROW_ROR8>(a[0]);
+    float t = n3 >= 2 ? bfly4(a[0], a[1], lane) : a[0] + dpp_mov<DPP_ROW_HALF_MIRROR>(a[0]);
+    t += dpp_mov<DPP_QUAD_XOR2>(t);
+    t += dpp_mov<DPP_QUAD_XOR1>(t);
+    return t;
+}
+__host__ __device__ constexpr int wave_sums_lane(int j) {
+    return 32 * (j & 1) + 16 * ((j >> 1) & 1) + 8 * ((j >> 2) & 1) + 4 * ((j >> 3) & 1);
+}
+// the value index a lane holds (for the lanes wave_sums_lane names)
+__device__ __forceinline__ int wave_sums_index(int lane) {
+    return ((lane >> 5) & 1) | (((lane >> 4) & 1) << 1) | (((lane >> 3) & 1) << 2) | (((lane >> 2) & 1) << 3);
+}
+
+// ---------------------------------------------------------------------------
 // Which weight rows a tile of R rows covers.
 //   QKV: R/2 rotary pairs (i, i + head_dim/2) of one head, so the epilogue
 //        can rotate q and k in place;
@@ -224,9 +302,36 @@ __device__ void head_finalize(const LinearArgs &a, int n_tiles, int M) {
 // Epilogues.  fin[i * MR + m] holds the raw dot product of tile row i and
 // input row m; inv[m] the RMSNorm scale of row m (1 without a norm).
 
+// The residual-stream value an output projection adds to does not depend
+// on the products: the VALU kernels load it before their main loop, so the
+// round trip overlaps the loop instead of ending the kernel.  Thread j loads
+// what epilogue element j needs (R * MR is at most the work-group size);
+// indexes are clamped, so rows past the forward's row count read valid
+// memory that is never used.  (Loading the QKV tile's rotary factors the same
+// way made the one-row layer slower: their address waits for the control
+// block's position before the first weight load.)
+struct EpiPre {
+    float res;
+    bool ok;
+};
+
+template <int EPI>
+__device__ __forceinline__ EpiPre epi_prefetch(const LinearArgs &a, int t, int R, int MR) {
+    EpiPre p{0.0f, false};
+    if constexpr (EPI == EPI_RESID) {
+        const EpiArgs &e = a.epi;
+        const int j = min((int)threadIdx.x, R * MR - 1);
+        const int i = j % R, m = j / R;
+        const int n = min(t * R + i, a.N - 1);
+        p.res = e.out[(int64_t)m * e.ld_out + n];
+        p.ok = true;
+    }
+    return p;
+}
+
 template <typename TK, int EPI>
 __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, int R, int MR, const float *inv, int t,
-                                             int M) {
+                                             int M, const EpiPre &pre = EpiPre{0.0f, false}) {
     const int tid = threadIdx.x;
     const EpiArgs &e = a.epi;
     if constexpr (EPI == EPI_PARTIAL) {
@@ -243,7 +348,7 @@ __device__ __forceinline__ void run_epilogue(const LinearArgs &a, float *fin, in
                 const float v = fin[i * MR + m] * inv[m];
                 float *o = e.out + (int64_t)m * e.ld_out + n;
                 if constexpr (EPI == EPI_RESID) {
-                    *o += v;
+                    *o = (pre.ok && j == tid ? pre.res : *o) + v;
                 } else {
                     *o = v;
                 }
@@ -362,6 +467,7 @@ __global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
     __shared__ float inv_s[MR];
     const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int M = MR == 1 ? 1 : a.ctl->m;
+    const EpiPre pre = epi_prefetch<EPI>(a, t, R, MR);
     const int K = a.K, nch = K >> 3;
     const TW *W = reinterpret_cast<const TW *>(a.W);
     const TW *G = reinterpret_cast<const TW *>(a.gain);
@@ -517,19 +623,35 @@ __global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
         }
     }
 
+    // wave sums of every row's products (rows past M too: their values are
+    // never used) and of the sums of squares, up to 16 at a time
+    {
+        constexpr int NA = MR * R, NC = NA < 16 ? NA : 16;
+        static_assert((NA & (NA - 1)) == 0, "a power of two of products per lane");
+        const int j = wave_sums_index(lane) & (NC - 1);
+        const bool owner = lane == wave_sums_lane(j);
 #pragma unroll
-    for (int r = 0; r < MR; ++r) {
-        if (r < M) {
+        for (int c0 = 0; c0 < NA; c0 += NC) {
+            float part[NC];
 #pragma unroll
-            for (int i = 0; i < R; ++i) {
-                const float v = wave_sum(acc[r][i]);
-                if (lane == 0)
-                    red[wave][r * R + i] = v;
-            }
-            if constexpr (NORM) {
-                const float v = wave_sum(ss[r]);
-                if (lane == 0)
-                    red[wave][MR * R + r] = v;
+            for (int u = 0; u < NC; ++u)
+                part[u] = acc[(c0 + u) / R][(c0 + u) % R];
+            const float v = wave_sums<NC>(part, lane);
+            if (owner)
+                red[wave][c0 + j] = v;
+        }
+        if constexpr (NORM) {
+            constexpr int NS = MR < 16 ? MR : 16;
+            const int js = wave_sums_index(lane) & (NS - 1);
+#pragma unroll
+            for (int c0 = 0; c0 < MR; c0 += NS) {
+                float part[NS];
+#pragma unroll
+                for (int u = 0; u < NS; ++u)
+                    part[u] = ss[c0 + u];
+                const float v = wave_sums<NS>(part, lane);
+                if (lane == wave_sums_lane(js))
+                    red[wave][MR * R + c0 + js] = v;
             }
         }
     }
@@ -558,7 +680,7 @@ __global__ __launch_bounds__(NT) void k_linear_valu(LinearArgs a) {
     // The one-row path reads ctl->m only here and only when the launch may
     // be cancelled: a branch on it before the first loads delays every
     // launch.
-    run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, (MR == 1 && a.guarded) ? a.ctl->m : M);
+    run_epilogue<TW, EPI>(a, fin, R, MR, inv_s, t, (MR == 1 && a.guarded) ? a.ctl->m : M, pre);
 }
 
 // ---------------------------------------------------------------------------
@@ -661,6 +783,9 @@ __global__ __launch_bounds__(FP8_WAVES * 64) void k_linear_fp8(LinearArgs a) {
         rows[i] = row_valid<EPI>(t, i, R, a.N, a.epi) ? tile_row<EPI>(t, i, R, a.epi) : 0;
         roff[i] = (int64_t)rows[i] * K;
     }
+    // the row exponent and the residual value the epilogue needs, in flight during the loop
+    const int wexp = a.wexp[rows[min(tid, R - 1)]];
+    const EpiPre pre = epi_prefetch<EPI>(a, t, R, 1);
     float acc[R], ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < R; ++i)
@@ -707,16 +832,16 @@ __global__ __launch_bounds__(FP8_WAVES * 64) void k_linear_fp8(LinearArgs a) {
                 acc[i] = fmaf(hi[1], x[4 * j + 3], acc[i]);
             }
     }
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-        const float v = wave_sum(acc[i]);
-        if (lane == 0)
-            red[wave][i] = v;
-    }
-    if constexpr (NORM) {
-        const float v = wave_sum(ss);
-        if (lane == 0)
-            red[wave][R] = v;
+    {
+        const int j = wave_sums_index(lane) & (R - 1);
+        const float v = wave_sums<R>(acc, lane);
+        if (lane == wave_sums_lane(j))
+            red[wave][j] = v;
+        if constexpr (NORM) {
+            const float s = wave_sums<1>({ss}, lane);
+            if (lane == 0)
+                red[wave][R] = s;
+        }
     }
     __syncthreads();
     auto waves_sum = [&](int j) {
@@ -727,12 +852,12 @@ __global__ __launch_bounds__(FP8_WAVES * 64) void k_linear_fp8(LinearArgs a) {
         return v;
     };
     if (tid < R)
-        fin[tid] = ldexpf(waves_sum(tid), a.wexp[rows[tid]]);
+        fin[tid] = ldexpf(waves_sum(tid), wexp);
     if (tid == 0)
         inv_s[0] = NORM ? 1.0f / sqrtf(waves_sum(R) / (float)K + a.eps) : 1.0f;
     __syncthreads();
     // a cancelled step (ctl->m = 0) writes nothing; see k_linear_valu
-    run_epilogue<uint16_t, EPI>(a, fin, R, 1, inv_s, t, a.guarded ? a.ctl->m : 1);
+    run_epilogue<uint16_t, EPI>(a, fin, R, 1, inv_s, t, a.guarded ? a.ctl->m : 1, pre);
 }
 
 template <int R>
