@@ -31,6 +31,14 @@ __device__ __forceinline__ void load8_kv(const float *p, float *dst) {
     }
 }
 
+__device__ __forceinline__ void unpack8_bf16(u32x4_t v, float (&w)[8]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        w[2 * j] = __uint_as_float(v[j] << 16);
+        w[2 * j + 1] = __uint_as_float(v[j] & 0xffff0000u);
+    }
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1)
@@ -498,6 +506,173 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
     }
 }
 
+// Decode attention of one or two query vectors per kv head (the draft,
+// autoregressive and one-draft verification steps of multi-head attention)
+// over a bfloat16 cache with head_dim 128, on the VALU: one work-group of
+// four waves per (128-key chunk, kv head), 32 keys per wave.
+//
+// Lane group j4 (lanes 16 j4 .. 16 j4 + 15) holds the key rows
+// cw + 4 i + j4 (i = 0..7) of its wave and lane e16 of the group the
+// elements 8 e16 .. 8 e16 + 7 of each row, so every K and V load
+// instruction reads four whole rows (1 KB, coalesced).  A lane's partial
+// dot products of its 8 rows are summed over the 16 lanes of the group by a
+// butterfly over lane bits 3, 2, 1 that leaves row 4 b1 + 2 b2 + b3 in each
+// lane (b = the lane's bits), then a quad exchange over bit 0: one score
+// per lane, each key in two lanes.  The softmax of the wave's 32 keys is a
+// whole-wave max and sum; the weights go through LDS to the lanes that hold
+// the V rows, whose products are summed over the four groups by a butterfly
+// over lane bits 5, 4 (two output elements per lane).  The four waves merge
+// in LDS in wave order and the chunk leaves one partial state per (query,
+// split) for the ordered combine.  Keys past the context read the last row
+// inside it and are masked.
+constexpr int VW = 4;
+static_assert(ATTN_CHUNK == VW * 32, "32 keys per wave");
+
+template <int QV>
+__global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
+    constexpr int DH = 128;
+    __shared__ float sp[VW][QV][32];
+    __shared__ float so[VW][QV][DH];
+    __shared__ float2 sml[VW][QV];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int j4 = lane >> 4, e16 = lane & 15;
+    const int split = blockIdx.x, g = blockIdx.y;
+    const int pos = a.ctl->pos, M = a.ctl->m;
+    const int ctx = pos + M;
+    const int H = a.n_heads, G = H / a.n_kv_heads, Q = G * M;
+    const int c0 = split * ATTN_CHUNK;
+    if (M == 0 || c0 >= ctx)
+        return;  // uniform over the work-group (M = 0: a cancelled step)
+    const int cw = c0 + wave * 32;
+    const uint16_t *Kg = reinterpret_cast<const uint16_t *>(a.kcache) + (int64_t)g * a.kv_head_stride + 8 * e16;
+    const uint16_t *Vg = reinterpret_cast<const uint16_t *>(a.vcache) + (int64_t)g * a.kv_head_stride + 8 * e16;
+
+    // query vector qi: row qi / G, head g G + qi % G; a vector past Q reads
+    // the first one and is masked
+    f32x4_t qraw[QV][2];
+#pragma unroll
+    for (int qi = 0; qi < QV; ++qi) {
+        const int qidx = qi < Q ? qi : 0, r = qidx / G;
+        const float *qs = a.q + (int64_t)r * a.ld_q + (int64_t)(g * G + qidx - r * G) * DH + 8 * e16;
+        qraw[qi][0] = reinterpret_cast<const f32x4_t *>(qs)[0];
+        qraw[qi][1] = reinterpret_cast<const f32x4_t *>(qs)[1];
+    }
+    u32x4_t kr[8], vr[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int key = min(cw + 4 * i + j4, ctx - 1);
+        kr[i] = *reinterpret_cast<const u32x4_t *>(Kg + (int64_t)key * DH);
+        vr[i] = *reinterpret_cast<const u32x4_t *>(Vg + (int64_t)key * DH);
+    }
+    // every load above is issued before the first result is waited for
+    __builtin_amdgcn_sched_barrier(0);
+
+    const float scale = 1.0f / sqrtf((float)DH);
+    float s[QV][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float kx[8];
+        unpack8_bf16(kr[i], kx);
+#pragma unroll
+        for (int qi = 0; qi < QV; ++qi) {
+            float t = 0.0f;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                t = fmaf(qraw[qi][0][u] * scale, kx[u], t);
+                t = fmaf(qraw[qi][1][u] * scale, kx[4 + u], t);
+            }
+            s[qi][i] = t;
+        }
+    }
+    const int b0 = lane & 1, b1 = (lane >> 1) & 1, b2 = (lane >> 2) & 1, b3 = (lane >> 3) & 1;
+    const int row = 4 * b1 + 2 * b2 + b3;  // the row whose score this lane ends with
+    const int key = cw + 4 * row + j4;
+    float p[QV], mx[QV], ls[QV];
+#pragma unroll
+    for (int qi = 0; qi < QV; ++qi) {
+        float x4[4], x2[2];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            x4[u] = bfly8(s[qi][2 * u], s[qi][2 * u + 1], lane);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            x2[u] = bfly4(x4[2 * u], x4[2 * u + 1], lane);
+        float t = bfly2(x2[0], x2[1], lane);
+        t += dpp_mov<DPP_QUAD_XOR1>(t);
+        const int r = qi < Q ? qi / G : 0;
+        const bool ok = qi < Q && key < ctx && key <= pos + r;
+        const float sv = ok ? t : -INFINITY;
+        mx[qi] = wave_max_all(sv);
+        p[qi] = mx[qi] == -INFINITY ? 0.0f : expf(sv - mx[qi]);
+        ls[qi] = wave_sum_all(b0 ? 0.0f : p[qi]);
+        if (!b0)
+            sp[wave][qi][8 * j4 + row] = p[qi];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    // O = sum over the rows of p V, for the lane's 8 elements
+    float o[QV][8];
+#pragma unroll
+    for (int qi = 0; qi < QV; ++qi)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            o[qi][u] = 0.0f;
+#pragma unroll
+    for (int qi = 0; qi < QV; ++qi) {
+        const f32x4_t pa = *reinterpret_cast<const f32x4_t *>(&sp[wave][qi][8 * j4]);
+        const f32x4_t pb = *reinterpret_cast<const f32x4_t *>(&sp[wave][qi][8 * j4 + 4]);
+        const float pw[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float vx[8];
+            unpack8_bf16(vr[i], vx);
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                o[qi][u] = fmaf(pw[i], vx[u], o[qi][u]);
+        }
+    }
+#pragma unroll
+    for (int qi = 0; qi < QV; ++qi) {
+        float y4[4], y2[2];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            y4[u] = bfly32(o[qi][2 * u], o[qi][2 * u + 1]);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            y2[u] = bfly16(y4[2 * u], y4[2 * u + 1]);
+        // element 8 e16 + 4 u + 2 b4 + b5 of the wave's output
+        const int e0 = 8 * e16 + 2 * ((lane >> 4) & 1) + ((lane >> 5) & 1);
+        so[wave][qi][e0] = y2[0];
+        so[wave][qi][e0 + 4] = y2[1];
+        if (lane == 0)
+            sml[wave][qi] = make_float2(mx[qi], ls[qi]);
+    }
+    __syncthreads();
+    // merge the waves in wave order; one (query, element) per thread
+    const int t = threadIdx.x;
+    if (t < QV * DH) {
+        const int qi = t / DH, e = t - qi * DH;
+        if (qi < Q) {
+            float m = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < VW; ++w)
+                m = fmaxf(m, sml[w][qi].x);
+            float L = 0.0f, O = 0.0f;
+#pragma unroll
+            for (int w = 0; w < VW; ++w) {
+                const float2 ml = sml[w][qi];
+                const float wt = (m == -INFINITY || ml.x == -INFINITY) ? 0.0f : expf(ml.x - m);
+                L = fmaf(wt, ml.y, L);
+                O = fmaf(wt, so[w][qi][e], O);
+            }
+            const int r = qi / G, head = g * G + (qi - r * G);
+            const int64_t slot = ((int64_t)split * H + head) * MAX_ROWS + r;
+            a.part_o[slot * DH + e] = O;
+            if (e == 0)
+                a.part_ml[slot] = make_float2(m, L);
+        }
+    }
+}
+
 // Decode attention without a combine pass: one work-group of HW waves per
 // kv head, for up to QH query vectors (the draft, autoregressive and short
 // verification steps of multi-head attention).  Wave w takes the 16-key
@@ -830,8 +1005,14 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
     if (G * max_rows <= QH && a.splits * ATTN_CHUNK <= 256)
         return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
     const int max_q = G * max_rows;
-    hipError_t e;
-    if (bf16 && a.head_dim >= 32 && max_q >= ATTN_MFMA_MIN_Q)
+    hipError_t e = hipSuccess;
+    if (bf16 && a.head_dim == 128 && max_q <= 2) {
+        // one or two query vectors per kv head: VALU tiles
+        if (max_q <= 1)
+            hipLaunchKernelGGL(k_attn_valu<1>, dim3(a.splits, a.n_kv_heads), dim3(VW * 64), 0, s, a);
+        else
+            hipLaunchKernelGGL(k_attn_valu<2>, dim3(a.splits, a.n_kv_heads), dim3(VW * 64), 0, s, a);
+    } else if (bf16 && a.head_dim >= 32 && max_q >= ATTN_MFMA_MIN_Q)
         e = launch_attn_mfma(a, max_q, s);
     else
         e = bf16 ? launch_attn_split<uint16_t>(a, max_q, s) : launch_attn_split<float>(a, max_q, s);

@@ -85,84 +85,6 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// Wave sums of several values at once, on the VALU.  A butterfly over the
-// lane bits 5, 4, 3, 2 halves the number of values at each level: a lane
-// keeps the half of its values that the lane bit selects and adds its
-// partner's copy of the same half (the pair of lanes 32 and 16 apart swaps
-// halves with one v_permlane32_swap / v_permlane16_swap, the pair 8 apart
-// exchanges through a row rotation, the pair 4 apart through a half-row
-// mirror), then the four lanes of a quad add up by two quad permutations.
-// After that, value j's total is in the lanes whose bits 5, 4, 3, 2 spell
-// j's bits 0, 1, 2, 3 (all four lanes of the quad): 15 swaps or moves and
-// 15 adds for 16 values, against 96 shuffles through LDS (ds_bpermute) one
-// at a time.  A level with a single value left adds the partner's copy.
-// The order of the additions is fixed, so sums are deterministic.
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float v) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
-}
-constexpr int DPP_ROW_ROR8 = 0x128;
-constexpr int DPP_ROW_HALF_MIRROR = 0x141;
-constexpr int DPP_QUAD_XOR2 = 0x4e;  // quad_perm [2, 3, 0, 1]
-constexpr int DPP_QUAD_XOR1 = 0xb1;  // quad_perm [1, 0, 3, 2]
-
-// lanes 0-31 get a's sum over lanes l and l + 32, lanes 32-63 b's
-__device__ __forceinline__ float bfly32(float a, float b) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-// rows 0 and 2 (lanes 0-15, 32-47) get a's sum over rows 2i, 2i + 1, rows 1 and 3 b's
-__device__ __forceinline__ float bfly16(float a, float b) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-// lanes with bit 3 clear get a's sum over lanes l and l ^ 8, the others b's
-__device__ __forceinline__ float bfly8(float a, float b, int lane) {
-    const bool hi = lane & 8;
-    return (hi ? b : a) + dpp_mov<DPP_ROW_ROR8>(hi ? a : b);
-}
-// lanes with bit 2 clear get a's sum over lanes l and the mirror 7 - l of the half row, the others b's
-__device__ __forceinline__ float bfly4(float a, float b, int lane) {
-    const bool hi = lane & 4;
-    return (hi ? b : a) + dpp_mov<DPP_ROW_HALF_MIRROR>(hi ? a : b);
-}
-
-// Totals over the wave of v[0..N) (N a power of two, at most 16), returned
-// per lane as described above; wave_sums_lane(j) is the first lane holding j.
-template <int N>
-__device__ __forceinline__ float wave_sums(const float (&v)[N], int lane) {
-    static_assert(N >= 1 && N <= 16 && (N & (N - 1)) == 0, "1, 2, 4, 8 or 16 values");
-    float a[16];
-#pragma unroll
-    for (int j = 0; j < N; ++j)
-        a[j] = v[j];
-    // value index bits, low first, follow lane bits 5, 4, 3, 2
-    constexpr int n1 = N >= 2 ? N / 2 : 1;
-#pragma unroll
-    for (int j = 0; j < n1; ++j)
-        a[j] = N >= 2 ? bfly32(a[2 * j], a[2 * j + 1]) : bfly32(a[0], a[0]);
-    constexpr int n2 = n1 >= 2 ? n1 / 2 : 1;
-#pragma unroll
-    for (int j = 0; j < n2; ++j)
-        a[j] = n1 >= 2 ? bfly16(a[2 * j], a[2 * j + 1]) : bfly16(a[0], a[0]);
-    constexpr int n3 = n2 >= 2 ? n2 / 2 : 1;
-#pragma unroll
-    for (int j = 0; j < n3; ++j)
-        a[j] = n2 >= 2 ? bfly8(a[2 * j], a[2 * j + 1], lane) : a[0] + dpp_mov<DPP_ROW_ROR8>(a[0]);
-    float t = n3 >= 2 ? bfly4(a[0], a[1], lane) : a[0] + dpp_mov<DPP_ROW_HALF_MIRROR>(a[0]);
-    t += dpp_mov<DPP_QUAD_XOR2>(t);
-    t += dpp_mov<DPP_QUAD_XOR1>(t);
-    return t;
-}
-__host__ __device__ constexpr int wave_sums_lane(int j) {
-    return 32 * (j & 1) + 16 * ((j >> 1) & 1) + 8 * ((j >> 2) & 1) + 4 * ((j >> 3) & 1);
-}
-// the value index a lane holds (for the lanes wave_sums_lane names)
-__device__ __forceinline__ int wave_sums_index(int lane) {
-    return ((lane >> 5) & 1) | (((lane >> 4) & 1) << 1) | (((lane >> 3) & 1) << 2) | (((lane >> 2) & 1) << 3);
-}
-
-// ---------------------------------------------------------------------------
 // Which weight rows a tile of R rows covers.
 //   QKV: R/2 rotary pairs (i, i + head_dim/2) of one head, so the epilogue
 //        can rotate q and k in place;

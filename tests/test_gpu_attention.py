@@ -5,7 +5,8 @@ One-layer bf16 models whose residual stream the attention output dominates
 attention closely.  Contexts span several 128-key chunks with a ragged last
 chunk, up to 33 chunks (more than the 16 partials the combine takes in one
 group); a forward of 1..16 rows gives up to 8 * 16 = 128 query vectors per kv
-head (8 tiles of 16 on the matrix-core path); head dims 128, 64 and 32.
+head (8 tiles of 16 on the matrix-core path); head dims 128, 64 and 32; one
+or two query vectors per kv head at head dim 128 (the VALU split kernel).
 
 Tolerance: TIGHT_REL * std(oracle logits of the row), 30x tighter than the
 bf16 model tolerance.  With one layer the GPU differs from the oracle only by
@@ -28,10 +29,20 @@ CONFIGS = {
     "gqa8_dh128": S.ModelConfig("gqa8_dh128", 1, 256, 16, 2, 128, 256, 512, "bf16"),
     "gqa4_dh64": S.ModelConfig("gqa4_dh64", 1, 256, 8, 2, 64, 256, 512, "bf16"),
     "mha_dh32": S.ModelConfig("mha_dh32", 1, 256, 16, 16, 32, 256, 512, "bf16"),
+    # one or two query vectors per kv head at head_dim 128 (the draft,
+    # autoregressive and one-draft verification steps of the 7B/13B shapes)
+    # take the VALU split kernel
+    "mha_dh128": S.ModelConfig("mha_dh128", 1, 256, 16, 16, 128, 256, 512, "bf16"),
+    "gqa2_dh128": S.ModelConfig("gqa2_dh128", 1, 256, 16, 8, 128, 256, 512, "bf16"),
 }
 CASES = [(name, pre, rows) for name in CONFIGS for pre, rows in [(300, 1), (300, 3), (300, 16), (700, 9)]]
 # past 16 chunks of 128 keys the combine loops over its partials in groups
 CASES += [("gqa8_dh128", 2100, 1), ("gqa4_dh64", 2100, 13), ("mha_dh32", 4100, 16)]
+# the VALU kernel: one and two rows of multi-head attention, one row of
+# grouped heads with two query heads per kv head; ragged last chunks, and
+# more than 16 chunks
+CASES += [("mha_dh128", 300, 2), ("mha_dh128", 700, 2), ("mha_dh128", 1283, 1), ("mha_dh128", 2300, 2),
+          ("gqa2_dh128", 700, 1), ("gqa2_dh128", 2170, 1)]
 _models = {}
 
 
