@@ -509,7 +509,7 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
 // Decode attention of one or two query vectors per kv head (the draft,
 // autoregressive and one-draft verification steps of multi-head attention)
 // over a bfloat16 cache with head_dim 128, on the VALU: one work-group of
-// four waves per (128-key chunk, kv head), 32 keys per wave.
+// two waves per (64-key chunk, kv head), 32 keys per wave.
 //
 // Lane group j4 (lanes 16 j4 .. 16 j4 + 15) holds the key rows
 // cw + 4 i + j4 (i = 0..7) of its wave and lane e16 of the group the
@@ -521,12 +521,19 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
 // per lane, each key in two lanes.  The softmax of the wave's 32 keys is a
 // whole-wave max and sum; the weights go through LDS to the lanes that hold
 // the V rows, whose products are summed over the four groups by a butterfly
-// over lane bits 5, 4 (two output elements per lane).  The four waves merge
+// over lane bits 5, 4 (two output elements per lane).  The two waves merge
 // in LDS in wave order and the chunk leaves one partial state per (query,
 // split) for the ordered combine.  Keys past the context read the last row
 // inside it and are masked.
-constexpr int VW = 4;
-static_assert(ATTN_CHUNK == VW * 32, "32 keys per wave");
+//
+// The V rows are requested after the scores: with the K and V rows of a
+// wave (16 loads per lane) requested at once, the short burst of a decode
+// step streamed markedly slower (measured: a plain read of the same 26 MB
+// with 16 loads in flight per thread took 8.7 us against 5.8 us with 4), and
+// small work-groups spread it better (13B, 1280 keys, one row: 8.3 us with
+// four waves of 32 keys and every load at once, 7.0 us like this).
+constexpr int VW = 2;
+static_assert(ATTN_CHUNK_VALU == VW * 32, "32 keys per wave");
 
 template <int QV>
 __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
@@ -540,7 +547,7 @@ __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
     const int pos = a.ctl->pos, M = a.ctl->m;
     const int ctx = pos + M;
     const int H = a.n_heads, G = H / a.n_kv_heads, Q = G * M;
-    const int c0 = split * ATTN_CHUNK;
+    const int c0 = split * ATTN_CHUNK_VALU;
     if (M == 0 || c0 >= ctx)
         return;  // uniform over the work-group (M = 0: a cancelled step)
     const int cw = c0 + wave * 32;
@@ -557,14 +564,13 @@ __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
         qraw[qi][0] = reinterpret_cast<const f32x4_t *>(qs)[0];
         qraw[qi][1] = reinterpret_cast<const f32x4_t *>(qs)[1];
     }
+    int keyrow[8];
     u32x4_t kr[8], vr[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int key = min(cw + 4 * i + j4, ctx - 1);
-        kr[i] = *reinterpret_cast<const u32x4_t *>(Kg + (int64_t)key * DH);
-        vr[i] = *reinterpret_cast<const u32x4_t *>(Vg + (int64_t)key * DH);
+        keyrow[i] = min(cw + 4 * i + j4, ctx - 1);
+        kr[i] = *reinterpret_cast<const u32x4_t *>(Kg + (int64_t)keyrow[i] * DH);
     }
-    // every load above is issued before the first result is waited for
     __builtin_amdgcn_sched_barrier(0);
 
     const float scale = 1.0f / sqrtf((float)DH);
@@ -584,10 +590,13 @@ __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
             s[qi][i] = t;
         }
     }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        vr[i] = *reinterpret_cast<const u32x4_t *>(Vg + (int64_t)keyrow[i] * DH);
     const int b0 = lane & 1, b1 = (lane >> 1) & 1, b2 = (lane >> 2) & 1, b3 = (lane >> 3) & 1;
     const int row = 4 * b1 + 2 * b2 + b3;  // the row whose score this lane ends with
     const int key = cw + 4 * row + j4;
-    float p[QV], mx[QV], ls[QV];
+    float mx[QV], ls[QV];
 #pragma unroll
     for (int qi = 0; qi < QV; ++qi) {
         float x4[4], x2[2];
@@ -603,10 +612,10 @@ __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
         const bool ok = qi < Q && key < ctx && key <= pos + r;
         const float sv = ok ? t : -INFINITY;
         mx[qi] = wave_max_all(sv);
-        p[qi] = mx[qi] == -INFINITY ? 0.0f : expf(sv - mx[qi]);
-        ls[qi] = wave_sum_all(b0 ? 0.0f : p[qi]);
+        const float p = mx[qi] == -INFINITY ? 0.0f : expf(sv - mx[qi]);
+        ls[qi] = wave_sum_all(b0 ? 0.0f : p);
         if (!b0)
-            sp[wave][qi][8 * j4 + row] = p[qi];
+            sp[wave][qi][8 * j4 + row] = p;
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     // O = sum over the rows of p V, for the lane's 8 elements
@@ -647,9 +656,8 @@ __global__ __launch_bounds__(VW * 64) void k_attn_valu(AttnArgs a) {
             sml[wave][qi] = make_float2(mx[qi], ls[qi]);
     }
     __syncthreads();
-    // merge the waves in wave order; one (query, element) per thread
-    const int t = threadIdx.x;
-    if (t < QV * DH) {
+    // merge the waves in wave order; one (query, element) per thread and pass
+    for (int t = threadIdx.x; t < QV * DH; t += VW * 64) {
         const int qi = t / DH, e = t - qi * DH;
         if (qi < Q) {
             float m = -INFINITY;
@@ -844,10 +852,10 @@ __global__ __launch_bounds__(NWV * 64) void k_attn_head(AttnArgs a) {
 // Ordered combine of the split partials of one (head, row): deterministic.
 // Thread e owns output element e.  The running maxima and sums of the first
 // 128 splits and the partial outputs of the first CB splits are all loaded
-// before any of them is used, so a context of up to CB * ATTN_CHUNK keys
-// costs one round trip to memory.
+// before any of them is used, so a context of up to CB chunks costs one
+// round trip to memory (CB = 16 or 32, by the host's bound on the splits).
+template <int CB>
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
-    constexpr int CB = 16;
     __shared__ float w_s[MAX_SPLITS];
     __shared__ float2 ml_s[MAX_SPLITS];
     __shared__ float red[2];
@@ -855,7 +863,7 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
     const int pos = a.ctl->pos, M = a.ctl->m;
     if (r >= M)
         return;
-    const int ns = (pos + M + ATTN_CHUNK - 1) / ATTN_CHUNK;
+    const int ns = (pos + M + a.chunk - 1) / a.chunk;
     const int dh = a.head_dim, H = a.n_heads, tid = threadIdx.x;
     auto o_at = [&](int sp, int e) { return a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e]; };
     auto ml_at = [&](int sp) { return a.part_ml[((int64_t)sp * H + head) * MAX_ROWS + r]; };
@@ -996,17 +1004,21 @@ static hipError_t launch_attn_head(const AttnArgs &a, hipStream_t s) {
 // Query vectors per kv head from which bfloat16 caches take the MFMA kernel.
 constexpr int ATTN_MFMA_MIN_Q = 1;
 
-hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStream_t s) {
-    if (a.splits > MAX_SPLITS)
+hipError_t launch_attention(const AttnArgs &a0, bool bf16, int max_rows, hipStream_t s) {
+    if (a0.cap < 1 || a0.cap > MAX_CONTEXT)
         return hipErrorInvalidValue;
+    AttnArgs a = a0;
     const int G = a.n_heads / a.n_kv_heads;
+    const int max_q = G * max_rows;
     // one work-group per kv head while the context is short and the query
     // vectors per head fit; otherwise split the keys over work-groups
-    if (G * max_rows <= QH && a.splits * ATTN_CHUNK <= 256)
+    if (max_q <= QH && a.cap <= 256)
         return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
-    const int max_q = G * max_rows;
+    const bool valu = bf16 && a.head_dim == 128 && max_q <= 2;
+    a.chunk = valu ? ATTN_CHUNK_VALU : ATTN_CHUNK;
+    a.splits = (a.cap + a.chunk - 1) / a.chunk;
     hipError_t e = hipSuccess;
-    if (bf16 && a.head_dim == 128 && max_q <= 2) {
+    if (valu) {
         // one or two query vectors per kv head: VALU tiles
         if (max_q <= 1)
             hipLaunchKernelGGL(k_attn_valu<1>, dim3(a.splits, a.n_kv_heads), dim3(VW * 64), 0, s, a);
@@ -1019,7 +1031,10 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16, int max_rows, hipStrea
     if (e != hipSuccess)
         return e;
     // one work-group per (head, row) the forward can have
-    hipLaunchKernelGGL(k_attn_combine, dim3(a.n_heads, max_rows), dim3(128), 0, s, a);
+    if (a.splits <= 16)
+        hipLaunchKernelGGL(k_attn_combine<16>, dim3(a.n_heads, max_rows), dim3(128), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_attn_combine<32>, dim3(a.n_heads, max_rows), dim3(128), 0, s, a);
     return hipGetLastError();
 }
 

@@ -327,7 +327,7 @@ sd_status ensure_rope(sd_model *m, int cap) {
 }
 
 sd_status ensure_attn(sd_model *m, int cap) {
-    const int splits = cdiv(cap, ATTN_CHUNK);
+    const int splits = attn_split_slots(cap);
     if (splits <= m->attn_splits_cap)
         return SD_OK;
     SD_HIP(hipStreamSynchronize(m->stream));
@@ -538,7 +538,7 @@ sd_status forward_layers(sd_model *m, const Workspace &w, void *kv, int32_t cap,
             at.n_heads = c.n_heads;
             at.n_kv_heads = c.n_kv_heads;
             at.head_dim = c.head_dim;
-            at.splits = cdiv(cap, ATTN_CHUNK);
+            at.cap = cap;
             at.ctl = w.ctl;
             SD_TRY(launch(launch_attention(at, m->bf16, max_rows, m->stream), "attention"));
             EpiArgs eo{};
@@ -647,8 +647,8 @@ sd_status check_mask(const sd_model *m, const uint8_t *skip) {
 sd_status create_cache(sd_model *m, int32_t cap, void *buf, sd_kv_cache **out) {
     if (cap < 1)
         return fail(SD_ERR_INVALID_ARG, "capacity must be >= 1");
-    if (cap > MAX_SPLITS * ATTN_CHUNK)
-        return fail(SD_ERR_CAPACITY, "capacity above " + std::to_string(MAX_SPLITS * ATTN_CHUNK) + " positions");
+    if (cap > MAX_CONTEXT)
+        return fail(SD_ERR_CAPACITY, "capacity above " + std::to_string(MAX_CONTEXT) + " positions");
     if (buf && !aligned16(buf))
         return fail(SD_ERR_INVALID_ARG, "cache buffer must be 16-byte aligned");
     SD_TRY(ensure_rope(m, cap));
@@ -1212,7 +1212,7 @@ size_t carve_workspace(const sd_model *m, int32_t cap, char *base, Workspace *w)
         off += (bytes + 255) & ~(size_t)255;
         return p;
     };
-    const size_t hd = (size_t)c.n_heads * c.head_dim, splits = (size_t)cdiv(cap, ATTN_CHUNK);
+    const size_t hd = (size_t)c.n_heads * c.head_dim, splits = (size_t)attn_split_slots(cap);
     w->xld = xld_of(c);
     w->h = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * c.d_model));
     w->q = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * hd));

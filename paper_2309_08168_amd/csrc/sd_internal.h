@@ -10,12 +10,19 @@ namespace sdk {
 // Rows of one forward: the verification of K_max <= 15 drafts plus the last
 // committed token, one 16-row MFMA tile, and the prefill chunk size.
 constexpr int MAX_ROWS = 16;
-// Keys per attention work-group (split-KV chunk): 8 waves of 16 keys.
+// Keys per attention work-group (split-KV chunk): 128 for the matrix-core
+// and float32 kernels, 64 for the VALU kernel of one or two query vectors
+// per kv head (two waves of 32 keys).
 constexpr int ATTN_CHUNK = 128;
+constexpr int ATTN_CHUNK_VALU = 64;
 // Largest head_dim the attention kernel stages in LDS.
 constexpr int MAX_HEAD_DIM = 128;
-// Most key chunks one attention call combines: 65536 positions.
-constexpr int MAX_SPLITS = 512;
+// Longest context (cache capacity) and the most key chunks one attention
+// call combines: 65536 positions in 64-key chunks.
+constexpr int MAX_CONTEXT = 65536;
+constexpr int MAX_SPLITS = MAX_CONTEXT / ATTN_CHUNK_VALU;
+// Split partial slots a cache of capacity cap needs (the finest chunking).
+__host__ __device__ constexpr int attn_split_slots(int cap) { return (cap + ATTN_CHUNK_VALU - 1) / ATTN_CHUNK_VALU; }
 
 // Where and what the current forward computes.  Device resident: the
 // greedy head of one step writes the control block of the next step, so
@@ -235,7 +242,9 @@ struct AttnArgs {
     float *out;            // [m][n_heads * head_dim]
     uint16_t *out_x;       // when set, the output split into bf16 terms in fragment layout instead
     int64_t ld_out;
-    int32_t n_heads, n_kv_heads, head_dim, splits;
+    int32_t n_heads, n_kv_heads, head_dim;
+    int32_t cap;           // cache capacity: positions past it are never read
+    int32_t splits, chunk; // set by launch_attention: key chunks and keys per chunk
     const DevCtl *ctl;
 };
 
