@@ -850,56 +850,60 @@ __global__ __launch_bounds__(NWV * 64) void k_attn_head(AttnArgs a) {
 }
 
 // Ordered combine of the split partials of one (head, row): deterministic.
-// Thread e owns output element e.  The running maxima and sums of the first
-// 128 splits and the partial outputs of the first CB splits are all loaded
-// before any of them is used, so a context of up to CB chunks costs one
-// round trip to memory (CB = 16 or 32, by the host's bound on the splits).
+// Thread e owns output element e.  The partial outputs of the first CB
+// splits and the running maxima and sums of the first 128 are loaded before
+// the control block is known: indexes are clamped to the host's bound on
+// the splits, and the values of splits past the live context (stale, never
+// used) are masked once the context is known.  So a context of up to CB
+// chunks costs one round trip to memory (CB = 16 or 32, by the host's
+// bound).  The maximum is a whole-wave max per wave; the sum of the
+// rescaled split sums is a fixed tree (a wave butterfly per wave, then
+// wave 0 + wave 1), so the result is the same on every run.
 template <int CB>
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
     __shared__ float w_s[MAX_SPLITS];
-    __shared__ float2 ml_s[MAX_SPLITS];
-    __shared__ float red[2];
+    __shared__ float2 red[2];
     const int head = blockIdx.x, r = blockIdx.y;
-    const int pos = a.ctl->pos, M = a.ctl->m;
-    if (r >= M)
-        return;
-    const int ns = (pos + M + a.chunk - 1) / a.chunk;
-    const int dh = a.head_dim, H = a.n_heads, tid = threadIdx.x;
+    const int dh = a.head_dim, H = a.n_heads, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int S = a.splits;
     auto o_at = [&](int sp, int e) { return a.part_o[(((int64_t)sp * H + head) * MAX_ROWS + r) * dh + e]; };
     auto ml_at = [&](int sp) { return a.part_ml[((int64_t)sp * H + head) * MAX_ROWS + r]; };
-    // every load below reads a split inside [0, ns) and an element inside
-    // [0, dh); the values past ns or dh are discarded
+    // every load of a split inside [0, S) and an element inside [0, dh)
     const int e = tid < dh ? tid : 0;
     float ov[CB];
 #pragma unroll
     for (int u = 0; u < CB; ++u)
-        ov[u] = o_at(min(u, ns - 1), e);
-    const float2 ml0 = ml_at(min(tid, ns - 1));
-    float mx = -INFINITY;
-    if (tid < ns) {
-        ml_s[tid] = ml0;
-        mx = ml0.x;
-    }
-    for (int sp = tid + 128; sp < ns; sp += 128) {
-        const float2 v = ml_at(sp);
-        ml_s[sp] = v;
-        mx = fmaxf(mx, v.x);
-    }
-    mx = wave_max(mx);
-    if ((tid & 63) == 0)
-        red[tid >> 6] = mx;
+        ov[u] = o_at(min(u, S - 1), e);
+    float2 ml0 = ml_at(min(tid, S - 1));
+    const int pos = a.ctl->pos, M = a.ctl->m;
+    if (r >= M)
+        return;  // uniform over the work-group
+    const int ns = (pos + M + a.chunk - 1) / a.chunk;
+    if (tid >= ns)
+        ml0 = make_float2(-INFINITY, 0.0f);
+    float mx = ml0.x;
+    for (int sp = tid + 128; sp < ns; sp += 128)
+        mx = fmaxf(mx, ml_at(sp).x);
+    mx = wave_max_all(mx);
+    if (lane == 0)
+        red[wave].x = mx;
     __syncthreads();
-    mx = fmaxf(red[0], red[1]);
+    mx = fmaxf(red[0].x, red[1].x);
+    // split weights exp(m_s - max) and the rescaled sums, split sp by thread sp % 128
+    float ls = 0.0f;
     for (int sp = tid; sp < ns; sp += 128) {
-        const float2 v = ml_s[sp];
-        w_s[sp] = v.x == -INFINITY ? 0.0f : expf(v.x - mx);
+        const float2 v = sp == tid ? ml0 : ml_at(sp);
+        const float w = v.x == -INFINITY ? 0.0f : expf(v.x - mx);
+        w_s[sp] = w;
+        ls = fmaf(w, v.y, ls);
     }
+    ls = wave_sum_all(ls);
+    if (lane == 0)
+        red[wave].y = ls;
     __syncthreads();
     if (tid >= dh)
         return;
-    float L = 0.0f;
-    for (int sp = 0; sp < ns; ++sp)
-        L = fmaf(w_s[sp], ml_s[sp].y, L);
+    const float L = red[0].y + red[1].y;
     // the splits in order: the preloaded ones, then the rest 8 at a time
     float O = 0.0f;
 #pragma unroll
