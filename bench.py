@@ -95,15 +95,16 @@ def source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
 
 
-def traffic_for(kernel: str):
+def traffic_for(kernel: str, workload: str = "13b"):
     """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source."""
+    taken on the current kernel source and on the same workload's shapes
+    (the summary is the 13B verification microbenchmark's)."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     e = t.get("kernels", {}).get(kernel)
-    if not e or t.get("source_hash") != source_hash():
+    if not e or t.get("source_hash") != source_hash() or t.get("workload", "13b") != workload:
         return None
     return e["bytes_per_launch"]
 
@@ -352,7 +353,7 @@ def run_bench(args):
         achieved = nbytes / (avg_ms / 1e3) / 1e9
         roofline = {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_for(kt["kernel"]),
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_for(kt["kernel"], args.workload),
             "kernel": kt["kernel"], "layer": f"gate_up, verification of <= {regime} rows",
             "bytes_per_launch": int(nbytes), "avg_launch_us": round(avg_ms * 1e3, 2), "launches": kt["launches"],
         }

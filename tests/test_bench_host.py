@@ -130,6 +130,10 @@ def test_traffic_is_null_once_the_kernel_source_changes(tmp_path, monkeypatch):
     json.dump({"source_hash": bench.source_hash(), "kernels": {"k": {"bytes_per_launch": 123.0}}},
               open(tmp_path / "traffic.json", "w"))
     assert bench.traffic_for("k") == 123.0
+    assert bench.traffic_for("k", "13b") == 123.0
+    # the counters were taken on the 13B shapes: another workload's launch of
+    # the same kernel moves other bytes
+    assert bench.traffic_for("k", "7b") is None
     assert bench.traffic_for("another kernel") is None
     src.write_text("// version 2\n")
     assert bench.traffic_for("k") is None
