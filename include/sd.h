@@ -177,8 +177,8 @@ sd_status sd_forward(sd_model *model, const int32_t *tokens, int32_t n, const ui
  * (activations, split partials, attention partials, lm-head partials, the
  * control block) lives in a static device array of 32 MiB that each GPU the
  * library runs on holds until the process ends; a model and cache capacity
- * that need more (about 16 MiB at the 13B shape over 4096 positions, 30 MiB
- * at the 70B shape) are refused.  Every call on one GPU shares that GPU's
+ * that need more are refused (over 4096 positions the 13B shape needs about
+ * 28 MiB, the 70B shape 30 MiB).  Every call on one GPU shares that GPU's
  * array: calls that overlap on one GPU (other streams, other threads, other
  * models) race and must not be made.  The model's workspace and the cache
  * are the caller's, created beforehand (those calls allocate); the call

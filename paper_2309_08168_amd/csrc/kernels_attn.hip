@@ -1018,6 +1018,8 @@ hipError_t launch_attention(const AttnArgs &a0, bool bf16, int max_rows, hipStre
     // vectors per head fit; otherwise split the keys over work-groups
     if (max_q <= QH && a.cap <= 256)
         return bf16 ? launch_attn_head<uint16_t>(a, s) : launch_attn_head<float>(a, s);
+    // (the workspace holds the partials of 64-key chunks whenever a model can
+    // take this path: attn_chunk_min)
     const bool valu = bf16 && a.head_dim == 128 && max_q <= 2;
     a.chunk = valu ? ATTN_CHUNK_VALU : ATTN_CHUNK;
     a.splits = (a.cap + a.chunk - 1) / a.chunk;

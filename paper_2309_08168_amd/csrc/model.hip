@@ -326,8 +326,12 @@ sd_status ensure_rope(sd_model *m, int cap) {
     return SD_OK;
 }
 
+int attn_chunk_min_of(const sd_model *m) {
+    return attn_chunk_min(m->bf16, m->cfg.head_dim, m->cfg.n_heads, m->cfg.n_kv_heads);
+}
+
 sd_status ensure_attn(sd_model *m, int cap) {
-    const int splits = attn_split_slots(cap);
+    const int splits = attn_split_slots(cap, attn_chunk_min_of(m));
     if (splits <= m->attn_splits_cap)
         return SD_OK;
     SD_HIP(hipStreamSynchronize(m->stream));
@@ -1212,7 +1216,7 @@ size_t carve_workspace(const sd_model *m, int32_t cap, char *base, Workspace *w)
         off += (bytes + 255) & ~(size_t)255;
         return p;
     };
-    const size_t hd = (size_t)c.n_heads * c.head_dim, splits = (size_t)attn_split_slots(cap);
+    const size_t hd = (size_t)c.n_heads * c.head_dim, splits = (size_t)attn_split_slots(cap, attn_chunk_min_of(m));
     w->xld = xld_of(c);
     w->h = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * c.d_model));
     w->q = reinterpret_cast<float *>(take(sizeof(float) * MAX_ROWS * hd));

@@ -21,8 +21,14 @@ constexpr int MAX_HEAD_DIM = 128;
 // call combines: 65536 positions in 64-key chunks.
 constexpr int MAX_CONTEXT = 65536;
 constexpr int MAX_SPLITS = MAX_CONTEXT / ATTN_CHUNK_VALU;
-// Split partial slots a cache of capacity cap needs (the finest chunking).
-__host__ __device__ constexpr int attn_split_slots(int cap) { return (cap + ATTN_CHUNK_VALU - 1) / ATTN_CHUNK_VALU; }
+// Keys per chunk of the finest split a model's attention can take: 64 when
+// it can run the VALU kernel (bfloat16, head_dim 128, at most two query
+// heads per kv head), else 128; and the split partial slots a cache of
+// capacity cap then needs.
+__host__ __device__ constexpr int attn_chunk_min(bool bf16, int head_dim, int n_heads, int n_kv_heads) {
+    return (bf16 && head_dim == 128 && n_heads <= 2 * n_kv_heads) ? ATTN_CHUNK_VALU : ATTN_CHUNK;
+}
+__host__ __device__ constexpr int attn_split_slots(int cap, int chunk_min) { return (cap + chunk_min - 1) / chunk_min; }
 
 // Where and what the current forward computes.  Device resident: the
 // greedy head of one step writes the control block of the next step, so
