@@ -1171,6 +1171,8 @@ static hipError_t launch_mfma(const LinearArgs &a, int epi, int n_tiles, hipStre
 
 // The work-group shape follows the output kind and the packing count
 // (mfma_shape_tn / mfma_shape_nw).
+constexpr int MFMA_WIDE_TILES = 1600;
+
 static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipStream_t s,
                                  const LaunchTiming &t) {
     const int np = mfma_packs(a.max_rows);
@@ -1192,6 +1194,14 @@ static hipError_t launch_mfma_np(const LinearArgs &a, int epi, int n_tiles, hipS
     case 2:
         return launch_mfma<mfma_shape_tn(EPI_STORE, 2), mfma_shape_nw(EPI_STORE, 2), 2>(a, epi, n_tiles, s, t);
     case 3:
+        // Three packings on a wide gate/up or lm-head: eight tiles per
+        // work-group halve the activation-fragment loads per weight byte.
+        // Measured at the 13B shapes, 13 rows: gate/up (1728 tiles) 57.9 ->
+        // 53.2 us, lm-head (2000 tiles) 60.7 -> 58.0; QKV (960 tiles, 120
+        // work-groups of eight) 33.0 -> 50.6, and at 4 or 8 rows eight tiles
+        // lose everywhere.
+        if ((epi == EPI_SWIGLU || epi == EPI_HEAD) && n_tiles >= MFMA_WIDE_TILES)
+            return launch_mfma<8, 4, 3>(a, epi, n_tiles, s, t);
         return launch_mfma<mfma_shape_tn(EPI_STORE, 3), mfma_shape_nw(EPI_STORE, 3), 3>(a, epi, n_tiles, s, t);
     default:
         return hipErrorInvalidValue;

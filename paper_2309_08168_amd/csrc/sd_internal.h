@@ -111,7 +111,8 @@ __host__ __device__ constexpr int mfma_packs(int max_rows) { return (X_TERMS * m
 // MFMA work-group shape (16-row tiles per work-group, waves per work-group)
 // by output kind and packing count, from sweeps at the 13B shapes: two
 // tiles for the split-K output projections, four otherwise (at 4, 8 and 13
-// rows); four waves throughout.
+// rows); four waves throughout.  The launcher takes eight tiles for wide
+// gate/up and lm-head layers at three packings (launch_mfma_np).
 __host__ __device__ constexpr int mfma_shape_tn(int epi, int np) {
     return (void)np, epi == EPI_PARTIAL ? 2 : 4;
 }
