@@ -233,6 +233,142 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Wide GEMM with direct-to-LDS operand loads
+//
+// The same product and accumulation order as k_pf_gemm (bit-identical
+// results; plain stores) for layers with at least one 256 x 256 tile per CU: 256 weight
+// rows x 256 activation rows per work-group, 8 waves of 128 x 64 (32
+// accumulator tiles each, so each fragment read from LDS feeds 4 or 8
+// MFMAs), 32-k stages.  Operands go from global memory straight into LDS
+// with global_load_lds_dwordx4: one instruction fills one 1 KB fragment
+// block (lane l's 16 bytes at 16 l), so no registers stage them and no
+// second pass writes LDS.  Two 64 KB stage buffers: the loads of stage
+// s + 1 are issued right after the barrier that ends stage s - 1.  The
+// barrier is a bare s_barrier: a release fence before it would also wait
+// for the next stage's loads.  K must be a multiple of 32.
+
+constexpr int GW_M = 256;                                        // activation rows per work-group
+constexpr int GW_MIN_TILES = 224;                                // tiles that make a launch "wide"
+constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage
+constexpr int GW_PER = GW_BLOCKS / 8;                            // load instructions per wave per stage
+static_assert(GW_BLOCKS % 8 == 0, "blocks per wave");
+
+// s_waitcnt immediate (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8) that waits for vmcnt 0 and leaves the other counters alone
+constexpr int WAIT_VMCNT0 = (7 << 4) | (15 << 8);
+
+__device__ __forceinline__ void load_to_lds16(const uint16_t *g, uint16_t *l) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)g,
+                                     (__attribute__((address_space(3))) void *)l, 16, 0, 0);
+}
+
+__global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
+    constexpr int T = X_TERMS, NWN = 2, NWM = 4;
+    constexpr int WN = GB_N / NWN, WM = GW_M / NWM;   // 128 x 64 per wave
+    constexpr int NT = WN / 16, MT = WM / 16;
+    constexpr int NBW = GB_N / 16;                     // weight blocks per stage
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * GW_BLOCKS * 512];
+
+    const int M = a.M, N = a.N, K = a.K;
+    // tile order as in k_pf_gemm: each XCD a contiguous range, walked in
+    // groups of up to 4 row tiles
+    const int TM = (M + GW_M - 1) / GW_M, TN = (N + GB_N - 1) / GB_N, TT = TM * TN;
+    const int per = (TT + 7) / 8;
+    const int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    if (L >= TT)
+        return;  // uniform over the work-group
+    const int GM = TM < 4 ? TM : 4;
+    const int grp_i = L / (GM * TN), first = grp_i * GM, gm = min(TM - first, GM);
+    const int in = L - grp_i * GM * TN;
+    const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * GB_N;
+    const int S = K / GB_K;
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int wn = wave % NWN, wm = wave / NWN;
+
+    // block b of a stage: b < NBW the weight rows n0 + 16 b .., else term t
+    // of activation rows m0 + 16 rg ..; lane l loads row 16 b + l % 16,
+    // k chunk l / 16 (rows past the end read the last row: never stored)
+    const uint16_t *src[GW_PER];
+#pragma unroll
+    for (int i = 0; i < GW_PER; ++i) {
+        const int b = wave + 8 * i;
+        if (b < NBW) {
+            src[i] = a.W + (int64_t)min(n0 + 16 * b + (lane & 15), N - 1) * K + 8 * (lane >> 4);
+        } else {
+            const int c = b - NBW, t = c / (GW_M / 16), rg = c % (GW_M / 16);
+            src[i] = a.A + t * a.a_term + (int64_t)min(m0 + 16 * rg + (lane & 15), M - 1) * a.lda + 8 * (lane >> 4);
+        }
+    }
+    auto issue = [&](int stage) {
+        uint16_t *dst = lds + (stage & 1) * GW_BLOCKS * 512;
+#pragma unroll
+        for (int i = 0; i < GW_PER; ++i)
+            load_to_lds16(src[i] + stage * GB_K, dst + (wave + 8 * i) * 512);
+    };
+
+    f32x4_t acc[NT][MT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+            acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    if (S > 0)
+        issue(0);
+    for (int s = 0; s < S; ++s) {
+        // this wave's stage-s blocks have landed (nothing else is in flight)
+        __builtin_amdgcn_s_waitcnt(WAIT_VMCNT0);
+        // all waves' blocks have landed and every wave's reads of the other
+        // buffer (stage s - 1) have returned
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (s + 1 < S)
+            issue(s + 1);
+        const uint16_t *ws = lds + (s & 1) * GW_BLOCKS * 512, *as = ws + NBW * 512;
+        u32x4_t wf[NT], af[MT][T];
+#pragma unroll
+        for (int i = 0; i < NT; ++i)
+            wf[i] = *reinterpret_cast<const u32x4_t *>(&ws[(wn * NT + i) * 512 + lane * 8]);
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+                af[j][t] = *reinterpret_cast<const u32x4_t *>(&as[(t * (GW_M / 16) + wm * MT + j) * 512 + lane * 8]);
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int i = 0; i < NT; ++i)
+#pragma unroll
+                for (int j = 0; j < MT; ++j)
+                    acc[i][j] = mfma16(wf[i], af[j][t], acc[i][j]);
+    }
+
+    // lane holds C^T[n0 + wn WN + 16 i + 4 grp + v][m0 + wm WM + 16 j + col]
+    const int col = lane & 15, grp = lane >> 4;
+    float *C = a.C;
+    const bool vec = (a.ldc & 3) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        const int n = n0 + wn * WN + 16 * i + 4 * grp;
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            const int m = m0 + wm * WM + 16 * j + col;
+            if (m >= M || n >= N)
+                continue;
+            float *c = C + (int64_t)m * a.ldc + n;
+            if (vec && n + 3 < N) {
+                *reinterpret_cast<f32x4_t *>(c) = acc[i][j];
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (n + v < N)
+                        c[v] = acc[i][j][v];
+            }
+        }
+    }
+}
+
 // C[m][n] += part[0][m][n] + part[1][m][n] + ..., in split order.
 __global__ __launch_bounds__(256) void k_pf_split_sum(const float *part, int splits, int64_t stride, float *C,
                                                       int64_t n_elems) {
@@ -515,6 +651,15 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
     if (a.M < 1 || a.N < 1 || a.K < 8 || a.K % 8 || a.lda % 8 || a.M > PF_ROWS)
         return hipErrorInvalidValue;
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
+    // The widest layers (at least 224 tiles of 256 x 256, most of one per
+    // CU): direct-to-LDS loads (13B shape, 1023 rows: QKV 509 -> 456 us,
+    // gate/up 959 -> 881 us).  Below that the 256 x 128 tiles keep more CUs
+    // busy.
+    const int wide_tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GW_M - 1) / GW_M);
+    if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
+        hipLaunchKernelGGL(k_pf_gemm_wide, dim3(8 * ((wide_tiles + 7) / 8)), dim3(G_THREADS), 0, s, a);
+        return hipGetLastError();
+    }
     // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
     // flight; narrow ones: split residual updates (below), else 2 x 4 waves
     // with two stages in flight

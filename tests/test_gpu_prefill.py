@@ -38,6 +38,9 @@ ODD_BF16 = S.ModelConfig("odd_bf16", 2, 136, 3, 1, 32, 200, 777, "bf16")
 # wide enough that the residual-update GEMMs split their reduction (2 ways
 # for the output projection, 4 for the down projection)
 WIDE_BF16 = S.ModelConfig("wide_bf16", 1, 1024, 8, 8, 128, 2048, 512, "bf16")
+# a gate/up GEMM wide enough (14400 columns: 57 tiles of 256, the last one
+# 64 wide) that forwards of 769 rows or more take the direct-to-LDS kernel
+FFN_WIDE_BF16 = S.ModelConfig("ffn_wide_bf16", 1, 256, 4, 4, 64, 7200, 512, "bf16")
 MODELS = {"mini_bf16": U.MINI_BF16, "odd_bf16": ODD_BF16, "gqa8_dh128": A.CONFIGS["gqa8_dh128"],
           "wide_bf16": WIDE_BF16}
 _models = {}
@@ -66,6 +69,22 @@ def test_long_forward_from_zero(name, rows):
     got = _logits(dm, toks, dm.cache(rows))
     r = U.check_logits(cfg, got, ref, f"{name} {rows} rows")
     print(f"{name} {rows} rows from 0: max |d| / tol {r:.3f}")
+
+
+@pytest.mark.parametrize("rows", [1000, 1024])
+def test_forward_on_the_wide_gemm(rows):
+    """gate/up of 4 x 57 tiles of 256 x 256 (a ragged last row tile at 1000
+    rows, a 64-column last column tile): the direct-to-LDS GEMM."""
+    if ("ffn_wide_bf16", 0) not in _models:
+        cfg = FFN_WIDE_BF16
+        w = S.make_weights(cfg, 0)
+        _models[("ffn_wide_bf16", 0)] = (cfg, w, oracle.Model(cfg, w), U.device_model(cfg, w))
+    cfg, w, om, dm = _models[("ffn_wide_bf16", 0)]
+    toks = S.prompt(cfg, rows, seed=rows + 5)
+    ref = om.score(toks)["logits"]
+    got = _logits(dm, toks, dm.cache(rows))
+    r = U.check_logits(cfg, got, ref, f"ffn_wide_bf16 {rows} rows")
+    print(f"ffn_wide_bf16 {rows} rows from 0: max |d| / tol {r:.3f}")
 
 
 @pytest.mark.parametrize("name", ["mini_bf16", "odd_bf16"])
