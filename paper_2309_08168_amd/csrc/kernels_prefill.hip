@@ -237,10 +237,10 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 // Wide GEMM with direct-to-LDS operand loads
 //
 // The same product and accumulation order as k_pf_gemm (bit-identical
-// results; plain stores) for layers with at least one 256 x 256 tile per CU: 256 weight
-// rows x 256 activation rows per work-group, 8 waves of 128 x 64 (32
-// accumulator tiles each, so each fragment read from LDS feeds 4 or 8
-// MFMAs), 32-k stages.  Operands go from global memory straight into LDS
+// results; plain stores) for layers with at least 128 tiles of 256 x 256:
+// 256 weight rows x 256 activation rows per work-group, 8 waves of
+// 128 x 64 (32 accumulator tiles each, so each fragment read from LDS
+// feeds 4 or 8 MFMAs), 32-k stages.  Operands go from global memory straight into LDS
 // with global_load_lds_dwordx4: one instruction fills one 1 KB fragment
 // block (lane l's 16 bytes at 16 l), so no registers stage them and no
 // second pass writes LDS.  Two 64 KB stage buffers: the loads of stage
@@ -249,7 +249,7 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 // for the next stage's loads.  K must be a multiple of 32.
 
 constexpr int GW_M = 256;                                        // activation rows per work-group
-constexpr int GW_MIN_TILES = 224;                                // tiles that make a launch "wide"
+constexpr int GW_MIN_TILES = 128;                                // tiles that make a launch "wide"
 constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage
 constexpr int GW_PER = GW_BLOCKS / 8;                            // load instructions per wave per stage
 static_assert(GW_BLOCKS % 8 == 0, "blocks per wave");
@@ -651,10 +651,12 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
     if (a.M < 1 || a.N < 1 || a.K < 8 || a.K % 8 || a.lda % 8 || a.M > PF_ROWS)
         return hipErrorInvalidValue;
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
-    // The widest layers (at least 224 tiles of 256 x 256, most of one per
-    // CU): direct-to-LDS loads (13B shape, 1023 rows: QKV 509 -> 456 us,
-    // gate/up 959 -> 881 us).  Below that the 256 x 128 tiles keep more CUs
-    // busy.
+    // Wide layers (at least 128 tiles of 256 x 256) take the direct-to-LDS
+    // kernel.  Both kernels fill the same fraction of the last round (one
+    // 256 x 256 work-group per CU against two of 256 x 128), so the wide one
+    // wins wherever half the CUs have a tile (1023 rows: 13B QKV 509 -> 456
+    // us, gate/up 959 -> 881; 7B QKV 368 -> 335, gate/up 646 -> 661; 70B
+    // QKV 653 -> 599, gate/up 2640 -> 2603).
     const int wide_tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GW_M - 1) / GW_M);
     if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
         hipLaunchKernelGGL(k_pf_gemm_wide, dim3(8 * ((wide_tiles + 7) / 8)), dim3(G_THREADS), 0, s, a);

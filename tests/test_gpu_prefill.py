@@ -39,7 +39,7 @@ ODD_BF16 = S.ModelConfig("odd_bf16", 2, 136, 3, 1, 32, 200, 777, "bf16")
 # for the output projection, 4 for the down projection)
 WIDE_BF16 = S.ModelConfig("wide_bf16", 1, 1024, 8, 8, 128, 2048, 512, "bf16")
 # a gate/up GEMM wide enough (14400 columns: 57 tiles of 256, the last one
-# 64 wide) that forwards of 769 rows or more take the direct-to-LDS kernel
+# 64 wide) that forwards of 513 rows or more take the direct-to-LDS kernel
 FFN_WIDE_BF16 = S.ModelConfig("ffn_wide_bf16", 1, 256, 4, 4, 64, 7200, 512, "bf16")
 MODELS = {"mini_bf16": U.MINI_BF16, "odd_bf16": ODD_BF16, "gqa8_dh128": A.CONFIGS["gqa8_dh128"],
           "wide_bf16": WIDE_BF16}
@@ -71,10 +71,10 @@ def test_long_forward_from_zero(name, rows):
     print(f"{name} {rows} rows from 0: max |d| / tol {r:.3f}")
 
 
-@pytest.mark.parametrize("rows", [1000, 1024])
+@pytest.mark.parametrize("rows", [600, 1000, 1024])
 def test_forward_on_the_wide_gemm(rows):
-    """gate/up of 4 x 57 tiles of 256 x 256 (a ragged last row tile at 1000
-    rows, a 64-column last column tile): the direct-to-LDS GEMM."""
+    """gate/up of 3 or 4 x 57 tiles of 256 x 256 (a ragged last row tile at
+    600 and 1000 rows, a 64-column last column tile): the direct-to-LDS GEMM."""
     if ("ffn_wide_bf16", 0) not in _models:
         cfg = FFN_WIDE_BF16
         w = S.make_weights(cfg, 0)
