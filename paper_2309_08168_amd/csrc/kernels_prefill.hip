@@ -585,6 +585,46 @@ __global__ __launch_bounds__(256) void k_pf_norm_split(const float *h, int K, co
     }
 }
 
+// h[m] += the split partials (in split order), then g * h / rms(h) as terms:
+// the arithmetic of k_pf_split_sum followed by k_pf_norm_split, in one pass
+// over the row (each thread re-reads only elements the work-group wrote
+// before the barrier).
+__global__ __launch_bounds__(256) void k_pf_fold_norm_split(float *h, const float *part, int splits, int64_t stride,
+                                                            int K, const uint16_t *gain, float eps, uint16_t *out,
+                                                            int64_t out_term) {
+    __shared__ float red[4];
+    const int m = blockIdx.x, tid = threadIdx.x;
+    float *x = h + (int64_t)m * K;
+    const float *p = part + (int64_t)m * K;
+    float ss = 0.0f;
+    for (int k = tid; k < K; k += 256) {
+        float v = p[k];
+        for (int s = 1; s < splits; ++s)
+            v += p[(int64_t)s * stride + k];
+        const float hn = x[k] + v;
+        x[k] = hn;
+        ss = fmaf(hn, hn, ss);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        ss += __shfl_xor(ss, o, 64);
+    if ((tid & 63) == 0)
+        red[tid >> 6] = ss;
+    __syncthreads();
+    const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + eps);
+    for (int k = 8 * tid; k < K; k += 8 * 256) {
+        float u[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            u[j] = bf_to_f(gain[k + j]) * (x[k + j] * inv);
+        u32x4_t t[X_TERMS];
+        split8(u, t);
+#pragma unroll
+        for (int i = 0; i < X_TERMS; ++i)
+            *reinterpret_cast<u32x4_t *>(out + i * out_term + (int64_t)m * K + k) = t[i];
+    }
+}
+
 __global__ __launch_bounds__(256) void k_pf_rope_kv(const float *qkv, int start, const float2 *rope, int H, int KVH,
                                                     int dh, float *q, uint16_t *kc, uint16_t *vc, int64_t stride) {
     const int m = blockIdx.x, pos = start + m, half = dh >> 1;
@@ -647,7 +687,26 @@ hipError_t launch_pf_norm_split(const float *h, int K, int M, const uint16_t *ga
     return hipGetLastError();
 }
 
-hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
+hipError_t launch_pf_fold_norm_split(float *h, const float *part, int splits, int K, int M, const uint16_t *gain,
+                                     float eps, uint16_t *out, int64_t out_term, hipStream_t s) {
+    if (K % 8 || splits < 1 || splits > PF_MAX_SPLITS)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pf_fold_norm_split, dim3(M), dim3(256), 0, s, h, part, splits, (int64_t)M * K, K, gain, eps,
+                       out, out_term);
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_split_sum(const float *part, int splits, int64_t n, float *C, hipStream_t s) {
+    if (splits < 1 || splits > PF_MAX_SPLITS || n < 1)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pf_split_sum, dim3((unsigned)std::min<int64_t>((n + 255) / 256, 4096)), dim3(256), 0, s, part,
+                       splits, n, C, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold) {
+    if (fold)
+        *fold = 0;
     if (a.M < 1 || a.N < 1 || a.K < 8 || a.K % 8 || a.lda % 8 || a.M > PF_ROWS)
         return hipErrorInvalidValue;
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
@@ -692,9 +751,14 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s) {
     const dim3 grid(8 * ((tiles * b.splits + 7) / 8)), block(G_THREADS);
     if (splits > 1) {
         hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
-        const int64_t n = (int64_t)a.M * a.ldc;
-        hipLaunchKernelGGL(k_pf_split_sum, dim3((unsigned)std::min<int64_t>((n + 255) / 256, 4096)), dim3(256), 0, s,
-                           a.part, splits, n, a.C, n);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        if (fold && a.ldc == a.N) {
+            *fold = splits;  // the next norm adds the partials
+            return hipSuccess;
+        }
+        return launch_pf_split_sum(a.part, splits, (int64_t)a.M * a.ldc, a.C, s);
     } else if (epi == EPI_STORE) {
         hipLaunchKernelGGL((k_pf_gemm<EPI_STORE, 2, 4, 2>), grid, block, 0, s, b);
     } else if (epi == EPI_RESID) {

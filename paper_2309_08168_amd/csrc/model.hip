@@ -718,6 +718,9 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
     const int64_t head_stride = (int64_t)cap * dh;
     const int64_t xt = m->pf_term;
     hipStream_t s = m->stream;
+    // A split residual update leaves its partials in pf_part; the next norm
+    // adds them into the residual stream (fold = their count, 0: none).
+    int fold = 0;
     auto gemm = [&](const void *W, int N, int K, float *C, int64_t ldc, int epi) {
         PfGemmArgs g{};
         g.W = static_cast<const uint16_t *>(W);
@@ -730,12 +733,17 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
         g.K = K;
         g.lda = K;
         g.part = epi == EPI_RESID ? m->pf_part : nullptr;  // [PF_MAX_SPLITS][M][d]: split reductions
-        return launch(launch_pf_gemm(g, epi, s), "prefill GEMM");
+        return launch(launch_pf_gemm(g, epi, s, epi == EPI_RESID && C == m->pf_h ? &fold : nullptr), "prefill GEMM");
     };
     auto norm = [&](const void *gain) {
-        return launch(launch_pf_norm_split(m->pf_h, d, M, static_cast<const uint16_t *>(gain), c.rms_eps, m->pf_x,
-                                           xt, s),
-                      "prefill norm");
+        const uint16_t *g = static_cast<const uint16_t *>(gain);
+        if (fold) {
+            const int f = fold;
+            fold = 0;
+            return launch(launch_pf_fold_norm_split(m->pf_h, m->pf_part, f, d, M, g, c.rms_eps, m->pf_x, xt, s),
+                          "prefill norm");
+        }
+        return launch(launch_pf_norm_split(m->pf_h, d, M, g, c.rms_eps, m->pf_x, xt, s), "prefill norm");
     };
     SD_TRY(launch(launch_pf_embed(static_cast<const uint16_t *>(m->tok_emb), d, dev_tokens, M, m->pf_h, s),
                   "prefill embedding"));
@@ -775,6 +783,9 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
     if (logits) {
         SD_TRY(norm(m->final_norm));
         SD_TRY(gemm(m->lm_head, c.vocab, d, logits, c.vocab, EPI_STORE));
+    } else if (fold) {
+        // no norm follows: leave the residual stream whole
+        SD_TRY(launch(launch_pf_split_sum(m->pf_part, fold, (int64_t)M * d, m->pf_h, s), "prefill split sum"));
     }
     return SD_OK;
 }

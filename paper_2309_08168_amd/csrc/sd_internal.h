@@ -292,7 +292,17 @@ hipError_t launch_pf_embed(const uint16_t *emb, int d, const int32_t *tokens, in
 // g * h / rms(h) of every row (g: gain [K] bf16), as X_TERMS terms into out.
 hipError_t launch_pf_norm_split(const float *h, int K, int M, const uint16_t *gain, float eps, uint16_t *out,
                                 int64_t out_term, hipStream_t s);
-hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s);
+// The same after folding split-K partials into h: h[m] += part[0][m] +
+// part[1][m] + ... (splits of them, [splits][M][K], in split order) first.
+hipError_t launch_pf_fold_norm_split(float *h, const float *part, int splits, int K, int M, const uint16_t *gain,
+                                     float eps, uint16_t *out, int64_t out_term, hipStream_t s);
+// C = A W^T (EPI_STORE) or C += A W^T (EPI_RESID).  A narrow EPI_RESID may
+// split its reduction into a.part; with fold null the partials are added
+// into C before the call returns (on the stream), else *fold receives the
+// number of splits left in a.part for launch_pf_fold_norm_split (0: none).
+hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold = nullptr);
+// C[i] += part[0][i] + part[1][i] + ... for i < n (part [splits][n]).
+hipError_t launch_pf_split_sum(const float *part, int splits, int64_t n, float *C, hipStream_t s);
 // Rotary embedding of q and k from the QKV GEMM output [M][(H + 2 KVH) dh];
 // q into q [M][H dh], k and v into the cache at positions start + m.
 hipError_t launch_pf_rope_kv(const float *qkv, int M, int start, const float2 *rope, int H, int KVH, int dh,

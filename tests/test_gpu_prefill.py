@@ -38,17 +38,22 @@ ODD_BF16 = S.ModelConfig("odd_bf16", 2, 136, 3, 1, 32, 200, 777, "bf16")
 # wide enough that the residual-update GEMMs split their reduction (2 ways
 # for the output projection, 4 for the down projection)
 WIDE_BF16 = S.ModelConfig("wide_bf16", 1, 1024, 8, 8, 128, 2048, 512, "bf16")
+# two layers whose output and down projections split their reduction (2
+# and 4 ways): each split's partials are added into the residual stream by
+# the norm that follows, whichever sublayer that is
+WIDE2_BF16 = S.ModelConfig("wide2_bf16", 2, 1024, 8, 8, 128, 2048, 512, "bf16")
 # a gate/up GEMM wide enough (14400 columns: 57 tiles of 256, the last one
 # 64 wide) that forwards of 513 rows or more take the direct-to-LDS kernel
 FFN_WIDE_BF16 = S.ModelConfig("ffn_wide_bf16", 1, 256, 4, 4, 64, 7200, 512, "bf16")
 MODELS = {"mini_bf16": U.MINI_BF16, "odd_bf16": ODD_BF16, "gqa8_dh128": A.CONFIGS["gqa8_dh128"],
           "wide_bf16": WIDE_BF16}
+EXTRA = {"ffn_wide_bf16": FFN_WIDE_BF16, "wide2_bf16": WIDE2_BF16}
 _models = {}
 
 
 def _pair(name, seed=0):
     if (name, seed) not in _models:
-        cfg = MODELS[name]
+        cfg = MODELS[name] if name in MODELS else EXTRA[name]
         w = S.make_weights(cfg, seed)
         _models[(name, seed)] = (cfg, w, oracle.Model(cfg, w), U.device_model(cfg, w))
     return _models[(name, seed)]
@@ -75,11 +80,7 @@ def test_long_forward_from_zero(name, rows):
 def test_forward_on_the_wide_gemm(rows):
     """gate/up of 3 or 4 x 57 tiles of 256 x 256 (a ragged last row tile at
     600 and 1000 rows, a 64-column last column tile): the direct-to-LDS GEMM."""
-    if ("ffn_wide_bf16", 0) not in _models:
-        cfg = FFN_WIDE_BF16
-        w = S.make_weights(cfg, 0)
-        _models[("ffn_wide_bf16", 0)] = (cfg, w, oracle.Model(cfg, w), U.device_model(cfg, w))
-    cfg, w, om, dm = _models[("ffn_wide_bf16", 0)]
+    cfg, w, om, dm = _pair("ffn_wide_bf16")
     toks = S.prompt(cfg, rows, seed=rows + 5)
     ref = om.score(toks)["logits"]
     got = _logits(dm, toks, dm.cache(rows))
@@ -109,6 +110,42 @@ def test_forward_of_two_chunks():
     got = _logits(dm, toks, dm.cache(1100))
     r = U.check_logits(cfg, got, ref, "1100 rows")
     print(f"mini_bf16 1100 rows (two chunks): max |d| / tol {r:.3f}")
+
+
+@pytest.mark.parametrize("mask", ["none", "1", "2", "3"])
+def test_split_partials_fold_into_the_next_norm(mask):
+    """Split output and down projections on a two-layer model: unmasked the
+    partials go into the next MLP or attention norm and the final norm; with
+    layer 0's MLP skipped (1) the output projection's go into layer 1's
+    attention norm, with layer 1's attention skipped (2) the down
+    projection's into layer 1's MLP norm, with layer 1's MLP skipped (3)
+    into the final norm."""
+    cfg, w, om, dm = _pair("wide2_bf16")
+    z = S.skip_mask(cfg, mask, seed=0)
+    toks = S.prompt(cfg, 300, seed=31)
+    ref = om.forward(om.cache(300), toks, skip=z)["logits"]
+    got = _logits(dm, toks, dm.cache(300), skip=z)
+    r = U.check_logits(cfg, got, ref, f"wide2_bf16 mask {mask} 300 rows")
+    print(f"wide2_bf16 mask {mask}: max |d| / tol {r:.3f}")
+
+
+def test_generate_after_a_split_prefill():
+    """The prompt prefill of a model with split residual updates and no
+    logits: the last down projection's partials are added by a plain sum, and
+    layer 1's keys and values depend on every fold before them."""
+    cfg, w, om, dm = _pair("wide2_bf16")
+    pr = S.prompt(cfg, 200, seed=23)
+    z = S.skip_mask(cfg, "1", seed=0)
+    ar_ref, ar_margin = om.generate_ar(pr, 16)
+    sd_ref = om.generate_sd(pr, 16, z, 4, 0.0)
+    ar, _ = dm.generate_ar(pr, 16)
+    sd, _ = dm.generate_sd(pr, 16, z, 4, 0.0)
+    std = om.score(np.concatenate([pr, ar_ref])[:-1])["logits"][len(pr) - 1:].std(axis=1)
+    n_ar = U.check_free_running(cfg, ar, ar_ref, ar_margin, std, "wide2_bf16 AR after 200")
+    n_sd = U.check_free_running(cfg, sd, sd_ref["tokens"], sd_ref["margin"], std, "wide2_bf16 SD after 200")
+    U.check_tokens_teacher_forced(cfg, om, pr, sd, "wide2_bf16 SD after 200 teacher-forced")
+    U.check_tokens_teacher_forced(cfg, om, pr, ar, "wide2_bf16 AR after 200 teacher-forced")
+    print(f"wide2_bf16: AR equal for {n_ar}/16, SD for {n_sd}/16 after a 200-token prompt")
 
 
 @pytest.mark.parametrize("name", ["mini_bf16", "odd_bf16"])
