@@ -1124,18 +1124,17 @@ static hipError_t launch_valu_r(const LinearArgs &a, int epi, int R, int n_tiles
     }
 }
 
-// Two rows on one-wave tiles (bf16 weights): loads of two chunks in flight
-// for 4 weight rows, one chunk for 8 (a sweep at the 13B shapes).
-static hipError_t launch_valu_wave2(const LinearArgs &a, int epi, int R, int n_tiles, hipStream_t s,
+// Two rows on one-wave tiles (bf16 weights): 4 weight rows with one or two
+// chunks' loads in flight, or 8 rows with one (the plan picks per shape).
+static hipError_t launch_valu_wave2(const LinearArgs &a, int epi, int R, int U, int n_tiles, hipStream_t s,
                                     const LaunchTiming &t) {
-    switch (R) {
-    case 4:
+    if (R == 4 && U == 2)
         return launch_valu<uint16_t, 2, 4, 64, 2>(a, epi, n_tiles, s, t);
-    case 8:
+    if (R == 4 && U == 1)
+        return launch_valu<uint16_t, 2, 4, 64, 1>(a, epi, n_tiles, s, t);
+    if (R == 8 && U == 1)
         return launch_valu<uint16_t, 2, 8, 64, 1>(a, epi, n_tiles, s, t);
-    default:
-        return hipErrorInvalidValue;
-    }
+    return hipErrorInvalidValue;
 }
 
 template <int TN, int NW, int NP>
@@ -1216,7 +1215,7 @@ hipError_t launch_head_finalize(const LinearArgs &a, int n_tiles, hipStream_t s)
 }
 
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
-                         hipStream_t s, const LaunchTiming &t) {
+                         hipStream_t s, const LaunchTiming &t, int chunks) {
     if (n_tiles <= 0)
         return hipSuccess;
     if (path == PATH_MFMA) {
@@ -1250,7 +1249,9 @@ hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int 
         return bf16 ? launch_valu_r<uint16_t, 2>(a, epi, rows_per_tile, n_tiles, s, t)
                     : launch_valu_r<float, 2>(a, epi, rows_per_tile, n_tiles, s, t);
     if (path == PATH_WAVE2)
-        return bf16 ? launch_valu_wave2(a, epi, rows_per_tile, n_tiles, s, t) : hipErrorInvalidValue;
+        return bf16 ? launch_valu_wave2(a, epi, rows_per_tile, chunks ? chunks : wave2_default_chunks(rows_per_tile),
+                                        n_tiles, s, t)
+                    : hipErrorInvalidValue;
     return bf16 ? launch_valu_r<uint16_t, 16>(a, epi, rows_per_tile, n_tiles, s, t)
                 : launch_valu_r<float, 16>(a, epi, rows_per_tile, n_tiles, s, t);
 }

@@ -69,6 +69,7 @@ struct Plan {
     int n_tiles;  // GEMV/VALU: work-groups; MFMA: 16-row tiles
     int waves;    // MFMA: waves per work-group splitting the reduction
     int splits;   // MFMA output projections: split-K partials folded by the next norm
+    int chunks;   // PATH_WAVE2: loads in flight per wave (0: the path's default)
     int N, K, epi;
 };
 
@@ -229,6 +230,24 @@ Plan make_plan(const sd_model *m, LinearKind kind, int rows) {
     if (rows == 2 && m->bf16) {
         p.path = PATH_WAVE2;
         p.rows = kind == LK_QKV ? qkv_gemv_rows(c.head_dim, 8) : ((kind == LK_O || kind == LK_DOWN) ? 4 : 8);
+        // Shapes where another tile measured faster: the 70B output and down
+        // projections with one chunk's loads in flight (standalone 24.5
+        // against 25.8 us and 76.9 against 81.9; the 70B two-row
+        // verification 24.37 -> 22.66 ms).  At 7B neither 4-row QKV and
+        // gate/up tiles (standalone 21.5 against 23.9 us, 35.1 against 36.2)
+        // nor one chunk in flight for O and down made the verification
+        // faster (2.98 -> 3.03 and 3.10 ms), so it keeps these defaults.
+        struct Tuned {
+            int kind, N, K, rows, chunks;
+        };
+        static const Tuned tuned[] = {{LK_O, 8192, 8192, 4, 1}, {LK_DOWN, 8192, 28672, 4, 1}};
+        for (const Tuned &t : tuned) {
+            const bool fits = kind != LK_QKV || qkv_gemv_rows(c.head_dim, t.rows) == t.rows;
+            if (t.kind == kind && t.N == p.N && t.K == p.K && fits) {
+                p.rows = t.rows;
+                p.chunks = t.chunks;
+            }
+        }
         if (kind == LK_QKV)
             p.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * ((c.head_dim / 2) / (p.rows / 2));
         else if (kind == LK_GATE_UP)
@@ -420,7 +439,8 @@ sd_status run_linear(sd_model *m, const Workspace &w, const Plan &p, int max_row
         lt.start = m->tev[m->tev_used];
         lt.stop = m->tev[m->tev_used + 1];
     }
-    SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream, lt), "linear layer"));
+    SD_TRY(launch(launch_linear(a, p.epi, m->bf16, p.path, p.rows, p.n_tiles, m->stream, lt, p.chunks),
+                  "linear layer"));
     if (timed)
         m->tev_used += 2;
     if (p.epi == EPI_HEAD && epi.head.sampled) {
@@ -1531,7 +1551,7 @@ std::string kernel_symbol(const sd_model *m, const Plan &p) {
                        ? 1
                        : ((p.path == PATH_VALU2 || p.path == PATH_WAVE2) ? 2 : 16);
     const bool wave = p.path == PATH_WAVE2;
-    const int nt = wave ? 64 : 256, u = wave && p.rows == 4 ? 2 : 1;
+    const int nt = wave ? 64 : 256, u = wave ? (p.chunks ? p.chunks : wave2_default_chunks(p.rows)) : 1;
     return std::string("void sdk::k_linear_valu<") + tw + ", " + std::to_string(mr) + ", " + std::to_string(p.rows) +
            ", " + std::to_string(p.epi) + ", " + (norm ? "true" : "false") + ", " + std::to_string(nt) + ", " +
            std::to_string(u) + ">(sdk::LinearArgs)";

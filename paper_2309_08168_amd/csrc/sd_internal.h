@@ -323,8 +323,13 @@ struct LaunchTiming {
 };
 
 // Host-side launchers (kernels_*.hip).  bf16 selects bfloat16 weights and KV.
+// chunks: PATH_WAVE2 loads in flight per wave (1 or 2; 0: two for 4 weight
+// rows, one for 8).
 hipError_t launch_linear(const LinearArgs &a, int epi, bool bf16, int path, int rows_per_tile, int n_tiles,
-                         hipStream_t s, const LaunchTiming &t = LaunchTiming{});
+                         hipStream_t s, const LaunchTiming &t = LaunchTiming{}, int chunks = 0);
+// PATH_WAVE2 loads in flight for a tile of `rows` weight rows when the plan
+// leaves it open.
+constexpr int wave2_default_chunks(int rows) { return rows == 4 ? 2 : 1; }
 // FP8 E4M3 copy of a bf16 matrix [N][K]: bytes Q [N][K] and the exponent of
 // each row's power-of-two scale E [N] (see k_quantize_fp8).
 hipError_t launch_quantize_fp8(const uint16_t *W, int32_t N, int32_t K, uint8_t *Q, int32_t *E, hipStream_t s);
