@@ -11,7 +11,8 @@
 //     XCD's L2; layers with fewer tiles than CUs split the reduction in two;
 //   - k_pf_attn: causal attention, one wave per 16 query rows of a head,
 //     scores and the weighted sum of values on matrix cores with an online
-//     softmax over 32-key blocks;
+//     softmax over 32-key blocks, the longest row blocks dispatched first and
+//     spread evenly over the XCDs;
 //   - small row kernels between them: embedding, RMSNorm + split, rotary
 //     embedding + KV append, SwiGLU + split.
 #include "sd_internal.h"
@@ -25,6 +26,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 __device__ __forceinline__ f32x4_t mfma16(u32x4_t a, u32x4_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
@@ -404,8 +407,15 @@ __global__ __launch_bounds__(256) void k_pf_attn(PfAttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[4][PA_KB * VP];
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
-    const int head = blockIdx.y, g = head / (a.n_heads / a.n_kv_heads);
-    const int r0 = blockIdx.x * 64 + wave * 16;
+    // Work-group i takes head i % H and row block TM - 1 - i / H: the
+    // longest row blocks (most keys) start first, and consecutive indices,
+    // which the dispatcher deals to the 8 XCDs in turn, carry the same mix of
+    // row blocks on every XCD.  (With the row block as the fast grid index,
+    // row blocks x and x + 8 of every head landed on one XCD: the one holding
+    // the last row blocks had 2.4 times the work of the lightest.)
+    const int TM = (a.M + 63) / 64;
+    const int head = (int)(blockIdx.x % a.n_heads), g = head / (a.n_heads / a.n_kv_heads);
+    const int r0 = (TM - 1 - (int)(blockIdx.x / a.n_heads)) * 64 + wave * 16;
     if (r0 >= a.M)
         return;  // uniform over the wave; the waves never synchronise
     const bool qok = r0 + col < a.M;
@@ -496,7 +506,7 @@ __global__ __launch_bounds__(256) void k_pf_attn(PfAttnArgs a) {
         split8(p, pf);
 
         // values of the block into the wave's tile (after the previous
-        // block's gathers), then O^T += V^T P^T tile by tile
+        // block's reads), then O^T += V^T P^T tile by tile
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 #pragma unroll
         for (int j = 0; j < NVJ; ++j)
@@ -504,13 +514,19 @@ __global__ __launch_bounds__(256) void k_pf_attn(PfAttnArgs a) {
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 #pragma unroll
         for (int et = 0; et < ET; ++et) {
+            // A operand V^T: lane (col, grp) needs column 16 et + col of keys
+            // kb + 16 (u >> 2) + 4 (u & 3) + grp, u = 0..7 (the score slots).
+            // ds_read_b64_tr_b16 hands lane l of each 16-lane group element
+            // l % 4 of the 8 bytes that lanes l / 4 + 4 k (k = 0..3) point at,
+            // so lane r points at key kb + 16 I + 4 (r >> 2) + grp, columns
+            // 16 et + 4 (r & 3) ..: two reads give the eight keys in order.
             uint32_t w[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int u0 = 2 * j, u1 = 2 * j + 1;
-                const uint32_t h0 = vs[(16 * (u0 >> 2) + 4 * (u0 & 3) + grp) * VP + 16 * et + col];
-                const uint32_t h1 = vs[(16 * (u1 >> 2) + 4 * (u1 & 3) + grp) * VP + 16 * et + col];
-                w[j] = h0 | (h1 << 16);
+            for (int I = 0; I < 2; ++I) {
+                const uint16_t *src = vs + (16 * I + 4 * (col >> 2) + grp) * VP + 16 * et + 4 * (col & 3);
+                const s16x4_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)src);
+                w[2 * I] = (uint32_t)(uint16_t)r[0] | ((uint32_t)(uint16_t)r[1] << 16);
+                w[2 * I + 1] = (uint32_t)(uint16_t)r[2] | ((uint32_t)(uint16_t)r[3] << 16);
             }
             const u32x4_t vf = {w[0], w[1], w[2], w[3]};
             oacc[et] *= sc;
@@ -777,7 +793,9 @@ hipError_t launch_pf_rope_kv(const float *qkv, int M, int start, const float2 *r
 }
 
 hipError_t launch_pf_attention(const PfAttnArgs &a, hipStream_t s) {
-    const dim3 grid((a.M + 63) / 64, a.n_heads), block(256);
+    if (a.M < 1 || a.n_heads < 1 || a.n_kv_heads < 1 || a.n_heads % a.n_kv_heads)
+        return hipErrorInvalidValue;
+    const dim3 grid(((a.M + 63) / 64) * a.n_heads), block(256);
     switch (a.head_dim) {
     case 32:
         hipLaunchKernelGGL(k_pf_attn<32>, grid, block, 0, s, a);
