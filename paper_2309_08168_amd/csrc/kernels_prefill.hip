@@ -253,6 +253,7 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 
 constexpr int GW_M = 256;                                        // activation rows per work-group
 constexpr int GW_MIN_TILES = 128;                                // tiles that make a launch "wide"
+constexpr int GW_MIN_SPLIT_GROUPS = 160;                         // work-groups of a wide split reduction
 constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage
 constexpr int GW_PER = GW_BLOCKS / 8;                            // load instructions per wave per stage
 static_assert(GW_BLOCKS % 8 == 0, "blocks per wave");
@@ -266,6 +267,7 @@ __device__ __forceinline__ void load_to_lds16(const uint16_t *g, uint16_t *l) {
                                      (__attribute__((address_space(3))) void *)l, 16, 0, 0);
 }
 
+template <int EPI>
 __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
     constexpr int T = X_TERMS, NWN = 2, NWM = 4;
     constexpr int WN = GB_N / NWN, WM = GW_M / NWM;   // 128 x 64 per wave
@@ -274,18 +276,22 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * GW_BLOCKS * 512];
 
     const int M = a.M, N = a.N, K = a.K;
-    // tile order as in k_pf_gemm: each XCD a contiguous range, walked in
-    // groups of up to 4 row tiles
-    const int TM = (M + GW_M - 1) / GW_M, TN = (N + GB_N - 1) / GB_N, TT = TM * TN;
+    // tile and k-split order as in k_pf_gemm: each XCD a contiguous range,
+    // walked in groups of up to 4 row tiles
+    const int TM = (M + GW_M - 1) / GW_M, TN = (N + GB_N - 1) / GB_N, TT = TM * TN * a.splits;
     const int per = (TT + 7) / 8;
-    const int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+    int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
     if (L >= TT)
         return;  // uniform over the work-group
+    const int split = L % a.splits;
+    L /= a.splits;
     const int GM = TM < 4 ? TM : 4;
     const int grp_i = L / (GM * TN), first = grp_i * GM, gm = min(TM - first, GM);
     const int in = L - grp_i * GM * TN;
     const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * GB_N;
-    const int S = K / GB_K;
+    // the split's stages (possibly none: its partial tile is then zeros)
+    const int S_all = K / GB_K, S_per = (S_all + a.splits - 1) / a.splits;
+    const int s_begin = split * S_per, S = max(0, min(S_all - s_begin, S_per));
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int wn = wave % NWN, wm = wave / NWN;
@@ -308,7 +314,7 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
         uint16_t *dst = lds + (stage & 1) * GW_BLOCKS * 512;
 #pragma unroll
         for (int i = 0; i < GW_PER; ++i)
-            load_to_lds16(src[i] + stage * GB_K, dst + (wave + 8 * i) * 512);
+            load_to_lds16(src[i] + (s_begin + stage) * GB_K, dst + (wave + 8 * i) * 512);
     };
 
     f32x4_t acc[NT][MT];
@@ -348,8 +354,10 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
     }
 
     // lane holds C^T[n0 + wn WN + 16 i + 4 grp + v][m0 + wm WM + 16 j + col]
+    // (EPI_PARTIAL: of the split's partial sum, part[split][m][n])
+    static_assert(EPI == EPI_STORE || EPI == EPI_PARTIAL, "stores only");
     const int col = lane & 15, grp = lane >> 4;
-    float *C = a.C;
+    float *C = EPI == EPI_PARTIAL ? a.part + (int64_t)split * M * a.ldc : a.C;
     const bool vec = (a.ldc & 3) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
@@ -734,7 +742,9 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     // QKV 653 -> 599, gate/up 2640 -> 2603).
     const int wide_tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GW_M - 1) / GW_M);
     if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
-        hipLaunchKernelGGL(k_pf_gemm_wide, dim3(8 * ((wide_tiles + 7) / 8)), dim3(G_THREADS), 0, s, a);
+        PfGemmArgs b = a;
+        b.splits = 1;
+        hipLaunchKernelGGL(k_pf_gemm_wide<EPI_STORE>, dim3(8 * ((wide_tiles + 7) / 8)), dim3(G_THREADS), 0, s, b);
         return hipGetLastError();
     }
     // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
@@ -757,16 +767,32 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     // to 512 (13B output and down projections: 160 tiles, 3 splits; at
     // least 16 stages per split).  Other narrow layers run unsplit.
     int splits = 1;
+    bool wide_split = false;
     if (epi == EPI_RESID && a.part) {
         splits = std::min(PF_MAX_SPLITS, 512 / tiles);
         while (splits > 1 && a.K < splits * GB_K * 16)
             --splits;
+        // The same split on 256 x 256 tiles (one work-group per CU) when it
+        // keeps at least 160 CUs busy: 1023 rows, 13B O 185 -> 168 us, down
+        // 462 -> 436; 511 rows, 70B O 221 -> 197, down 775 -> 684.  At the
+        // 7B shape (511 rows, 128 work-groups) the 256 x 128 tiles stay
+        // faster (O 76 against 86 us).
+        int ws = std::min(PF_MAX_SPLITS, 256 / std::max(wide_tiles, 1));
+        while (ws > 1 && a.K < ws * GB_K * 16)
+            --ws;
+        if (a.K % GB_K == 0 && ws > 1 && wide_tiles * ws >= GW_MIN_SPLIT_GROUPS) {
+            splits = ws;
+            wide_split = true;
+        }
     }
     PfGemmArgs b = a;
     b.splits = splits;
     const dim3 grid(8 * ((tiles * b.splits + 7) / 8)), block(G_THREADS);
     if (splits > 1) {
-        hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
+        if (wide_split)
+            hipLaunchKernelGGL(k_pf_gemm_wide<EPI_PARTIAL>, dim3(8 * ((wide_tiles * splits + 7) / 8)), block, 0, s, b);
+        else
+            hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

@@ -47,7 +47,11 @@ WIDE2_BF16 = S.ModelConfig("wide2_bf16", 2, 1024, 8, 8, 128, 2048, 512, "bf16")
 FFN_WIDE_BF16 = S.ModelConfig("ffn_wide_bf16", 1, 256, 4, 4, 64, 7200, 512, "bf16")
 MODELS = {"mini_bf16": U.MINI_BF16, "odd_bf16": ODD_BF16, "gqa8_dh128": A.CONFIGS["gqa8_dh128"],
           "wide_bf16": WIDE_BF16}
-EXTRA = {"ffn_wide_bf16": FFN_WIDE_BF16, "wide2_bf16": WIDE2_BF16}
+# output and down projections of 10 column tiles of 256: at 1000 rows (4 row
+# tiles) they split their reduction 4 ways on the 256 x 256 kernel (160
+# work-groups)
+D2560_BF16 = S.ModelConfig("d2560_bf16", 1, 2560, 20, 20, 128, 2048, 512, "bf16")
+EXTRA = {"ffn_wide_bf16": FFN_WIDE_BF16, "wide2_bf16": WIDE2_BF16, "d2560_bf16": D2560_BF16}
 _models = {}
 
 
@@ -127,6 +131,18 @@ def test_split_partials_fold_into_the_next_norm(mask):
     got = _logits(dm, toks, dm.cache(300), skip=z)
     r = U.check_logits(cfg, got, ref, f"wide2_bf16 mask {mask} 300 rows")
     print(f"wide2_bf16 mask {mask}: max |d| / tol {r:.3f}")
+
+
+def test_split_reduction_on_the_wide_gemm():
+    """The output and down projections of a d 2560 model over 1000 rows: 40
+    tiles of 256 x 256, each reduction split 4 ways, the partials folded
+    into the MLP norm and the final norm."""
+    cfg, w, om, dm = _pair("d2560_bf16")
+    toks = S.prompt(cfg, 1000, seed=41)
+    ref = om.score(toks)["logits"]
+    got = _logits(dm, toks, dm.cache(1000))
+    r = U.check_logits(cfg, got, ref, "d2560_bf16 1000 rows")
+    print(f"d2560_bf16 1000 rows: max |d| / tol {r:.3f}")
 
 
 def test_generate_after_a_split_prefill():
