@@ -241,9 +241,8 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 //
 // The same product and accumulation order as k_pf_gemm (bit-identical
 // results; plain stores) for layers with at least 128 tiles of 256 x 256:
-// 256 weight rows x 256 activation rows per work-group, 8 waves of
-// 128 x 64 (32 accumulator tiles each, so each fragment read from LDS
-// feeds 4 or 8 MFMAs), 32-k stages.  Operands go from global memory straight into LDS
+// 256 weight rows x 256 activation rows per work-group, 16 waves of 64 x 64
+// (four per SIMD; eight waves of 128 x 64 were 1-4% slower), 32-k stages.  Operands go from global memory straight into LDS
 // with global_load_lds_dwordx4: one instruction fills one 1 KB fragment
 // block (lane l's 16 bytes at 16 l), so no registers stage them and no
 // second pass writes LDS.  Two 64 KB stage buffers: the loads of stage
@@ -252,11 +251,13 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 // for the next stage's loads.  K must be a multiple of 32.
 
 constexpr int GW_M = 256;                                        // activation rows per work-group
+constexpr int GW_WAVES = 16;                                     // 4 x 4 waves of 64 x 64
+constexpr int GW_THREADS = 64 * GW_WAVES;
 constexpr int GW_MIN_TILES = 128;                                // tiles that make a launch "wide"
 constexpr int GW_MIN_SPLIT_GROUPS = 160;                         // work-groups of a wide split reduction
 constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage
-constexpr int GW_PER = GW_BLOCKS / 8;                            // load instructions per wave per stage
-static_assert(GW_BLOCKS % 8 == 0, "blocks per wave");
+constexpr int GW_PER = GW_BLOCKS / GW_WAVES;                     // load instructions per wave per stage
+static_assert(GW_BLOCKS % GW_WAVES == 0, "blocks per wave");
 
 // s_waitcnt immediate (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4,
 // lgkmcnt 11:8) that waits for vmcnt 0 and leaves the other counters alone
@@ -268,9 +269,9 @@ __device__ __forceinline__ void load_to_lds16(const uint16_t *g, uint16_t *l) {
 }
 
 template <int EPI>
-__global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
-    constexpr int T = X_TERMS, NWN = 2, NWM = 4;
-    constexpr int WN = GB_N / NWN, WM = GW_M / NWM;   // 128 x 64 per wave
+__global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
+    constexpr int T = X_TERMS, NWN = 4, NWM = 4;
+    constexpr int WN = GB_N / NWN, WM = GW_M / NWM;   // 64 x 64 per wave
     constexpr int NT = WN / 16, MT = WM / 16;
     constexpr int NBW = GB_N / 16;                     // weight blocks per stage
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * GW_BLOCKS * 512];
@@ -302,7 +303,7 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
     const uint16_t *src[GW_PER];
 #pragma unroll
     for (int i = 0; i < GW_PER; ++i) {
-        const int b = wave + 8 * i;
+        const int b = wave + GW_WAVES * i;
         if (b < NBW) {
             src[i] = a.W + (int64_t)min(n0 + 16 * b + (lane & 15), N - 1) * K + 8 * (lane >> 4);
         } else {
@@ -314,7 +315,7 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm_wide(PfGemmArgs a) {
         uint16_t *dst = lds + (stage & 1) * GW_BLOCKS * 512;
 #pragma unroll
         for (int i = 0; i < GW_PER; ++i)
-            load_to_lds16(src[i] + (s_begin + stage) * GB_K, dst + (wave + 8 * i) * 512);
+            load_to_lds16(src[i] + (s_begin + stage) * GB_K, dst + (wave + GW_WAVES * i) * 512);
     };
 
     f32x4_t acc[NT][MT];
@@ -752,7 +753,7 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
         PfGemmArgs b = a;
         b.splits = 1;
-        hipLaunchKernelGGL(k_pf_gemm_wide<EPI_STORE>, dim3(8 * ((wide_tiles + 7) / 8)), dim3(G_THREADS), 0, s, b);
+        hipLaunchKernelGGL(k_pf_gemm_wide<EPI_STORE>, dim3(8 * ((wide_tiles + 7) / 8)), dim3(GW_THREADS), 0, s, b);
         return hipGetLastError();
     }
     // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
@@ -798,7 +799,8 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     const dim3 grid(8 * ((tiles * b.splits + 7) / 8)), block(G_THREADS);
     if (splits > 1) {
         if (wide_split)
-            hipLaunchKernelGGL(k_pf_gemm_wide<EPI_PARTIAL>, dim3(8 * ((wide_tiles * splits + 7) / 8)), block, 0, s, b);
+            hipLaunchKernelGGL(k_pf_gemm_wide<EPI_PARTIAL>, dim3(8 * ((wide_tiles * splits + 7) / 8)), dim3(GW_THREADS),
+                               0, s, b);
         else
             hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
         const hipError_t e = hipGetLastError();
