@@ -745,10 +745,12 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
     // Wide layers (at least 128 tiles of 256 x 256) take the direct-to-LDS
     // kernel.  Both kernels fill the same fraction of the last round (one
-    // 256 x 256 work-group per CU against two of 256 x 128), so the wide one
-    // wins wherever half the CUs have a tile (1023 rows: 13B QKV 509 -> 456
-    // us, gate/up 959 -> 881; 7B QKV 368 -> 335, gate/up 646 -> 661; 70B
-    // QKV 653 -> 599, gate/up 2640 -> 2603).
+    // 256 x 256 work-group per CU against two of 256 x 128); measured with
+    // the 256 x 128 kernel's time first (us): 1023 rows, 13B QKV 509 -> 448,
+    // gate/up 959 -> 857, 7B QKV 368 -> 335, 70B QKV 653 -> 599; 511 rows,
+    // 7B gate/up 353 -> 311, 70B gate/up 1426 -> 1307.  With fewer tiles
+    // (the QKV layers at 511 rows: 80-120 tiles) the 256 x 128 kernel stays
+    // faster (13B 334 against 354).
     const int wide_tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GW_M - 1) / GW_M);
     if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
         PfGemmArgs b = a;
