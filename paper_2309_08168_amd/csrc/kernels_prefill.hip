@@ -663,26 +663,40 @@ __global__ __launch_bounds__(256) void k_pf_rope_kv(const float *qkv, int start,
     const int m = blockIdx.x, pos = start + m, half = dh >> 1;
     const int nq = (H + 2 * KVH) * dh;
     const float *x = qkv + (int64_t)m * nq;
-    for (int idx = threadIdx.x; idx < (H + 2 * KVH) * half; idx += 256) {
+    // four pair indices i .. i + 3 of one head per step (half is a multiple
+    // of 4): 16-byte loads and stores, 8-byte stores into the cache
+    for (int idx = 4 * threadIdx.x; idx < (H + 2 * KVH) * half; idx += 4 * 256) {
         const int head = idx / half, i = idx - head * half;
-        float y0 = x[head * dh + i], y1 = x[head * dh + i + half];
+        f32x4_t y0 = *reinterpret_cast<const f32x4_t *>(x + head * dh + i);
+        f32x4_t y1 = *reinterpret_cast<const f32x4_t *>(x + head * dh + i + half);
         if (head < H + KVH) {
-            const float2 cs = rope[(int64_t)pos * half + i];
-            const float r0 = y0 * cs.x - y1 * cs.y;
-            const float r1 = y1 * cs.x + y0 * cs.y;
-            y0 = r0;
-            y1 = r1;
+            const f32x4_t c01 = *reinterpret_cast<const f32x4_t *>(rope + (int64_t)pos * half + i);
+            const f32x4_t c23 = *reinterpret_cast<const f32x4_t *>(rope + (int64_t)pos * half + i + 2);
+            const float cx[4] = {c01[0], c01[2], c23[0], c23[2]}, cy[4] = {c01[1], c01[3], c23[1], c23[3]};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float r0 = y0[j] * cx[j] - y1[j] * cy[j];
+                const float r1 = y1[j] * cx[j] + y0[j] * cy[j];
+                y0[j] = r0;
+                y1[j] = r1;
+            }
         }
         if (head < H) {
             float *qo = q + (int64_t)m * H * dh + head * dh + i;
-            qo[0] = y0;
-            qo[half] = y1;
+            *reinterpret_cast<f32x4_t *>(qo) = y0;
+            *reinterpret_cast<f32x4_t *>(qo + half) = y1;
         } else {
             const bool is_k = head < H + KVH;
             const int g = is_k ? head - H : head - H - KVH;
             uint16_t *c = (is_k ? kc : vc) + (int64_t)g * stride + (int64_t)pos * dh + i;
-            c[0] = bf16_rne_bits(y0);
-            c[half] = bf16_rne_bits(y1);
+            u32x2_t w0, w1;
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                w0[j] = (uint32_t)bf16_rne_bits(y0[2 * j]) | ((uint32_t)bf16_rne_bits(y0[2 * j + 1]) << 16);
+                w1[j] = (uint32_t)bf16_rne_bits(y1[2 * j]) | ((uint32_t)bf16_rne_bits(y1[2 * j + 1]) << 16);
+            }
+            *reinterpret_cast<u32x2_t *>(c) = w0;
+            *reinterpret_cast<u32x2_t *>(c + half) = w1;
         }
     }
 }
@@ -825,6 +839,8 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
 
 hipError_t launch_pf_rope_kv(const float *qkv, int M, int start, const float2 *rope, int H, int KVH, int dh,
                              float *q, uint16_t *kcache, uint16_t *vcache, int64_t kv_head_stride, hipStream_t s) {
+    if (dh % 8 || kv_head_stride % 4)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_pf_rope_kv, dim3(M), dim3(256), 0, s, qkv, start, rope, H, KVH, dh, q, kcache, vcache,
                        kv_head_stride);
     return hipGetLastError();
