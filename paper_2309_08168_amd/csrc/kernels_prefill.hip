@@ -255,7 +255,7 @@ constexpr int GW_WAVES = 16;                                     // 4 x 4 waves 
 constexpr int GW_THREADS = 64 * GW_WAVES;
 constexpr int GW_MIN_TILES = 128;                                // tiles that make a launch "wide"
 constexpr int GW_MIN_SPLIT_GROUPS = 160;                         // work-groups of a wide split reduction
-constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage
+constexpr int GW_BLOCKS = GB_N / 16 + X_TERMS * GW_M / 16;       // 1 KB fragment blocks per stage (at most)
 constexpr int GW_PER = GW_BLOCKS / GW_WAVES;                     // load instructions per wave per stage
 static_assert(GW_BLOCKS % GW_WAVES == 0, "blocks per wave");
 
@@ -268,18 +268,24 @@ __device__ __forceinline__ void load_to_lds16(const uint16_t *g, uint16_t *l) {
                                      (__attribute__((address_space(3))) void *)l, 16, 0, 0);
 }
 
-template <int EPI>
+// BN: weight rows per tile, 256 (4 x 4 waves of 64 x 64) or 224 (2 x 8
+// waves of 112 x 32, 14 weight blocks per stage, the last two load slots of
+// a stage idle).
+template <int EPI, int BN>
 __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
-    constexpr int T = X_TERMS, NWN = 4, NWM = 4;
-    constexpr int WN = GB_N / NWN, WM = GW_M / NWM;   // 64 x 64 per wave
+    static_assert(BN == 256 || BN == 224, "tile width");
+    constexpr int T = X_TERMS, NWN = BN == 256 ? 4 : 2, NWM = GW_WAVES / NWN;
+    constexpr int WN = BN / NWN, WM = GW_M / NWM;
     constexpr int NT = WN / 16, MT = WM / 16;
-    constexpr int NBW = GB_N / 16;                     // weight blocks per stage
+    constexpr int NBW = BN / 16;                       // weight blocks per stage
+    constexpr int NB = NBW + X_TERMS * GW_M / 16;      // blocks per stage
+    static_assert(NB <= GW_BLOCKS && NT * 16 == WN && MT * 16 == WM, "tile split");
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * GW_BLOCKS * 512];
 
     const int M = a.M, N = a.N, K = a.K;
     // tile and k-split order as in k_pf_gemm: each XCD a contiguous range,
     // walked in groups of up to 4 row tiles
-    const int TM = (M + GW_M - 1) / GW_M, TN = (N + GB_N - 1) / GB_N, TT = TM * TN * a.splits;
+    const int TM = (M + GW_M - 1) / GW_M, TN = (N + BN - 1) / BN, TT = TM * TN * a.splits;
     const int per = (TT + 7) / 8;
     int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
     if (L >= TT)
@@ -289,7 +295,7 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     const int GM = TM < 4 ? TM : 4;
     const int grp_i = L / (GM * TN), first = grp_i * GM, gm = min(TM - first, GM);
     const int in = L - grp_i * GM * TN;
-    const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * GB_N;
+    const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * BN;
     // the split's stages (possibly none: its partial tile is then zeros)
     const int S_all = K / GB_K, S_per = (S_all + a.splits - 1) / a.splits;
     const int s_begin = split * S_per, S = max(0, min(S_all - s_begin, S_per));
@@ -303,7 +309,7 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     const uint16_t *src[GW_PER];
 #pragma unroll
     for (int i = 0; i < GW_PER; ++i) {
-        const int b = wave + GW_WAVES * i;
+        const int b = min(wave + GW_WAVES * i, NB - 1);  // slots past NB load nothing (below)
         if (b < NBW) {
             src[i] = a.W + (int64_t)min(n0 + 16 * b + (lane & 15), N - 1) * K + 8 * (lane >> 4);
         } else {
@@ -315,7 +321,8 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
         uint16_t *dst = lds + (stage & 1) * GW_BLOCKS * 512;
 #pragma unroll
         for (int i = 0; i < GW_PER; ++i)
-            load_to_lds16(src[i] + (s_begin + stage) * GB_K, dst + (wave + GW_WAVES * i) * 512);
+            if (NB % GW_WAVES == 0 || wave + GW_WAVES * i < NB)  // uniform over the wave
+                load_to_lds16(src[i] + (s_begin + stage) * GB_K, dst + (wave + GW_WAVES * i) * 512);
     };
 
     f32x4_t acc[NT][MT];
@@ -769,7 +776,16 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     if (wide_tiles >= GW_MIN_TILES && a.K % GB_K == 0 && epi == EPI_STORE) {
         PfGemmArgs b = a;
         b.splits = 1;
-        hipLaunchKernelGGL(k_pf_gemm_wide<EPI_STORE>, dim3(8 * ((wide_tiles + 7) / 8)), dim3(GW_THREADS), 0, s, b);
+        // Tiles 224 wide when that takes fewer tile-widths of rounds on 256
+        // CUs: a round lasts about as long as a tile is wide, and 13B gate/up
+        // (1023 rows) is 432 tiles of 256 (1.7 rounds) or 496 of 224 (1.9).
+        const int tiles224 = ((a.N + 223) / 224) * ((a.M + GW_M - 1) / GW_M);
+        const int64_t cost256 = (int64_t)((wide_tiles + 255) / 256) * 256;
+        const int64_t cost224 = (int64_t)((tiles224 + 255) / 256) * 224;
+        if (cost224 < cost256)
+            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 224>), dim3(8 * ((tiles224 + 7) / 8)), dim3(GW_THREADS), 0, s, b);
+        else
+            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 256>), dim3(8 * ((wide_tiles + 7) / 8)), dim3(GW_THREADS), 0, s, b);
         return hipGetLastError();
     }
     // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
@@ -815,8 +831,8 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
     const dim3 grid(8 * ((tiles * b.splits + 7) / 8)), block(G_THREADS);
     if (splits > 1) {
         if (wide_split)
-            hipLaunchKernelGGL(k_pf_gemm_wide<EPI_PARTIAL>, dim3(8 * ((wide_tiles * splits + 7) / 8)), dim3(GW_THREADS),
-                               0, s, b);
+            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_PARTIAL, 256>), dim3(8 * ((wide_tiles * splits + 7) / 8)),
+                               dim3(GW_THREADS), 0, s, b);
         else
             hipLaunchKernelGGL((k_pf_gemm<EPI_PARTIAL, 4, 2, 1>), grid, block, 0, s, b);
         const hipError_t e = hipGetLastError();
