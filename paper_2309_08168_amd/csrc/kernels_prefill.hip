@@ -241,17 +241,18 @@ __global__ __launch_bounds__(G_THREADS, 2) void k_pf_gemm(PfGemmArgs a) {
 //
 // The same product and accumulation order as k_pf_gemm (bit-identical
 // results; plain stores) for layers with at least 128 tiles of 256 x 256:
-// 256 weight rows x 256 activation rows per work-group, 16 waves of 64 x 64
-// (four per SIMD; eight waves of 128 x 64 were 1-4% slower), 32-k stages.  Operands go from global memory straight into LDS
-// with global_load_lds_dwordx4: one instruction fills one 1 KB fragment
-// block (lane l's 16 bytes at 16 l), so no registers stage them and no
-// second pass writes LDS.  Two 64 KB stage buffers: the loads of stage
-// s + 1 are issued right after the barrier that ends stage s - 1.  The
-// barrier is a bare s_barrier: a release fence before it would also wait
-// for the next stage's loads.  K must be a multiple of 32.
+// 256 activation rows x 256 (or 224) weight rows per work-group as 16 waves
+// (four per SIMD; eight waves of 128 x 64 were 1-4% slower), 32-k stages.
+// Operands go from global memory straight into LDS with
+// global_load_lds_dwordx4: one instruction fills one 1 KB fragment block
+// (lane l's 16 bytes at 16 l), so no registers stage them and no second
+// pass writes LDS.  Two 64 KB stage buffers: the loads of stage s + 1 are
+// issued right after the barrier that ends stage s - 1.  The barrier is a
+// bare s_barrier: a release fence before it would also wait for the next
+// stage's loads.  K must be a multiple of 32.
 
 constexpr int GW_M = 256;                                        // activation rows per work-group
-constexpr int GW_WAVES = 16;                                     // 4 x 4 waves of 64 x 64
+constexpr int GW_WAVES = 16;                                     // waves per work-group
 constexpr int GW_THREADS = 64 * GW_WAVES;
 constexpr int GW_MIN_TILES = 128;                                // tiles that make a launch "wide"
 constexpr int GW_MIN_SPLIT_GROUPS = 160;                         // work-groups of a wide split reduction
@@ -783,9 +784,11 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
         const int64_t cost256 = (int64_t)((wide_tiles + 255) / 256) * 256;
         const int64_t cost224 = (int64_t)((tiles224 + 255) / 256) * 224;
         if (cost224 < cost256)
-            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 224>), dim3(8 * ((tiles224 + 7) / 8)), dim3(GW_THREADS), 0, s, b);
+            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 224>), dim3(8 * ((tiles224 + 7) / 8)), dim3(GW_THREADS), 0, s,
+                               b);
         else
-            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 256>), dim3(8 * ((wide_tiles + 7) / 8)), dim3(GW_THREADS), 0, s, b);
+            hipLaunchKernelGGL((k_pf_gemm_wide<EPI_STORE, 256>), dim3(8 * ((wide_tiles + 7) / 8)), dim3(GW_THREADS), 0,
+                               s, b);
         return hipGetLastError();
     }
     // wide layers (at least one tile per CU): 4 x 2 waves, one stage in
