@@ -8,13 +8,17 @@
 //     stages of 32 k staged through double-buffered LDS in MFMA fragment
 //     order, v_mfma 16x16x32 bf16; tiles are ordered so the work-groups one
 //     XCD runs together share their weight and activation slices in that
-//     XCD's L2; layers with fewer tiles than CUs split the reduction in two;
+//     XCD's L2; narrow residual updates split the reduction into partials;
+//   - k_pf_gemm_wide: the same product on 256 x 256 (or 256 x 224) tiles
+//     with the operands loaded straight into LDS, for the layers with
+//     enough tiles to fill the CUs, and for split residual updates that do;
 //   - k_pf_attn: causal attention, one wave per 16 query rows of a head,
 //     scores and the weighted sum of values on matrix cores with an online
 //     softmax over 32-key blocks, the longest row blocks dispatched first and
 //     spread evenly over the XCDs;
-//   - small row kernels between them: embedding, RMSNorm + split, rotary
-//     embedding + KV append, SwiGLU + split.
+//   - small row kernels between them: embedding, RMSNorm + split (adding a
+//     split residual update's partials first), rotary embedding + KV
+//     append, SwiGLU + split.
 #include "sd_internal.h"
 
 #include <algorithm>
