@@ -275,7 +275,10 @@ __device__ __forceinline__ void load_to_lds16(const uint16_t *g, uint16_t *l) {
 
 // BN: weight rows per tile, 256 (4 x 4 waves of 64 x 64) or 224 (2 x 8
 // waves of 112 x 32, 14 weight blocks per stage, the last two load slots of
-// a stage idle).
+// a stage idle).  EPI_SWIGLU (W = [gate; up], N = 2 F): a tile takes the
+// gate and the up rows of the same BN / 2 columns f of the MLP, the waves
+// holding up pass their sums to the waves holding gate through LDS, and
+// those write silu(gate) * up as terms.
 template <int EPI, int BN>
 __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     static_assert(BN == 256 || BN == 224, "tile width");
@@ -287,10 +290,13 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     static_assert(NB <= GW_BLOCKS && NT * 16 == WN && MT * 16 == WM, "tile split");
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * GW_BLOCKS * 512];
 
-    const int M = a.M, N = a.N, K = a.K;
+    constexpr bool SWI = EPI == EPI_SWIGLU;
+    constexpr int BC = SWI ? BN / 2 : BN;              // output columns per tile
+    const int M = a.M, N = a.N, K = a.K, F = N / 2;
+    const int NC = SWI ? F : N;                        // output columns
     // tile and k-split order as in k_pf_gemm: each XCD a contiguous range,
     // walked in groups of up to 4 row tiles
-    const int TM = (M + GW_M - 1) / GW_M, TN = (N + BN - 1) / BN, TT = TM * TN * a.splits;
+    const int TM = (M + GW_M - 1) / GW_M, TN = (NC + BC - 1) / BC, TT = TM * TN * a.splits;
     const int per = (TT + 7) / 8;
     int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
     if (L >= TT)
@@ -300,7 +306,7 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     const int GM = TM < 4 ? TM : 4;
     const int grp_i = L / (GM * TN), first = grp_i * GM, gm = min(TM - first, GM);
     const int in = L - grp_i * GM * TN;
-    const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * BN;
+    const int m0 = (first + in % gm) * GW_M, n0 = (in / gm) * BC;  // SWI: n0 is the first f
     // the split's stages (possibly none: its partial tile is then zeros)
     const int S_all = K / GB_K, S_per = (S_all + a.splits - 1) / a.splits;
     const int s_begin = split * S_per, S = max(0, min(S_all - s_begin, S_per));
@@ -316,7 +322,12 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
     for (int i = 0; i < GW_PER; ++i) {
         const int b = min(wave + GW_WAVES * i, NB - 1);  // slots past NB load nothing (below)
         if (b < NBW) {
-            src[i] = a.W + (int64_t)min(n0 + 16 * b + (lane & 15), N - 1) * K + 8 * (lane >> 4);
+            int row;
+            if constexpr (SWI)  // gate rows f, then up rows F + f
+                row = (b < NBW / 2 ? 0 : F) + min(n0 + 16 * (b % (NBW / 2)) + (lane & 15), F - 1);
+            else
+                row = min(n0 + 16 * b + (lane & 15), N - 1);
+            src[i] = a.W + (int64_t)row * K + 8 * (lane >> 4);
         } else {
             const int c = b - NBW, t = c / (GW_M / 16), rg = c % (GW_M / 16);
             src[i] = a.A + t * a.a_term + (int64_t)min(m0 + 16 * rg + (lane & 15), M - 1) * a.lda + 8 * (lane >> 4);
@@ -368,8 +379,64 @@ __global__ __launch_bounds__(GW_THREADS, 4) void k_pf_gemm_wide(PfGemmArgs a) {
 
     // lane holds C^T[n0 + wn WN + 16 i + 4 grp + v][m0 + wm WM + 16 j + col]
     // (EPI_PARTIAL: of the split's partial sum, part[split][m][n])
-    static_assert(EPI == EPI_STORE || EPI == EPI_PARTIAL, "stores only");
+    static_assert(EPI == EPI_STORE || EPI == EPI_PARTIAL || EPI == EPI_SWIGLU, "stores only");
     const int col = lane & 15, grp = lane >> 4;
+    if constexpr (SWI) {
+        // wave column wn < NWN / 2 holds gate, wn + NWN / 2 up of the same f
+        constexpr int HALF = NWN / 2, SLOT = NT * MT * 64;  // f32x4 per up wave
+        static_assert(NWM * HALF * SLOT * 16 <= (int)sizeof(lds), "exchange fits the stage buffers");
+        f32x4_t *xl = reinterpret_cast<f32x4_t *>(lds);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // all reads of the stages done
+        if (wn >= HALF) {
+#pragma unroll
+            for (int i = 0; i < NT; ++i)
+#pragma unroll
+                for (int j = 0; j < MT; ++j)
+                    xl[(wm * HALF + wn - HALF) * SLOT + (i * MT + j) * 64 + lane] = acc[i][j];
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (wn >= HALF)
+            return;
+        const bool vec = (F & 3) == 0 && (a.x_term & 3) == 0 && (reinterpret_cast<uintptr_t>(a.xout) & 7) == 0;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int f = n0 + wn * WN + 16 * i + 4 * grp;
+#pragma unroll
+            for (int j = 0; j < MT; ++j) {
+                const int m = m0 + wm * WM + 16 * j + col;
+                const f32x4_t up = xl[(wm * HALF + wn) * SLOT + (i * MT + j) * 64 + lane];
+                if (m >= M || f >= F)
+                    continue;
+                uint16_t t4[T][4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float g = acc[i][j][v];
+                    uint16_t t3[T];
+                    split3(g / (1.0f + expf(-g)) * up[v], t3);
+#pragma unroll
+                    for (int q = 0; q < T; ++q)
+                        t4[q][v] = t3[q];
+                }
+                uint16_t *o = a.xout + (int64_t)m * F + f;
+                if (vec && f + 3 < F) {
+#pragma unroll
+                    for (int q = 0; q < T; ++q) {
+                        const u32x2_t w = {(uint32_t)t4[q][0] | ((uint32_t)t4[q][1] << 16),
+                                           (uint32_t)t4[q][2] | ((uint32_t)t4[q][3] << 16)};
+                        *reinterpret_cast<u32x2_t *>(o + q * a.x_term) = w;
+                    }
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (f + v < F)
+#pragma unroll
+                            for (int q = 0; q < T; ++q)
+                                o[q * a.x_term + v] = t4[q][v];
+                }
+            }
+        }
+        return;
+    }
     float *C = EPI == EPI_PARTIAL ? a.part + (int64_t)split * M * a.ldc : a.C;
     const bool vec = (a.ldc & 3) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
 #pragma unroll
@@ -768,6 +835,32 @@ hipError_t launch_pf_gemm(const PfGemmArgs &a, int epi, hipStream_t s, int *fold
         *fold = 0;
     if (a.M < 1 || a.N < 1 || a.K < 8 || a.K % 8 || a.lda % 8 || a.M > PF_ROWS)
         return hipErrorInvalidValue;
+    if (epi == EPI_SWIGLU) {
+        // gate/up: the SwiGLU in the wide kernel's epilogue when the launch
+        // is wide (xout must not overlap A: other work-groups still read
+        // it), else the product into C and a separate SwiGLU kernel.  Same
+        // box, 13B prefill: 72.9 -> 72.4 ms.
+        const int F = a.N / 2;
+        if (a.N % 2 || F % 8 || !a.xout)
+            return hipErrorInvalidValue;
+        const int TMw = (a.M + GW_M - 1) / GW_M;
+        const int t256 = TMw * ((F + 127) / 128), t224 = TMw * ((F + 111) / 112);
+        if (t256 >= GW_MIN_TILES && a.K % GB_K == 0) {
+            PfGemmArgs b = a;
+            b.splits = 1;
+            if ((int64_t)((t224 + 255) / 256) * 224 < (int64_t)((t256 + 255) / 256) * 256)
+                hipLaunchKernelGGL((k_pf_gemm_wide<EPI_SWIGLU, 224>), dim3(8 * ((t224 + 7) / 8)), dim3(GW_THREADS), 0, s,
+                                   b);
+            else
+                hipLaunchKernelGGL((k_pf_gemm_wide<EPI_SWIGLU, 256>), dim3(8 * ((t256 + 7) / 8)), dim3(GW_THREADS), 0, s,
+                                   b);
+            return hipGetLastError();
+        }
+        const hipError_t e = launch_pf_gemm(a, EPI_STORE, s);
+        if (e != hipSuccess)
+            return e;
+        return launch_pf_swiglu_split(a.C, F, a.M, a.xout, a.x_term, s);
+    }
     const int tiles = ((a.N + GB_N - 1) / GB_N) * ((a.M + GB_M - 1) / GB_M);
     // Wide layers (at least 128 tiles of 256 x 256) take the direct-to-LDS
     // kernel.  Both kernels fill the same fraction of the last round (one

@@ -133,8 +133,10 @@ struct sd_model {
     // rotated queries, and the GEMM inputs as X_TERMS terms, PF_ROWS rows each
     bool pf_ok = false;
     float *pf_h = nullptr, *pf_c = nullptr, *pf_q = nullptr, *pf_part = nullptr;
-    uint16_t *pf_x = nullptr;
+    uint16_t *pf_x = nullptr;  // terms of the GEMM inputs: normed rows, attention output
     int64_t pf_term = 0;
+    uint16_t *pf_y = nullptr;  // terms of the MLP activation: the gate/up GEMM's output, the down GEMM's input
+    int64_t pf_y_term = 0;
     DevState *st = nullptr;
     Mailbox *mb_host = nullptr;
     Mailbox *mb_dev = nullptr;
@@ -741,11 +743,11 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
     // A split residual update leaves its partials in pf_part; the next norm
     // adds them into the residual stream (fold = their count, 0: none).
     int fold = 0;
-    auto gemm = [&](const void *W, int N, int K, float *C, int64_t ldc, int epi) {
+    auto gemm = [&](const void *W, int N, int K, float *C, int64_t ldc, int epi, const uint16_t *A, int64_t a_term) {
         PfGemmArgs g{};
         g.W = static_cast<const uint16_t *>(W);
-        g.A = m->pf_x;
-        g.a_term = xt;
+        g.A = A;
+        g.a_term = a_term;
         g.C = C;
         g.ldc = ldc;
         g.M = M;
@@ -753,6 +755,10 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
         g.K = K;
         g.lda = K;
         g.part = epi == EPI_RESID ? m->pf_part : nullptr;  // [PF_MAX_SPLITS][M][d]: split reductions
+        // EPI_SWIGLU: the MLP activation terms, not into A (other work-groups
+        // still read it)
+        g.xout = m->pf_y;
+        g.x_term = m->pf_y_term;
         return launch(launch_pf_gemm(g, epi, s, epi == EPI_RESID && C == m->pf_h ? &fold : nullptr), "prefill GEMM");
     };
     auto norm = [&](const void *gain) {
@@ -772,7 +778,7 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
             uint16_t *kbase = reinterpret_cast<uint16_t *>(kv) + (size_t)(2 * l) * KVH * head_stride;
             uint16_t *vbase = reinterpret_cast<uint16_t *>(kv) + (size_t)(2 * l + 1) * KVH * head_stride;
             SD_TRY(norm(m->attn_norm[l]));
-            SD_TRY(gemm(m->w_qkv[l], nq, d, m->pf_c, nq, EPI_STORE));
+            SD_TRY(gemm(m->w_qkv[l], nq, d, m->pf_c, nq, EPI_STORE, m->pf_x, xt));
             SD_TRY(launch(launch_pf_rope_kv(m->pf_c, M, start, m->rope, H, KVH, dh, m->pf_q, kbase, vbase,
                                             head_stride, s),
                           "prefill rotary"));
@@ -791,18 +797,17 @@ sd_status enqueue_forward_large(sd_model *m, void *kv, int32_t cap, const uint8_
             at.n_kv_heads = KVH;
             at.head_dim = dh;
             SD_TRY(launch(launch_pf_attention(at, s), "prefill attention"));
-            SD_TRY(gemm(m->w_o[l], d, hd, m->pf_h, d, EPI_RESID));
+            SD_TRY(gemm(m->w_o[l], d, hd, m->pf_h, d, EPI_RESID, m->pf_x, xt));
         }
         if (!(skip && skip[2 * l + 1])) {
             SD_TRY(norm(m->mlp_norm[l]));
-            SD_TRY(gemm(m->w_gate_up[l], 2 * F, d, m->pf_c, 2 * F, EPI_STORE));
-            SD_TRY(launch(launch_pf_swiglu_split(m->pf_c, F, M, m->pf_x, xt, s), "prefill SwiGLU"));
-            SD_TRY(gemm(m->w_down[l], d, F, m->pf_h, d, EPI_RESID));
+            SD_TRY(gemm(m->w_gate_up[l], 2 * F, d, m->pf_c, 2 * F, EPI_SWIGLU, m->pf_x, xt));
+            SD_TRY(gemm(m->w_down[l], d, F, m->pf_h, d, EPI_RESID, m->pf_y, m->pf_y_term));
         }
     }
     if (logits) {
         SD_TRY(norm(m->final_norm));
-        SD_TRY(gemm(m->lm_head, c.vocab, d, logits, c.vocab, EPI_STORE));
+        SD_TRY(gemm(m->lm_head, c.vocab, d, logits, c.vocab, EPI_STORE, m->pf_x, xt));
     } else if (fold) {
         // no norm follows: leave the residual stream whole
         SD_TRY(launch(launch_pf_split_sum(m->pf_part, fold, (int64_t)M * d, m->pf_h, s), "prefill split sum"));
@@ -1400,6 +1405,7 @@ void destroy_model(sd_model *m) {
     dev_free(m->pf_q);
     dev_free(m->pf_part);
     dev_free(m->pf_x);
+    dev_free(m->pf_y);
     dev_free(m->ws.ctl);
     dev_free(m->st);
     dev_free(m->d_tokens);
@@ -1496,6 +1502,8 @@ sd_status create_model(const sd_config *cfg, const sd_weights *w, void *stream, 
         chain(dev_alloc(&m->pf_q, (size_t)PF_ROWS * hd));
         chain(dev_alloc(&m->pf_part, (size_t)PF_MAX_SPLITS * PF_ROWS * c.d_model));
         chain(dev_alloc(&m->pf_x, (size_t)X_TERMS * m->pf_term));
+        m->pf_y_term = (int64_t)PF_ROWS * c.ffn_dim;
+        chain(dev_alloc(&m->pf_y, (size_t)X_TERMS * m->pf_y_term));
     }
     if (st != SD_OK) {
         destroy_model(m);

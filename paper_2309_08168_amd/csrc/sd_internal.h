@@ -274,6 +274,11 @@ struct PfGemmArgs {
     int32_t M, N, K, lda;
     float *part;        // EPI_RESID: [PF_MAX_SPLITS][M][ldc] scratch for a split reduction, or null
     int32_t splits;     // set by the launcher
+    // EPI_SWIGLU (W = [gate; up], N = 2 F): silu(gate) * up as X_TERMS bf16
+    // terms into xout [X_TERMS][.][F] (term stride x_term); C [M][2 F] is
+    // scratch for shapes the fused kernel does not take
+    uint16_t *xout;
+    int64_t x_term;
 };
 
 // Causal attention of M query rows (row m at position start + m) over the
@@ -296,7 +301,8 @@ hipError_t launch_pf_norm_split(const float *h, int K, int M, const uint16_t *ga
 // part[1][m] + ... (splits of them, [splits][M][K], in split order) first.
 hipError_t launch_pf_fold_norm_split(float *h, const float *part, int splits, int K, int M, const uint16_t *gain,
                                      float eps, uint16_t *out, int64_t out_term, hipStream_t s);
-// C = A W^T (EPI_STORE) or C += A W^T (EPI_RESID).  A narrow EPI_RESID may
+// C = A W^T (EPI_STORE), C += A W^T (EPI_RESID), or the SwiGLU of a gate/up
+// product as terms (EPI_SWIGLU, see PfGemmArgs).  A narrow EPI_RESID may
 // split its reduction into a.part; with fold null the partials are added
 // into C before the call returns (on the stream), else *fold receives the
 // number of splits left in a.part for launch_pf_fold_norm_split (0: none).

@@ -92,6 +92,18 @@ def test_forward_on_the_wide_gemm(rows):
     print(f"ffn_wide_bf16 {rows} rows from 0: max |d| / tol {r:.3f}")
 
 
+@pytest.mark.parametrize("rows", [600, 1000])
+def test_wide_gemm_forward_is_deterministic(rows):
+    """Three forwards on the SwiGLU-fused gate/up GEMM (224- and 256-wide
+    tiles) give bit-identical logits: no work-group writes its output where
+    another still reads its input."""
+    cfg, w, om, dm = _pair("ffn_wide_bf16")
+    toks = S.prompt(cfg, rows, seed=rows + 13)
+    first = _logits(dm, toks, dm.cache(rows))
+    for _ in range(2):
+        assert np.array_equal(_logits(dm, toks, dm.cache(rows)), first)
+
+
 @pytest.mark.parametrize("name", ["mini_bf16", "odd_bf16"])
 def test_long_forward_after_prefix(name):
     cfg, w, om, dm = _pair(name)
