@@ -825,8 +825,13 @@ static hipError_t launch_fp8_r(const LinearArgs &a, int epi, int n_tiles, hipStr
 // MFMAs per k-step cover all X_TERMS terms of M rows (one MFMA for up to 5
 // rows, two up to 10, three up to 16).  The host picks NP from its bound on
 // M (LinearArgs::max_rows).
+//
+// The launch bound asks for two waves per SIMD.  With one set of activation
+// registers (below) the four-tile kernel at three packings fits that in 218
+// registers without spilling; double-buffered activations took 260 (one
+// wave per SIMD), and 13B verification at 13-16 rows was 2% slower.
 template <int EPI, int TN, int NW, int NP>
-__global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
+__global__ __launch_bounds__(NW * 64, 2) void k_linear_mfma(LinearArgs a) {
     constexpr int WL = TN * 16 * 128;                // bf16 staging per wave
     constexpr int RC = NP * 16 + 1;                  // reduction row length
     constexpr size_t SMEM_W = (size_t)NW * WL * 2, SMEM_R = (size_t)NW * TN * 16 * RC * 4;
@@ -865,12 +870,14 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
         for (int p = 0; p < NP; ++p)
             acc[j][p] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     u32x4_t wv[TN][4], xv[NP][4];
-    auto load = [&](int q) {
+    auto load_w = [&](int q) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii)
                 wv[j][ii] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(W + woff[j][ii] + (q << 7)));
+    };
+    auto load_x = [&](int q) {
 #pragma unroll
         for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -878,11 +885,16 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
                 xv[p][i] = *reinterpret_cast<const u32x4_t *>(X + ((((int64_t)q * X_PACKS_MAX + p) * 4 + i) << 9));
     };
     int q = ks0 + wave;
-    if (q < ks1)
-        load(q);
+    if (q < ks1) {
+        load_w(q);
+        load_x(q);
+    }
     for (; q < ks1; q += NW) {
-        // this k-step's weights into the staging tile; its activations stay
-        // in registers while the next k-step's loads go out
+        // this k-step's weights into the staging tile, then the next k-step's
+        // weight loads go out.  Its activations (cache hits) are requested
+        // only once this k-step's MFMAs have read theirs, so one set of
+        // activation registers serves both: at three packings that keeps the
+        // four-tile kernel at two waves per SIMD.
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -890,14 +902,8 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
                 const int row = 4 * ii + lrow;
                 *reinterpret_cast<u32x4_t *>(wl + j * 2048 + row * 128 + ((lch ^ row) << 3)) = wv[j][ii];
             }
-        u32x4_t xc[NP][4];
-#pragma unroll
-        for (int p = 0; p < NP; ++p)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                xc[p][i] = xv[p][i];
         if (q + NW < ks1)
-            load(q + NW);
+            load_w(q + NW);
         // the staging tile is private to this wave, whose LDS accesses run in
         // program order; the fences only keep the compiler from reordering them
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -910,11 +916,14 @@ __global__ __launch_bounds__(NW * 64) void k_linear_mfma(LinearArgs a) {
 #pragma unroll
                 for (int p = 0; p < NP; ++p)
                     acc[j][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
-                                                                        __builtin_bit_cast(bf16x8_t, xc[p][i]),
+                                                                        __builtin_bit_cast(bf16x8_t, xv[p][i]),
                                                                         acc[j][p], 0, 0, 0);
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        __builtin_amdgcn_sched_barrier(0);
+        if (q + NW < ks1)
+            load_x(q + NW);
     }
 
     // D[n_local][c]: lane l holds rows 4 (l / 16) + v, column l % 16.  The
