@@ -282,12 +282,14 @@ __global__ __launch_bounds__(AW * 64) void k_attn_split(AttnArgs a) {
 // Outputs O^T[e][q] = sum_key V[key][e] P[q][key] are 16x16x32 MFMAs with
 // P (split into three bf16 terms likewise) as the B operand and V^T as the A
 // operand: the wave's 32 V rows are stored to a wave-private LDS tile with
-// coalesced 16-byte loads and read back transposed, 2 bytes a lane, from rows
-// padded by 32 bytes so the four lane groups hit disjoint banks.  The softmax
+// coalesced 16-byte loads and read back transposed (ds_read_b64_tr_b16, two
+// reads per output tile), from rows padded by 32 bytes.  The softmax
 // of a wave's 32 keys needs one cross-lane max and sum (lanes 16 apart); the
 // four waves merge in LDS in wave order and the chunk leaves one partial per
 // (query, split) for the ordered combine.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int MW = 4;                  // waves per work-group
 constexpr int MKW = ATTN_CHUNK / MW;   // keys per wave
@@ -333,7 +335,8 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
     constexpr int OP = 17;                 // LDS pitch of the merged output, floats per e
     constexpr int WB_V = MKW * VP * 2, WB_O = DH * OP * 4;
     constexpr int WS = (WB_V > WB_O ? WB_V : WB_O) / 4;  // words of one wave's LDS tile
-    __shared__ uint32_t tile[MW][WS];
+    static_assert(WS % 2 == 0 && (VP * 2) % 8 == 0, "8-byte aligned rows for the transposed reads");
+    __shared__ __attribute__((aligned(16))) uint32_t tile[MW][WS];
     __shared__ float2 red_ml[MW][16];
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -443,11 +446,21 @@ __global__ __launch_bounds__(MW * 64) void k_attn_mfma(AttnArgs a) {
     f32x4_t oacc[ET];
 #pragma unroll
     for (int et = 0; et < ET; ++et) {
-        uint16_t h[8];
+        // A operand V^T: lane (col, grp) needs column 16 et + col of keys
+        // 16 (u >> 2) + 4 (u & 3) + grp, u = 0..7 (the score slots).
+        // ds_read_b64_tr_b16 hands lane l of each 16-lane group element l % 4
+        // of the 8 bytes that lanes l / 4 + 4 k (k = 0..3) point at, so lane
+        // r points at key 16 I + 4 (r >> 2) + grp, columns 16 et + 4 (r & 3)
+        // ..: two reads give the eight keys in order.
+        uint32_t w[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            h[u] = vs[(16 * (u >> 2) + 4 * (u & 3) + grp) * VP + 16 * et + col];
-        const u32x4_t vf = pack_bf16x8(h);
+        for (int I = 0; I < 2; ++I) {
+            const uint16_t *src = vs + (16 * I + 4 * (col >> 2) + grp) * VP + 16 * et + 4 * (col & 3);
+            const s16x4_t rv = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)src);
+            w[2 * I] = (uint32_t)(uint16_t)rv[0] | ((uint32_t)(uint16_t)rv[1] << 16);
+            w[2 * I + 1] = (uint32_t)(uint16_t)rv[2] | ((uint32_t)(uint16_t)rv[3] << 16);
+        }
+        const u32x4_t vf = {w[0], w[1], w[2], w[3]};
         oacc[et] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int i = 0; i < X_TERMS; ++i)
