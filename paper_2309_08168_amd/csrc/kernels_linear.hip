@@ -826,12 +826,13 @@ static hipError_t launch_fp8_r(const LinearArgs &a, int epi, int n_tiles, hipStr
 // rows, two up to 10, three up to 16).  The host picks NP from its bound on
 // M (LinearArgs::max_rows).
 //
-// The launch bound asks for two waves per SIMD.  With one set of activation
+// The launch bound asks for two waves per SIMD up to four tiles (eight do
+// not fit twice in LDS or in the registers).  With one set of activation
 // registers (below) the four-tile kernel at three packings fits that in 218
 // registers without spilling; double-buffered activations took 260 (one
 // wave per SIMD), and 13B verification at 13-16 rows was 2% slower.
 template <int EPI, int TN, int NW, int NP>
-__global__ __launch_bounds__(NW * 64, 2) void k_linear_mfma(LinearArgs a) {
+__global__ __launch_bounds__(NW * 64, TN <= 4 ? 2 : 1) void k_linear_mfma(LinearArgs a) {
     constexpr int WL = TN * 16 * 128;                // bf16 staging per wave
     constexpr int RC = NP * 16 + 1;                  // reduction row length
     constexpr size_t SMEM_W = (size_t)NW * WL * 2, SMEM_R = (size_t)NW * TN * 16 * RC * 4;
